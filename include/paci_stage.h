@@ -1,0 +1,237 @@
+/*
+ * paci_stage.h -- C ABI of one PACI pipeline stage on an MI355X (gfx950).
+ *
+ * PACI (arXiv 2606.07881) runs asynchronous 1F1B pipeline training in which a
+ * stage accumulates the gradients of K local backwards before each optimizer
+ * update. This bounds how many parameter versions a micro-batch's backward can
+ * be behind its forward (Eq. 2: Delta <= ceil((N - i) / a)). This library is
+ * the per-stage hot path. For each micro-batch it runs the forward and the
+ * backward of a stack of pre-LN GPT blocks. It accumulates the local gradient
+ * into an fp32 buffer G and applies AdamW with G every K backwards. A stage
+ * at pipeline position p has delay = N - 1 - p micro-batches in flight
+ * (the paper's N - i).
+ *
+ * Notation: the paper's accumulation factor a is K here, and its downstream
+ * depth N - i (one-indexed stage i) is `delay`.
+ *
+ * Conventions for every call
+ *   - Every call returns an int status: PACI_OK (0), PACI_STEP_DUE (1) or a
+ *     negative PACI_E_* code. On a negative status the handle's counters and
+ *     buffers are unchanged (checks run before any device work is enqueued),
+ *     except for PACI_E_HIP, which leaves the handle unusable.
+ *   - Device work is enqueued on the HIP stream given to paci_stage_init and
+ *     is asynchronous to the host. Versions, counters and stamps are host
+ *     integers, so they are final when the call returns; device buffers are
+ *     final only after the stream is synchronized (paci_stage_sync).
+ *   - A handle is single-threaded: calls on one handle must not overlap.
+ *   - Pointers named `dev_*` or documented as device buffers are device
+ *     memory on the stage's GPU; the caller owns them and keeps them alive
+ *     until the stream has consumed them.
+ *   - Activations use the stage dtype (fp32 or bf16), row-major [T, d_model]
+ *     with T = micro_batch * seq tokens, token t = b * seq + s.
+ */
+#ifndef PACI_STAGE_H
+#define PACI_STAGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes -------------------------------------------------------- */
+#define PACI_OK 0
+#define PACI_STEP_DUE 1          /* backward completed the K-th micro-batch of a window */
+#define PACI_E_INVAL (-1)        /* bad argument (null pointer, size, shape relation) */
+#define PACI_E_UNSUPPORTED (-2)  /* valid but not implemented (head_dim, dtype) */
+#define PACI_E_NOMEM (-3)        /* arena smaller than paci_stage_arena_bytes */
+#define PACI_E_ORDER (-4)        /* micro-batch out of FIFO order */
+#define PACI_E_BACKPRESSURE (-5) /* forward refused: q > delay (admission rule) */
+#define PACI_E_STEP_PENDING (-6) /* forward/backward while an update is due */
+#define PACI_E_NOT_DUE (-7)      /* step before K backwards of the window */
+#define PACI_E_HIP (-8)          /* a HIP runtime call failed; see paci_last_hip_error */
+
+/* ---- stage description ---------------------------------------------------- */
+enum paci_kind { PACI_MIDDLE = 0, PACI_FIRST = 1, PACI_LAST = 2 };
+enum paci_dtype { PACI_FP32 = 0, PACI_BF16 = 1 };
+
+typedef struct paci_shapes {
+  int32_t n_layers;     /* pre-LN decoder blocks in this stage (>= 1) */
+  int32_t d_model;      /* d = n_heads * head_dim */
+  int32_t n_heads;
+  int32_t head_dim;     /* 32, 64 or 128 */
+  int32_t d_ff;         /* FFN width f, multiple of 32 */
+  int32_t seq;          /* S, tokens per sequence, <= max_pos for PACI_FIRST */
+  int32_t micro_batch;  /* mu, sequences per micro-batch */
+  int32_t vocab;        /* V (PACI_FIRST / PACI_LAST only) */
+  int32_t max_pos;      /* rows of the position table (PACI_FIRST only) */
+  int32_t kind;         /* enum paci_kind */
+  int32_t dtype;        /* enum paci_dtype: arithmetic type of the activations */
+  float lr, beta1, beta2, eps, weight_decay; /* AdamW hyper-parameters */
+  float ln_eps;         /* LayerNorm epsilon */
+} paci_shapes;
+
+typedef struct paci_counters {
+  int32_t version;      /* t: local optimizer updates applied so far */
+  int32_t c;            /* backwards in the current accumulation window */
+  int32_t q;            /* forwards whose backward has not yet run */
+  int32_t next_f;       /* micro-batch index the next forward must carry */
+  int32_t next_b;       /* micro-batch index the next backward must carry */
+  int32_t K, delay;
+} paci_counters;
+
+/* Description of one parameter tensor in the canonical order. */
+typedef struct paci_param_info {
+  char name[32];        /* e.g. "h3.w_qkv", "wte", "lnf_g" */
+  int32_t rows, cols;   /* matrices: [rows, cols] = [out, in]; vectors: [rows, 1] */
+  int64_t offset;       /* element offset in the flat canonical vector */
+  int64_t numel;
+  int32_t decay;        /* 1 if AdamW weight decay applies */
+} paci_param_info;
+
+typedef struct paci_stage paci_stage; /* opaque handle */
+typedef struct paci_fsm paci_fsm;     /* opaque host-only protocol object */
+
+/* ---- host-only protocol (Alg. 1 counters) --------------------------------
+ * The event rule of one stage (Alg. 1, appendix "Stage-level execution rule"),
+ * with no device work. A forward of micro-batch mb is admitted only if
+ * mb == next_f, no update is due and q <= delay (Sec. 3.2, admission rule
+ * q_i < N + 1 - i); it returns the version t it ran at (t^F) and increments q.
+ * A backward must carry mb == next_b < next_f (FIFO, 1F1B); it returns t^B,
+ * increments c, decrements q and returns PACI_STEP_DUE when c == K. A step is
+ * legal only when c == K; it resets c and increments t. paci_stage_* use this
+ * same object, so the stage and its protocol cannot disagree. */
+int paci_fsm_create(int K, int delay, paci_fsm** out);      /* E_INVAL: K < 1, delay < 0 */
+int paci_fsm_forward(paci_fsm* f, int mb, int* version);   /* E_ORDER, E_BACKPRESSURE, E_STEP_PENDING */
+int paci_fsm_backward(paci_fsm* f, int mb, int* version);  /* E_ORDER, E_STEP_PENDING; may return STEP_DUE */
+int paci_fsm_step(paci_fsm* f, int* new_version);          /* E_NOT_DUE */
+int paci_fsm_counters(const paci_fsm* f, paci_counters* out);
+int paci_fsm_destroy(paci_fsm* f);
+
+/* Canonical asynchronous 1F1B order of one stage (Alg. 1 with every forward
+ * issued as soon as it is admitted and every update right after the backward
+ * that completes its window): F_0 .. F_min(delay, M-1); then for j = 0..M-1:
+ * B_j, S if (j+1) % K == 0, F_{j+delay+1} if j+delay+1 < M.
+ * kinds[e] is 0 (forward), 1 (backward) or 2 (step); idx[e] is the micro-batch
+ * (-1 for a step). Host arrays of capacity `cap`; *n receives the event count
+ * (2M + floor(M/K)). E_INVAL if M < 0, K < 1, delay < 0 or cap is too small
+ * (then *n still receives the required count). */
+int paci_schedule(int M, int K, int delay, int32_t* kinds, int32_t* idx, int cap, int* n);
+
+/* ---- parameter layout (host only) ------------------------------------------
+ * The canonical order: first stage prefix wte [V, d], wpe [max_pos, d]; per
+ * block l: h{l}.ln1_g, ln1_b, w_qkv [3d, d], b_qkv, w_o [d, d], b_o, ln2_g,
+ * ln2_b, w_1 [f, d], b_1, w_2 [d, f], b_2; last stage suffix lnf_g, lnf_b,
+ * w_lm [V, d]. The flat canonical vector is the concatenation in this order
+ * with no padding. Weight decay applies to the w_* matrices only (appendix
+ * "Detailed experimental setup": no decay on biases, LayerNorm parameters or
+ * embeddings). */
+int paci_param_count(const paci_shapes* s, int* n_tensors, int64_t* n_elements);
+int paci_param_info_at(const paci_shapes* s, int index, paci_param_info* out); /* E_INVAL: bad index */
+
+/* ---- stage lifetime --------------------------------------------------------- */
+/* Bytes of device memory the stage needs: fp32 parameters, G, AdamW moments,
+ * the bf16 working copy (bf16 stages), an activation store of delay + 1
+ * micro-batch slots and the backward workspace. E_INVAL / E_UNSUPPORTED as for
+ * paci_stage_init. */
+int paci_stage_arena_bytes(const paci_shapes* s, int K, int delay, size_t* bytes);
+
+/* stage_init(shapes, K, delay). `dev_arena` is caller-owned device memory of
+ * at least paci_stage_arena_bytes bytes, 256-byte aligned, that must outlive
+ * the handle; `hip_stream` is the hipStream_t all work is enqueued on (NULL =
+ * the null stream). Parameters start at zero and G, m, v are cleared; load the
+ * initial parameters with paci_stage_load. Counters start at t = c = q = 0.
+ * Errors: E_INVAL (null pointer, d != n_heads * head_dim, K < 1, delay < 0,
+ * seq > max_pos on a first stage, non-positive size), E_UNSUPPORTED (head_dim
+ * not 32/64/128, d_ff or d not multiples of 32, unknown kind or dtype),
+ * E_NOMEM (arena too small), E_HIP. */
+int paci_stage_init(const paci_shapes* s, int K, int delay, void* dev_arena, size_t arena_bytes,
+                    void* hip_stream, paci_stage** out);
+int paci_stage_destroy(paci_stage* h); /* frees host state only; the arena stays the caller's */
+
+/* ---- state transfer --------------------------------------------------------- */
+enum paci_what { PACI_PARAMS = 0, PACI_GRADS = 1, PACI_EXP_AVG = 2, PACI_EXP_AVG_SQ = 3 };
+/* Copy n fp32 values in the canonical order into / out of the stage. n must
+ * equal the stage's element count (paci_param_count). `src`/`dst` are device
+ * pointers if `on_device` is non-zero, else host pointers (the call then
+ * synchronizes the stream). Loading PARAMS also rewrites the bf16 working copy.
+ * E_INVAL on a wrong count or null pointer. */
+int paci_stage_load(paci_stage* h, int what, const float* src, int64_t n, int on_device);
+int paci_stage_read(paci_stage* h, int what, float* dst, int64_t n, int on_device);
+
+/* ---- the three events of Alg. 1 ----------------------------------------------- */
+/* stage_forward(mb, &version): F_i of micro-batch mb at the current parameters.
+ * Middle/last stage: `dev_in` is the stage input [T, d] (stage dtype). First
+ * stage: `dev_in` is int32 token ids [micro_batch, seq] in [0, vocab).
+ * Middle/first stage: `dev_out` receives [T, d] (stage dtype). Last stage:
+ * `dev_targets` are int32 [micro_batch, seq] in [0, vocab) and `dev_out`
+ * receives one fp32, the mean cross-entropy over the T tokens.
+ * The input is copied into the activation store (slot mb % (delay + 1)), so the
+ * caller may reuse `dev_in` once the stream has passed this call. *version
+ * receives t^F; q is incremented.
+ * Errors (state unchanged): E_ORDER (mb != next_f), E_BACKPRESSURE (q > delay),
+ * E_STEP_PENDING (an update is due), E_INVAL (null pointer). */
+int paci_stage_forward(paci_stage* h, int mb, const void* dev_in, const int32_t* dev_targets,
+                       void* dev_out, int* version);
+
+/* stage_backward(mb, grad_out): B_i of micro-batch mb. It differentiates the
+ * activations stored by F_mb at the parameters current now (Eq. 1: a stale
+ * backward reads the newest version, with no weight stash), adds the local
+ * gradient to the fp32 accumulator G, and writes the input gradient.
+ * Middle/first stage: `dev_grad_out` is dL/d(out) [T, d] (stage dtype). Last
+ * stage: `dev_grad_out` must be NULL; the backward is seeded with
+ * (softmax(z) - onehot(target)) / (T * K). `dev_grad_in` receives dL/d(in)
+ * [T, d] (NULL to discard; always NULL for a first stage).
+ * *version receives t^B; c is incremented, q decremented. Returns PACI_STEP_DUE
+ * when this backward completes the window (c == K): paci_stage_step must run
+ * before the next forward or backward.
+ * Errors (state unchanged): E_ORDER (mb != next_b or no forward pending),
+ * E_STEP_PENDING, E_INVAL. */
+int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_out, void* dev_grad_in,
+                        int* version);
+
+/* stage_step(): one AdamW update with G (the plain sum of the window's K local
+ * gradients, Alg. 1), local step count t + 1 for bias correction, decoupled
+ * weight decay on the w_* matrices; then G <- 0, c <- 0, t <- t + 1 and the bf16
+ * working copy is rewritten. *new_version receives t. E_NOT_DUE if c != K. */
+int paci_stage_step(paci_stage* h, int* new_version);
+
+/* ---- schedule driver --------------------------------------------------------- */
+/* Replays paci_schedule(M, K, delay) on the handle by calling forward,
+ * backward and step. Micro-batch i reads dev_in_all + i * (input bytes) (ids
+ * for a first stage), dev_targets_all + i * T (last stage), dev_grad_out_all
+ * + i * (T * d elements) (middle/first), and writes dev_out_all + i * (output
+ * bytes) and dev_grad_in_all + i * (T * d elements); either output may be NULL
+ * to discard. host_stamps (host int32 [M][3], may be NULL) receives
+ * (t^F, t^B, Delta) per micro-batch. The handle must be fresh for the replay
+ * (next_f == next_b == 0, c == 0); the first error is returned. */
+int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, const int32_t* dev_targets_all,
+                   const void* dev_grad_out_all, void* dev_out_all, void* dev_grad_in_all,
+                   int32_t* host_stamps);
+
+/* Rewinds the counters to t = c = q = 0, next_f = next_b = 0, keeping
+ * parameters and moments (used to replay again from the current state). */
+int paci_stage_reset_counters(paci_stage* h);
+
+/* ---- introspection ------------------------------------------------------------- */
+int paci_stage_counters(const paci_stage* h, paci_counters* out);
+int paci_stage_sync(paci_stage* h);              /* hipStreamSynchronize; E_HIP on failure */
+int paci_last_hip_error(const paci_stage* h);    /* the hipError_t behind the last E_HIP */
+const char* paci_strerror(int status);
+
+/* Kernel timing: while enabled, each kernel launch of the stage is bracketed by
+ * HIP events on the stage stream. paci_stage_kernel_times (after a sync) reports,
+ * per kernel family, the number of launches, the summed device time in
+ * milliseconds and the summed algorithmic work (FLOP for matrix kernels, bytes
+ * for streaming kernels) since timing was enabled. Families are numbered
+ * 0 .. paci_kernel_family_count() - 1 and named by paci_kernel_family_name. */
+int paci_kernel_family_count(void);
+const char* paci_kernel_family_name(int family);
+int paci_stage_set_timing(paci_stage* h, int enable);
+int paci_stage_kernel_times(paci_stage* h, int family, int64_t* launches, double* ms, double* work);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PACI_STAGE_H */

@@ -1,0 +1,231 @@
+"""One PACI stage and the replay of its event list, float64 (test infrastructure).
+
+A stage holds a single parameter copy theta, a gradient accumulator G, the AdamW
+moments and the counters of Alg. 1 (appendix "Stage-level execution rule").
+Forward F_m stores the activations its backward needs; backward B_m computes
+the local gradient and the input gradient, adds the local gradient to G, and
+after every K-th backward the stage applies one AdamW update with G and clears
+G (Alg. 1, accumulate / update / reset). There is no weight stash
+(appendix "Memory and synchronization properties").
+
+Drift semantics (Eq. (1), Sec. 3.1, and the appendix "PyTorch modifications"):
+a backward differentiates the activations saved by its own forward, while every
+parameter it reads is the version current when it runs. Activations that depend
+on parameters are therefore saved at forward time, never recomputed.
+
+Parameter naming and order (nn.Linear weights are [out, in]):
+  first stage prefix  wte [V, d], wpe [max_pos, d]
+  block l             h{l}.ln1_g, h{l}.ln1_b, h{l}.w_qkv [3d, d], h{l}.b_qkv,
+                      h{l}.w_o [d, d], h{l}.b_o, h{l}.ln2_g, h{l}.ln2_b,
+                      h{l}.w_1 [f, d], h{l}.b_1, h{l}.w_2 [d, f], h{l}.b_2
+  last stage suffix   lnf_g, lnf_b, w_lm [V, d]
+Weight decay applies to the w_* matrices only (no decay on biases, LayerNorm
+parameters or embeddings, appendix "Detailed experimental setup").
+"""
+import numpy as np
+
+from . import adamw, model
+from .schedule import StageCounters, canonical_events
+
+BLOCK_PARAMS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
+                "ln2_g", "ln2_b", "w_1", "b_1", "w_2", "b_2")
+
+
+def param_shapes(cfg):
+    """Ordered (name, shape) list of a stage's parameters."""
+    d, f, V, P = cfg["d_model"], cfg["d_ff"], cfg.get("vocab", 0), cfg.get("max_pos", 0)
+    out = []
+    if cfg["kind"] == "first":
+        out += [("wte", (V, d)), ("wpe", (P, d))]
+    per = {"ln1_g": (d,), "ln1_b": (d,), "w_qkv": (3 * d, d), "b_qkv": (3 * d,),
+           "w_o": (d, d), "b_o": (d,), "ln2_g": (d,), "ln2_b": (d,),
+           "w_1": (f, d), "b_1": (f,), "w_2": (d, f), "b_2": (d,)}
+    for l in range(cfg["n_layers"]):
+        out += [(f"h{l}.{n}", per[n]) for n in BLOCK_PARAMS]
+    if cfg["kind"] == "last":
+        out += [("lnf_g", (d,)), ("lnf_b", (d,)), ("w_lm", (V, d))]
+    return out
+
+
+def decayed(name):
+    return name.split(".")[-1].startswith("w_")
+
+
+def stage_fwd(cfg, theta, inp, targets=None):
+    """F_i at parameters ``theta``. Returns (output, saved).
+
+    middle: inp is x [T, d], output y [T, d]; first: inp is ids [mu, S];
+    last: output is the mean cross-entropy of the micro-batch.
+    """
+    if cfg["kind"] == "first":
+        x = model.embed_fwd(inp, theta["wte"], theta["wpe"])
+    else:
+        x = inp
+    saved = {"blocks": []}
+    for l in range(cfg["n_layers"]):
+        p = {n: theta[f"h{l}.{n}"] for n in BLOCK_PARAMS}
+        x, s = model.block_fwd(x, p, cfg)
+        saved["blocks"].append(s)
+    if cfg["kind"] == "last":
+        loss, saved["head"] = model.head_fwd(x, targets, theta["lnf_g"], theta["lnf_b"],
+                                             theta["w_lm"], cfg["ln_eps"])
+        return loss, saved
+    return x, saved
+
+
+def stage_bwd(cfg, theta, saved, grad_out, K, ids=None):
+    """Backward of stage_fwd from ``saved`` at parameters ``theta``.
+
+    Returns (grad_in, grads). For the last stage the seed is
+    (softmax(z) - onehot(target)) / (T * K): the micro-batch loss is a mean over
+    its T tokens and K micro-batches make one update. grad_in is None for the
+    first stage (its input is token ids).
+    """
+    g = {}
+    if cfg["kind"] == "last":
+        T = cfg["micro_batch"] * cfg["seq"]
+        dy, g["lnf_g"], g["lnf_b"], g["w_lm"] = model.head_bwd(
+            saved["head"], theta["lnf_g"], theta["w_lm"], 1.0 / (T * K))
+    else:
+        dy = grad_out
+    for l in reversed(range(cfg["n_layers"])):
+        p = {n: theta[f"h{l}.{n}"] for n in BLOCK_PARAMS}
+        dy, gl = model.block_bwd(dy, saved["blocks"][l], p, cfg)
+        for n, v in gl.items():
+            g[f"h{l}.{n}"] = v
+    if cfg["kind"] == "first":
+        g["wte"], g["wpe"] = model.embed_bwd(dy, ids, cfg["vocab"], cfg["max_pos"])
+        return None, g
+    return dy, g
+
+
+class Stage:
+    """Alg. 1 for one stage over float64 state."""
+
+    def __init__(self, cfg, params, K, delay):
+        self.cfg, self.K, self.delay = cfg, K, delay
+        self.names = [n for n, _ in param_shapes(cfg)]
+        self.theta = {n: np.array(params[n], dtype=np.float64) for n in self.names}
+        self.G = {n: np.zeros_like(self.theta[n]) for n in self.names}
+        self.m = {n: np.zeros_like(self.theta[n]) for n in self.names}
+        self.v = {n: np.zeros_like(self.theta[n]) for n in self.names}
+        self.counters = StageCounters(K, delay)
+        self.saved = {}
+        self.ids = {}
+
+    @property
+    def version(self):
+        return self.counters.t
+
+    def forward(self, mb, inp, targets=None):
+        """F_mb: returns (output, t^F). Stores the activations until B_mb."""
+        version = self.counters.forward(mb)
+        out, self.saved[mb] = stage_fwd(self.cfg, self.theta, inp, targets)
+        if self.cfg["kind"] == "first":
+            self.ids[mb] = inp
+        return out, version
+
+    def backward(self, mb, grad_out=None):
+        """B_mb at the current parameters: returns (grad_in, t^B, update_due)."""
+        version = self.counters.backward(mb)
+        grad_in, g = stage_bwd(self.cfg, self.theta, self.saved.pop(mb), grad_out, self.K,
+                               ids=self.ids.pop(mb, None))
+        for n, v in g.items():
+            self.G[n] += v
+        return grad_in, version, self.counters.step_due
+
+    def step(self):
+        """AdamW with the accumulated G, then G <- 0; returns the new version."""
+        c = self.cfg
+        t_adam = self.counters.t + 1
+        for n in self.names:
+            wd = c["weight_decay"] if decayed(n) else 0.0
+            self.theta[n], self.m[n], self.v[n] = adamw.adamw_update(
+                self.theta[n], self.G[n], self.m[n], self.v[n], t_adam,
+                c["lr"], c["beta1"], c["beta2"], c["eps"], wd)
+            self.G[n] = np.zeros_like(self.G[n])
+        return self.counters.step()
+
+
+def _copy(d):
+    return {k: v.copy() for k, v in d.items()}
+
+
+def replay(cfg, params, K, delay, inputs, grad_outs=None, targets=None, events=None):
+    """Run ``events`` (default: the canonical asynchronous 1F1B order) on a Stage.
+
+    inputs[i] is micro-batch i's stage input, grad_outs[i] its output gradient
+    (middle and first stages) and targets[i] its token targets (last stage).
+    Returns a dict with per-micro-batch outputs, input gradients and stamps,
+    and per update the G it consumed and theta, m, v after it.
+    """
+    M = len(inputs)
+    if events is None:
+        events = canonical_events(M, K, delay)
+    st = Stage(cfg, params, K, delay)
+    rec = dict(out=[None] * M, grad_in=[None] * M, tF=[None] * M, tB=[None] * M,
+               G=[], theta=[], m=[], v=[], events=list(events))
+    for kind, i in events:
+        if kind == "F":
+            tgt = targets[i] if targets is not None else None
+            rec["out"][i], rec["tF"][i] = st.forward(i, inputs[i], tgt)
+        elif kind == "B":
+            go = grad_outs[i] if grad_outs is not None else None
+            rec["grad_in"][i], rec["tB"][i], _ = st.backward(i, go)
+        else:
+            rec["G"].append(_copy(st.G))
+            st.step()
+            rec["theta"].append(_copy(st.theta))
+            rec["m"].append(_copy(st.m))
+            rec["v"].append(_copy(st.v))
+    rec["delta"] = [b - f for f, b in zip(rec["tF"], rec["tB"])]
+    rec["final_version"] = st.version
+    rec["stage"] = st
+    return rec
+
+
+def replay_with_version_store(cfg, params, K, delay, inputs, grad_outs=None, targets=None,
+                              backward_at="current"):
+    """The same trajectory computed a second way, for cross-checking ``replay``.
+
+    Keeps every parameter version theta^(0), theta^(1), ... and no activation
+    store. At B_i it re-runs the forward of micro-batch i at theta^(t^F(i)) to
+    obtain the activations, then differentiates at theta^(t^B(i))
+    (``backward_at="current"``, Eq. (1)) or at theta^(t^F(i))
+    (``backward_at="forward"``, weight stashing; not PACI, used to show that
+    the drift is exercised). Versions are counted from the event list itself.
+    """
+    M = len(inputs)
+    events = canonical_events(M, K, delay)
+    names = [n for n, _ in param_shapes(cfg)]
+    versions = [{n: np.array(params[n], dtype=np.float64) for n in names}]
+    G = {n: np.zeros_like(versions[0][n]) for n in names}
+    m = {n: np.zeros_like(versions[0][n]) for n in names}
+    v = {n: np.zeros_like(versions[0][n]) for n in names}
+    tF, out, grad_in, thetas = {}, [None] * M, [None] * M, []
+    for kind, i in events:
+        t = len(versions) - 1
+        if kind == "F":
+            tF[i] = t
+            tgt = targets[i] if targets is not None else None
+            out[i], _ = stage_fwd(cfg, versions[t], inputs[i], tgt)
+        elif kind == "B":
+            tgt = targets[i] if targets is not None else None
+            _, saved = stage_fwd(cfg, versions[tF[i]], inputs[i], tgt)
+            at = versions[t] if backward_at == "current" else versions[tF[i]]
+            go = grad_outs[i] if grad_outs is not None else None
+            ids = inputs[i] if cfg["kind"] == "first" else None
+            grad_in[i], g = stage_bwd(cfg, at, saved, go, K, ids=ids)
+            for n in names:
+                G[n] = G[n] + g[n]
+        else:
+            new = {}
+            for n in names:
+                wd = cfg["weight_decay"] if decayed(n) else 0.0
+                new[n], m[n], v[n] = adamw.adamw_update(
+                    versions[t][n], G[n], m[n], v[n], t + 1,
+                    cfg["lr"], cfg["beta1"], cfg["beta2"], cfg["eps"], wd)
+                G[n] = np.zeros_like(G[n])
+            versions.append(new)
+            thetas.append(new)
+    return dict(out=out, grad_in=grad_in, theta=thetas)
