@@ -1,0 +1,217 @@
+// Device-side building blocks shared by the stage kernels (gfx950 / CDNA4).
+//
+// Matrix-core convention used everywhere
+// --------------------------------------
+// One MFMA "step" contracts 4 * V elements, where V = 16 bytes / sizeof(T)
+// (8 for bf16, 4 for fp32). In a step, lane l of a 64-wide wavefront supplies
+// one 16-byte vector per operand: row (l % 16) of a 16-row operand tile, and
+// the V contracted elements of group g = l / 16. bf16 uses one
+// v_mfma_f32_16x16x32_bf16 per step. fp32 uses four v_mfma_f32_16x16x4_f32,
+// the j-th taking element j of each lane's vector. Both operands use the same
+// lane -> contracted-index assignment, so any consistent permutation of the
+// contracted index inside a step gives the same sum.
+//
+// mma_step(acc, X, Y) accumulates D += X Y^T for two 16-row tiles X and Y. Lane
+// l then holds D[4 * (l / 16) + r][l % 16], r = 0..3: four consecutive X-rows
+// of one Y-row.
+//
+// LDS tile layout: a tile of R rows by 8 vectors (8 * V contracted elements)
+// is stored as [kv][row], one 16-byte slot each. The row is XOR-swizzled with
+// the vector index (physical row = row ^ (kv & 7)). This keeps conflict-free
+// 16-byte accesses for the three patterns the kernels use: 8 lanes writing
+// one row's 8 vectors, 8 lanes writing 8 vectors of a transposed 8x8 block,
+// and 16 lanes reading 16 consecutive rows of one vector index.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace paci {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
+typedef float floatx4 __attribute__((__vector_size__(4 * sizeof(float))));
+typedef uint32_t u32x4 __attribute__((__vector_size__(4 * sizeof(uint32_t))));
+typedef uint32_t u32x2 __attribute__((__vector_size__(2 * sizeof(uint32_t))));
+
+template <typename T> struct Vec { static constexpr int V = 16 / sizeof(T); };
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
+
+// ---- element access inside a raw 16-byte vector -----------------------------------
+template <typename T> __device__ __forceinline__ float vget(const u32x4& v, int j);
+template <> __device__ __forceinline__ float vget<float>(const u32x4& v, int j) {
+  return __builtin_bit_cast(float, v[j]);
+}
+template <> __device__ __forceinline__ float vget<bf16>(const u32x4& v, int j) {
+  uint32_t w = v[j >> 1];
+  return __builtin_bit_cast(float, (j & 1) ? (w & 0xffff0000u) : (w << 16));
+}
+
+// Zero the elements j >= n of a vector (n in [0, V]).
+template <typename T> __device__ __forceinline__ u32x4 vmask_tail(u32x4 v, int n) {
+  constexpr int V = Vec<T>::V;
+  if (n >= V) return v;
+  if (sizeof(T) == 4) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (j >= n) v[j] = 0;
+  } else {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if (2 * w >= n) v[w] = 0;
+      else if (2 * w + 1 >= n) v[w] &= 0xffffu;
+    }
+  }
+  return v;
+}
+
+// Transpose a V x V block held as V row vectors: out[i] gathers element i of
+// every input row, in row order.
+template <typename T> __device__ __forceinline__ void transpose_block(const u32x4* in, u32x4* out);
+template <> __device__ __forceinline__ void transpose_block<float>(const u32x4* in, u32x4* out) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) out[i][j] = in[j][i];
+}
+template <> __device__ __forceinline__ void transpose_block<bf16>(const u32x4* in, u32x4* out) {
+  // out[i] word p = (element i of row 2p) | (element i of row 2p+1) << 16
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      uint32_t a = in[2 * p][i >> 1], b = in[2 * p + 1][i >> 1];
+      out[i][p] = (i & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
+    }
+  }
+}
+
+// ---- MFMA step ---------------------------------------------------------------------
+template <typename T> __device__ __forceinline__ void mma_step(floatx4& acc, const u32x4& x, const u32x4& y);
+template <> __device__ __forceinline__ void mma_step<bf16>(floatx4& acc, const u32x4& x, const u32x4& y) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, x), __builtin_bit_cast(bf16x8, y),
+                                                acc, 0, 0, 0);
+}
+template <> __device__ __forceinline__ void mma_step<float>(floatx4& acc, const u32x4& x, const u32x4& y) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, x[j]), __builtin_bit_cast(float, y[j]),
+                                               acc, 0, 0, 0);
+}
+
+// ---- swizzled LDS tile addressing ------------------------------------------------------
+template <int ROWS> __device__ __forceinline__ int lds_slot(int kv, int row) {
+  return kv * ROWS + (row ^ (kv & 7));
+}
+
+// Fragment of a 16-row operand tile for MFMA step `s` (rows row0 .. row0+15).
+template <int ROWS> __device__ __forceinline__ u32x4 lds_frag(const u32x4* tile, int s, int row0) {
+  const int l = lane_id();
+  const int kv = s * 4 + (l >> 4);
+  return tile[lds_slot<ROWS>(kv, row0 + (l & 15))];
+}
+
+// ---- wave reductions ---------------------------------------------------------------------
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+// Reduce across the four 16-lane groups (lanes l, l^16, l^32, l^48).
+__device__ __forceinline__ float group4_sum(float v) {
+  v += __shfl_xor(v, 16, 64);
+  v += __shfl_xor(v, 32, 64);
+  return v;
+}
+__device__ __forceinline__ float group4_max(float v) {
+  v = fmaxf(v, __shfl_xor(v, 16, 64));
+  v = fmaxf(v, __shfl_xor(v, 32, 64));
+  return v;
+}
+
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ void st16(void* p, const u32x4& v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+// ---- one-shot tile staging (global -> LDS), used by the attention kernels -----------------
+// K-major source: element (row r, contracted c) at src[r * ld + c]. Stages rows
+// [0, ROWS) and contracted vectors [0, KVN); rows >= rows_valid read as zero.
+template <typename T, int ROWS, int KVN, int NT>
+__device__ __forceinline__ void stage_kmajor(u32x4* tile, const T* src, int ld, int rows_valid) {
+  constexpr int V = Vec<T>::V;
+  constexpr int ITEMS = ROWS * KVN;
+#pragma unroll
+  for (int it = threadIdx.x; it < ITEMS; it += NT) {
+    const int kv = it % KVN, r = it / KVN;
+    u32x4 v = {0, 0, 0, 0};
+    if (r < rows_valid) v = ld16(src + (size_t)r * ld + kv * V);
+    tile[lds_slot<ROWS>(kv, r)] = v;
+  }
+}
+
+// MN-major source: element (contracted c, row r) at src[c * ld + r]. The
+// contracted index of element j of vector kv is perm(kv, j) (a permutation of
+// 0 .. KVN*V-1 that keeps each MFMA step's 4*V indices together). Contracted
+// indices >= c_valid read as zero. Rows [0, ROWS) must be in bounds.
+template <typename T, int ROWS, int KVN, int NT, class Perm>
+__device__ __forceinline__ void stage_mnmajor(u32x4* tile, const T* src, int ld, int c_valid, Perm perm) {
+  constexpr int V = Vec<T>::V;
+  constexpr int ITEMS = (ROWS / V) * KVN;
+  for (int it = threadIdx.x; it < ITEMS; it += NT) {
+    const int kv = it % KVN, rb = it / KVN;
+    u32x4 in[V], out[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const int c = perm(kv, j);
+      in[j] = (c < c_valid) ? ld16(src + (size_t)c * ld + rb * V) : u32x4{0, 0, 0, 0};
+    }
+    transpose_block<T>(in, out);
+#pragma unroll
+    for (int i = 0; i < V; ++i) tile[lds_slot<ROWS>(kv, rb * V + i)] = out[i];
+  }
+}
+
+// Contracted-index permutations for stage_mnmajor.
+// LinearPerm: vector kv holds indices kv*V .. kv*V + V - 1.
+template <int V> struct LinearPerm {
+  __device__ __forceinline__ int operator()(int kv, int j) const { return kv * V + j; }
+};
+// StepPairPerm (bf16 only): the order in which two 16-row accumulator tiles
+// (lane group g holds rows 4g..4g+3 of each) become one 32-element MFMA step:
+// vector kv = 4s + g holds indices 32s + 4g + {0,1,2,3} and 32s + 16 + 4g + {0,1,2,3}.
+struct StepPairPerm {
+  __device__ __forceinline__ int operator()(int kv, int j) const {
+    const int g = kv & 3;
+    return 32 * (kv >> 2) + ((j < 4) ? (4 * g + j) : (16 + 4 * g + j - 4));
+  }
+};
+
+// The operand vector of MFMA step s built from fp32 accumulator tiles whose
+// lane layout is D[4 * (l / 16) + r][l % 16]: bf16 packs tiles 2s and 2s + 1
+// (StepPairPerm order); fp32 reuses tile s as is (LinearPerm order).
+template <typename T> __device__ __forceinline__ u32x4 acc_to_frag(const floatx4* tiles, int s);
+template <> __device__ __forceinline__ u32x4 acc_to_frag<float>(const floatx4* tiles, int s) {
+  return __builtin_bit_cast(u32x4, tiles[s]);
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (bf16)lo) | ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)hi) << 16);
+}
+template <> __device__ __forceinline__ u32x4 acc_to_frag<bf16>(const floatx4* tiles, int s) {
+  const floatx4 a = tiles[2 * s], b = tiles[2 * s + 1];
+  return u32x4{pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3])};
+}
+template <typename T> struct AccPerm;
+template <> struct AccPerm<float> { typedef LinearPerm<4> type; };
+template <> struct AccPerm<bf16> { typedef StepPairPerm type; };
+
+}  // namespace paci

@@ -1,0 +1,99 @@
+// Host-side launchers of the stage kernels. Every pointer is device memory;
+// every launcher enqueues on `st` and returns the launch status.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace paci {
+
+enum DType { DT_F32 = 0, DT_BF16 = 1 };
+
+// ---- GEMM: C[m][n] = sum_k A(m, k) B(k, n) -------------------------------------------
+// Operand layouts (ld in elements):
+//   GEMM_NT (forward, y = x W^T):      A(m,k) = A[m*lda + k], B(k,n) = B[n*ldb + k]
+//   GEMM_NN (input gradient, dX = dY W): A(m,k) = A[m*lda + k], B(k,n) = B[k*ldb + n]
+//   GEMM_TN (weight gradient, dW = dY^T X): A(m,k) = A[k*lda + m], B(k,n) = B[k*ldb + n]
+enum GemmLayout { GEMM_NT = 0, GEMM_NN = 1, GEMM_TN = 2 };
+// Fused epilogues (acc is the fp32 sum for one (m, n)):
+//   EPI_STORE      C = acc
+//   EPI_BIAS       C = acc + bias[n]
+//   EPI_BIAS_RES   C = acc + bias[n] + aux[m*ld_aux + n]        (residual add)
+//   EPI_BIAS_GELU  C = u = acc + bias[n];  C2 = gelu(u)          (FFN up-projection)
+//   EPI_GELU_GRAD  C = acc * gelu'(aux[m*ld_aux + n])            (FFN down-projection dgrad)
+//   EPI_ACC        Cf32 += acc  (plain read-modify-write; one split only)
+//   EPI_ATOMIC     Cf32 += acc  (atomic add; any number of splits)
+enum GemmEpi { EPI_STORE = 0, EPI_BIAS, EPI_BIAS_RES, EPI_BIAS_GELU, EPI_GELU_GRAD, EPI_ACC, EPI_ATOMIC };
+
+struct GemmArgs {
+  const void* A; int64_t lda;
+  const void* B; int64_t ldb;
+  int M, N, K;
+  void* C; int64_t ldc;
+  const float* bias;
+  const void* aux; int64_t ld_aux;
+  void* C2;
+};
+
+// dtype: element type of A, B, aux and of C/C2 unless out_f32 (then C is float).
+// splits > 1 is only valid with EPI_ATOMIC.
+hipError_t gemm(DType dt, bool out_f32, GemmLayout lay, GemmEpi epi, const GemmArgs& a, int splits, hipStream_t st);
+// Tile edge used by gemm(); callers size split-K against it.
+int gemm_tile_m();
+int gemm_tile_n();
+int gemm_tile_k(DType dt);
+
+// ---- causal attention over the fused projection qkv [T, 3d] --------------------------
+// Forward: o [T, d]; lse2 [mu*H*S] = log2-sum-exp2 of the scaled scores in log2 units.
+hipError_t attn_fwd(DType dt, const void* qkv, void* o, float* lse2, int mu, int S, int H, int dh, hipStream_t st);
+// Backward: D = rowsum(dO * O) per (b, h, query), then dK, dV and dQ into dqkv [T, 3d].
+hipError_t attn_bwd(DType dt, const void* qkv, const void* o, const void* dO, const float* lse2, float* Dbuf,
+                    void* dqkv, int mu, int S, int H, int dh, hipStream_t st);
+
+// ---- LayerNorm -----------------------------------------------------------------------
+// n = (x - mean) * rstd * gamma + beta, per row of d; xcopy (optional) receives x.
+hipError_t layernorm_fwd(DType dt, const void* x, void* n, float* mean, float* rstd, const float* gamma,
+                         const float* beta, void* xcopy, int rows, int d, float eps, hipStream_t st);
+// dx = res + rstd * (g - mean(g) - xhat * mean(g * xhat)), g = dn * gamma (res optional);
+// Ggamma += sum_rows dn * xhat, Gbeta += sum_rows dn (through `part`, >= ln_bwd_part_floats).
+hipError_t layernorm_bwd(DType dt, const void* dn, const void* x, const float* mean, const float* rstd,
+                         const float* gamma, const void* res, void* dx, float* Ggamma, float* Gbeta,
+                         float* part, int rows, int d, hipStream_t st);
+int64_t ln_bwd_part_floats(int rows, int d);
+
+// ---- column sums accumulated into fp32 (bias gradients) ---------------------------------
+// G[c] += sum_r Y[r*ld + c], c < ncols; `part` needs colsum_part_floats floats.
+hipError_t colsum_acc(DType dt, const void* Y, int64_t ld, int rows, int ncols, float* G, float* part, hipStream_t st);
+int64_t colsum_part_floats(int rows, int ncols);
+
+// ---- first stage: token + position embedding ----------------------------------------------
+// x[b*S + s] = wte[ids[b*S + s]] + wpe[s] (fp32 tables, x in the stage dtype).
+hipError_t embed_fwd(DType dt, const int32_t* ids, const float* wte, const float* wpe, void* x, int mu, int S, int d,
+                     int V, hipStream_t st);
+// Gwte[ids[t]] += dx[t] (atomic; repeated ids add), Gwpe[s] += sum_b dx[b*S + s].
+// Ids outside [0, V) read as a zero row and receive no gradient.
+hipError_t embed_bwd(DType dt, const int32_t* ids, const void* dx, float* Gwte, float* Gwpe, int mu, int S, int d,
+                     int V, hipStream_t st);
+
+// ---- last stage: softmax cross-entropy over fp32 logits z [T, ldz] (V valid columns) --------
+// lse[t] = logsumexp(z[t, :V]); loss_out (one float) = mean_t (lse[t] - z[t, tgt[t]]).
+// `part` needs ce_part_floats(T) floats.
+hipError_t ce_fwd(const float* z, int64_t ldz, const int32_t* tgt, float* lse, float* loss_out, float* part, int T,
+                  int V, hipStream_t st);
+int64_t ce_part_floats(int T);
+// dz[t, v] = scale * (exp(z[t, v] - lse[t]) - [v == tgt[t]]) in the stage dtype; columns
+// V .. ldz-1 are written as zero.
+hipError_t ce_bwd(DType dt, const float* z, int64_t ldz, const int32_t* tgt, const float* lse, void* dz, int T, int V,
+                  float scale, hipStream_t st);
+
+// ---- AdamW over the flat parameter arena --------------------------------------------------
+// One launch over every parameter: chunks[i] = {begin, end, decay, 0} (elements;
+// begin/end multiples of 4). theta <- theta * (1 - lr * wd * decay), then the
+// bias-corrected Adam direction; m, v updated; G cleared; theta_bf16 (nullable)
+// rewritten with the new theta.
+struct AdamwArgs { float lr, beta1, beta2, eps, weight_decay, bc1, bc2; };
+hipError_t adamw(float* theta, float* G, float* m, float* v, void* theta_bf16, const int4* chunks, int nchunks,
+                 const AdamwArgs& a, hipStream_t st);
+// dst (bf16) = round-to-nearest-even(src), n elements.
+hipError_t f32_to_bf16(const float* src, void* dst, int64_t n, hipStream_t st);
+
+}  // namespace paci

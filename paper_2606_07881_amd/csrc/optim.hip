@@ -1,0 +1,71 @@
+// Fused AdamW over the flat parameter arena, and the fp32 -> bf16 refresh.
+//
+// One launch updates every parameter of the stage. Workgroup i takes chunk i
+// of a table built at init: {begin, end, decay}, with chunks never crossing
+// a tensor boundary. Each thread streams float4 vectors of theta, G, m and v
+// and writes theta, m, v, the bf16 working copy and G = 0. That is 16 B read
+// and 14 B (bf16) or 12 B (fp32 stage) written per parameter, plus the 4 B
+// G clear, with no reuse.
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace paci {
+namespace {
+
+constexpr int NT = 256;
+
+__global__ void __launch_bounds__(NT) adamw_kernel(float* __restrict__ theta, float* __restrict__ G,
+                                                    float* __restrict__ m, float* __restrict__ v, bf16* theta16,
+                                                    const int4* __restrict__ chunks, AdamwArgs a) {
+  const int4 ch = chunks[blockIdx.x];
+  const float decay = ch.z ? (1.f - a.lr * a.weight_decay) : 1.f;
+  const float step = a.lr / a.bc1;
+  const float rbc2 = 1.f / sqrtf(a.bc2);
+  for (int64_t i = (int64_t)ch.x + 4 * (int64_t)threadIdx.x; i < ch.y; i += 4 * NT) {
+    const floatx4 g = *reinterpret_cast<const floatx4*>(G + i);
+    floatx4 th = *reinterpret_cast<const floatx4*>(theta + i);
+    floatx4 mm = *reinterpret_cast<const floatx4*>(m + i);
+    floatx4 vv = *reinterpret_cast<const floatx4*>(v + i);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      mm[j] = a.beta1 * mm[j] + (1.f - a.beta1) * g[j];
+      vv[j] = a.beta2 * vv[j] + (1.f - a.beta2) * g[j] * g[j];
+      const float denom = sqrtf(vv[j]) * rbc2 + a.eps;
+      th[j] = th[j] * decay - step * mm[j] / denom;
+    }
+    *reinterpret_cast<floatx4*>(theta + i) = th;
+    *reinterpret_cast<floatx4*>(m + i) = mm;
+    *reinterpret_cast<floatx4*>(v + i) = vv;
+    *reinterpret_cast<floatx4*>(G + i) = floatx4{0.f, 0.f, 0.f, 0.f};
+    if (theta16) *reinterpret_cast<u32x2*>(theta16 + i) = u32x2{pack_bf16x2(th[0], th[1]), pack_bf16x2(th[2], th[3])};
+  }
+}
+
+__global__ void __launch_bounds__(NT) f32_to_bf16_kernel(const float* __restrict__ src, bf16* dst, int64_t n) {
+  const int64_t i = 4 * ((int64_t)blockIdx.x * NT + threadIdx.x);
+  if (i + 3 < n) {
+    const floatx4 x = *reinterpret_cast<const floatx4*>(src + i);
+    *reinterpret_cast<u32x2*>(dst + i) = u32x2{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
+  } else {
+    for (int64_t j = i; j < n; ++j) dst[j] = (bf16)src[j];
+  }
+}
+
+}  // namespace
+
+hipError_t adamw(float* theta, float* G, float* m, float* v, void* theta_bf16, const int4* chunks, int nchunks,
+                 const AdamwArgs& a, hipStream_t st) {
+  if (nchunks <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(adamw_kernel, dim3(nchunks), dim3(NT), 0, st, theta, G, m, v, reinterpret_cast<bf16*>(theta_bf16),
+                     chunks, a);
+  return hipGetLastError();
+}
+
+hipError_t f32_to_bf16(const float* src, void* dst, int64_t n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = (n + 4 * NT - 1) / (4 * NT);
+  hipLaunchKernelGGL(f32_to_bf16_kernel, dim3((unsigned)blocks), dim3(NT), 0, st, src, reinterpret_cast<bf16*>(dst), n);
+  return hipGetLastError();
+}
+
+}  // namespace paci

@@ -1,0 +1,473 @@
+// Bandwidth-bound row and column kernels: LayerNorm forward/backward and the
+// column sums that feed bias and LayerNorm-affine gradients.
+//
+// LayerNorm uses one wavefront per row. The row is held in registers as
+// 16-byte vectors (lane i owns vectors i, i + 64, ...), so each element is
+// read once. Mean and variance are two-pass in fp32 with wavefront
+// reductions. The backward also produces per-column partial sums of
+// dn * xhat and dn over the rows of its workgroup. A second small kernel
+// adds the partial rows into the fp32 gradient accumulator. The sum order is
+// fixed, so results are reproducible run to run.
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace paci {
+namespace {
+
+constexpr int NT = 256;
+constexpr int LN_ROWS_PER_BLOCK = 32;   // backward: rows per workgroup (8 per wavefront)
+constexpr int CS_ROWS_PER_BLOCK = 64;   // column sums: rows per workgroup
+
+template <typename T> __device__ __forceinline__ u32x4 pack_vec(const float* f);
+template <> __device__ __forceinline__ u32x4 pack_vec<float>(const float* f) {
+  return u32x4{__builtin_bit_cast(uint32_t, f[0]), __builtin_bit_cast(uint32_t, f[1]),
+               __builtin_bit_cast(uint32_t, f[2]), __builtin_bit_cast(uint32_t, f[3])};
+}
+template <> __device__ __forceinline__ u32x4 pack_vec<bf16>(const float* f) {
+  return u32x4{pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]), pack_bf16x2(f[4], f[5]), pack_bf16x2(f[6], f[7])};
+}
+
+// ------------------------------------------------------------------------------------------
+template <typename T, int MAXV>
+__global__ void __launch_bounds__(NT) ln_fwd_kernel(const T* __restrict__ x, T* __restrict__ n, float* mean,
+                                                     float* rstd, const float* __restrict__ gamma,
+                                                     const float* __restrict__ beta, T* xcopy, int rows, int d,
+                                                     float eps) {
+  constexpr int V = Vec<T>::V;
+  const int row = blockIdx.x * (NT / 64) + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int l = lane_id();
+  const int nv = d / V;
+  const T* xr = x + (int64_t)row * d;
+  u32x4 xv[MAXV];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int vi = l + 64 * i;
+    xv[i] = (vi < nv) ? ld16(xr + vi * V) : u32x4{0, 0, 0, 0};
+#pragma unroll
+    for (int j = 0; j < V; ++j) s += vget<T>(xv[i], j);
+  }
+  const float mu = wave_sum(s) / d;
+  float s2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    if (l + 64 * i < nv) {
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const float c = vget<T>(xv[i], j) - mu;
+        s2 += c * c;
+      }
+    }
+  }
+  const float rs = rsqrtf(wave_sum(s2) / d + eps);
+  T* nr = n + (int64_t)row * d;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int vi = l + 64 * i;
+    if (vi < nv) {
+      float o[V];
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const int c = vi * V + j;
+        o[j] = (vget<T>(xv[i], j) - mu) * rs * gamma[c] + beta[c];
+      }
+      st16(nr + vi * V, pack_vec<T>(o));
+      if (xcopy) st16(xcopy + (int64_t)row * d + vi * V, xv[i]);
+    }
+  }
+  if (l == 0) {
+    mean[row] = mu;
+    rstd[row] = rs;
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Each wavefront handles rows w, w+4, ... of the block's LN_ROWS_PER_BLOCK rows;
+// partial column sums of the 4 wavefronts are combined through LDS and the
+// block writes one partial row of dgamma and one of dbeta.
+template <typename T, int MAXV>
+__global__ void __launch_bounds__(NT) ln_bwd_kernel(const T* __restrict__ dn, const T* __restrict__ x,
+                                                     const float* __restrict__ mean, const float* __restrict__ rstd,
+                                                     const float* __restrict__ gamma, const T* res, T* dx,
+                                                     float* part_g, float* part_b, int rows, int d) {
+  constexpr int V = Vec<T>::V;
+  __shared__ float red[2][NT / 64][64 * V];
+  const int w = threadIdx.x >> 6, l = lane_id();
+  const int nv = d / V;
+  float pg[MAXV][V], pb[MAXV][V];
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i)
+#pragma unroll
+    for (int j = 0; j < V; ++j) pg[i][j] = pb[i][j] = 0.f;
+
+  const int r0 = blockIdx.x * LN_ROWS_PER_BLOCK;
+  for (int rr = w; rr < LN_ROWS_PER_BLOCK; rr += NT / 64) {
+    const int row = r0 + rr;
+    if (row >= rows) break;
+    const float mu = mean[row], rs = rstd[row];
+    const T* dnr = dn + (int64_t)row * d;
+    const T* xr = x + (int64_t)row * d;
+    u32x4 gv[MAXV], xv[MAXV];
+    float sg = 0.f, sgx = 0.f;
+#pragma unroll
+    for (int i = 0; i < MAXV; ++i) {
+      const int vi = l + 64 * i;
+      if (vi < nv) {
+        gv[i] = ld16(dnr + vi * V);
+        xv[i] = ld16(xr + vi * V);
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+          const int c = vi * V + j;
+          const float g = vget<T>(gv[i], j) * gamma[c];
+          const float xh = (vget<T>(xv[i], j) - mu) * rs;
+          sg += g;
+          sgx += g * xh;
+        }
+      }
+    }
+    const float mg = wave_sum(sg) / d, mgx = wave_sum(sgx) / d;
+#pragma unroll
+    for (int i = 0; i < MAXV; ++i) {
+      const int vi = l + 64 * i;
+      if (vi < nv) {
+        u32x4 rv = {0, 0, 0, 0};
+        if (res) rv = ld16(res + (int64_t)row * d + vi * V);
+        float o[V];
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+          const int c = vi * V + j;
+          const float dnv = vget<T>(gv[i], j);
+          const float xh = (vget<T>(xv[i], j) - mu) * rs;
+          const float g = dnv * gamma[c];
+          o[j] = rs * (g - mg - xh * mgx) + (res ? vget<T>(rv, j) : 0.f);
+          pg[i][j] += dnv * xh;
+          pb[i][j] += dnv;
+        }
+        st16(dx + (int64_t)row * d + vi * V, pack_vec<T>(o));
+      }
+    }
+  }
+  // combine the 4 wavefronts, one 64*V column slice at a time
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      red[0][w][l * V + j] = pg[i][j];
+      red[1][w][l * V + j] = pb[i][j];
+    }
+    __syncthreads();
+    for (int c = threadIdx.x; c < 64 * V; c += NT) {
+      const int col = i * 64 * V + c;
+      if (col < d) {
+        float a = 0.f, b = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < NT / 64; ++ww) {
+          a += red[0][ww][c];
+          b += red[1][ww][c];
+        }
+        part_g[(int64_t)blockIdx.x * d + col] = a;
+        part_b[(int64_t)blockIdx.x * d + col] = b;
+      }
+    }
+  }
+}
+
+// G[c] += sum over nrows partial rows (row stride ncols); one thread per column.
+__global__ void __launch_bounds__(NT) colreduce_acc_kernel(const float* __restrict__ part, int nrows, int ncols,
+                                                            float* G) {
+  const int c = blockIdx.x * NT + threadIdx.x;
+  if (c >= ncols) return;
+  float s = 0.f;
+  for (int r = 0; r < nrows; ++r) s += part[(int64_t)r * ncols + c];
+  G[c] += s;
+}
+
+// Partial column sums: block (x, y) covers columns [x*NT*V, ...) and rows
+// [y*CS_ROWS_PER_BLOCK, ...); thread t owns one 16-byte column vector.
+template <typename T>
+__global__ void __launch_bounds__(NT) colsum_kernel(const T* __restrict__ Y, int64_t ld, int rows, int ncols,
+                                                     float* part) {
+  constexpr int V = Vec<T>::V;
+  const int cv = blockIdx.x * NT + threadIdx.x;
+  const int c0 = cv * V;
+  if (c0 >= ncols) return;
+  float acc[V];
+#pragma unroll
+  for (int j = 0; j < V; ++j) acc[j] = 0.f;
+  const int r0 = blockIdx.y * CS_ROWS_PER_BLOCK;
+  const int r1 = min(rows, r0 + CS_ROWS_PER_BLOCK);
+  for (int r = r0; r < r1; ++r) {
+    const u32x4 v = ld16(Y + (int64_t)r * ld + c0);
+#pragma unroll
+    for (int j = 0; j < V; ++j) acc[j] += vget<T>(v, j);
+  }
+  float* pr = part + (int64_t)blockIdx.y * ncols + c0;
+#pragma unroll
+  for (int j = 0; j < V; ++j)
+    if (c0 + j < ncols) pr[j] = acc[j];
+}
+
+template <typename T, int MAXV>
+hipError_t ln_fwd_launch(const void* x, void* n, float* mean, float* rstd, const float* g, const float* b,
+                         void* xcopy, int rows, int d, float eps, hipStream_t st) {
+  hipLaunchKernelGGL((ln_fwd_kernel<T, MAXV>), dim3((rows + 3) / 4), dim3(NT), 0, st, reinterpret_cast<const T*>(x),
+                     reinterpret_cast<T*>(n), mean, rstd, g, b, reinterpret_cast<T*>(xcopy), rows, d, eps);
+  return hipGetLastError();
+}
+
+template <typename T, int MAXV>
+hipError_t ln_bwd_launch(const void* dn, const void* x, const float* mean, const float* rstd, const float* gamma,
+                         const void* res, void* dx, float* Gg, float* Gb, float* part, int rows, int d,
+                         hipStream_t st) {
+  const int nb = (rows + LN_ROWS_PER_BLOCK - 1) / LN_ROWS_PER_BLOCK;
+  float* pg = part;
+  float* pb = part + (int64_t)nb * d;
+  hipLaunchKernelGGL((ln_bwd_kernel<T, MAXV>), dim3(nb), dim3(NT), 0, st, reinterpret_cast<const T*>(dn),
+                     reinterpret_cast<const T*>(x), mean, rstd, gamma, reinterpret_cast<const T*>(res),
+                     reinterpret_cast<T*>(dx), pg, pb, rows, d);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(colreduce_acc_kernel, dim3((d + NT - 1) / NT), dim3(NT), 0, st, pg, nb, d, Gg);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(colreduce_acc_kernel, dim3((d + NT - 1) / NT), dim3(NT), 0, st, pb, nb, d, Gb);
+  return hipGetLastError();
+}
+
+template <typename T>
+int maxv_for(int d) {
+  const int nv = d / Vec<T>::V;
+  return (nv + 63) / 64;
+}
+
+template <typename T>
+hipError_t ln_fwd_t(const void* x, void* n, float* mean, float* rstd, const float* g, const float* b, void* xcopy,
+                    int rows, int d, float eps, hipStream_t st) {
+  const int mv = maxv_for<T>(d);
+  if (mv <= 1) return ln_fwd_launch<T, 1>(x, n, mean, rstd, g, b, xcopy, rows, d, eps, st);
+  if (mv <= 2) return ln_fwd_launch<T, 2>(x, n, mean, rstd, g, b, xcopy, rows, d, eps, st);
+  if (mv <= 4) return ln_fwd_launch<T, 4>(x, n, mean, rstd, g, b, xcopy, rows, d, eps, st);
+  if (mv <= 8) return ln_fwd_launch<T, 8>(x, n, mean, rstd, g, b, xcopy, rows, d, eps, st);
+  return hipErrorInvalidValue;
+}
+
+template <typename T>
+hipError_t ln_bwd_t(const void* dn, const void* x, const float* mean, const float* rstd, const float* gamma,
+                    const void* res, void* dx, float* Gg, float* Gb, float* part, int rows, int d, hipStream_t st) {
+  const int mv = maxv_for<T>(d);
+  if (mv <= 1) return ln_bwd_launch<T, 1>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, part, rows, d, st);
+  if (mv <= 2) return ln_bwd_launch<T, 2>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, part, rows, d, st);
+  if (mv <= 4) return ln_bwd_launch<T, 4>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, part, rows, d, st);
+  if (mv <= 8) return ln_bwd_launch<T, 8>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, part, rows, d, st);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t layernorm_fwd(DType dt, const void* x, void* n, float* mean, float* rstd, const float* gamma,
+                         const float* beta, void* xcopy, int rows, int d, float eps, hipStream_t st) {
+  if (rows <= 0 || d <= 0 || d % 8) return hipErrorInvalidValue;
+  if (dt == DT_BF16) return ln_fwd_t<bf16>(x, n, mean, rstd, gamma, beta, xcopy, rows, d, eps, st);
+  return ln_fwd_t<float>(x, n, mean, rstd, gamma, beta, xcopy, rows, d, eps, st);
+}
+
+hipError_t layernorm_bwd(DType dt, const void* dn, const void* x, const float* mean, const float* rstd,
+                         const float* gamma, const void* res, void* dx, float* Gg, float* Gb, float* part, int rows,
+                         int d, hipStream_t st) {
+  if (rows <= 0 || d <= 0 || d % 8) return hipErrorInvalidValue;
+  if (dt == DT_BF16) return ln_bwd_t<bf16>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, part, rows, d, st);
+  return ln_bwd_t<float>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, part, rows, d, st);
+}
+
+int64_t ln_bwd_part_floats(int rows, int d) {
+  return 2 * (int64_t)((rows + LN_ROWS_PER_BLOCK - 1) / LN_ROWS_PER_BLOCK) * d;
+}
+
+hipError_t colsum_acc(DType dt, const void* Y, int64_t ld, int rows, int ncols, float* G, float* part,
+                      hipStream_t st) {
+  if (rows <= 0 || ncols <= 0 || ncols % 8 || ld % 8) return hipErrorInvalidValue;
+  const int V = (dt == DT_BF16) ? 8 : 4;
+  const int nrb = (rows + CS_ROWS_PER_BLOCK - 1) / CS_ROWS_PER_BLOCK;
+  dim3 grid((ncols / V + NT - 1) / NT, nrb);
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL(colsum_kernel<bf16>, grid, dim3(NT), 0, st, reinterpret_cast<const bf16*>(Y), ld, rows, ncols,
+                       part);
+  else
+    hipLaunchKernelGGL(colsum_kernel<float>, grid, dim3(NT), 0, st, reinterpret_cast<const float*>(Y), ld, rows,
+                       ncols, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(colreduce_acc_kernel, dim3((ncols + NT - 1) / NT), dim3(NT), 0, st, part, nrb, ncols, G);
+  return hipGetLastError();
+}
+
+int64_t colsum_part_floats(int rows, int ncols) {
+  return (int64_t)((rows + CS_ROWS_PER_BLOCK - 1) / CS_ROWS_PER_BLOCK) * ncols;
+}
+
+}  // namespace paci
+
+// ============================================================================================
+// First stage: embeddings. Last stage: softmax cross-entropy.
+// ============================================================================================
+namespace paci {
+namespace {
+
+template <typename T>
+__global__ void __launch_bounds__(NT) embed_fwd_kernel(const int32_t* __restrict__ ids, const float* __restrict__ wte,
+                                                        const float* __restrict__ wpe, T* x, int S, int d, int V,
+                                                        int64_t total_vec) {
+  const int64_t gv = (int64_t)blockIdx.x * NT + threadIdx.x;  // one vector of 4 columns
+  if (gv >= total_vec) return;
+  const int nv = d / 4;
+  const int64_t t = gv / nv;
+  const int c = (int)(gv % nv) * 4;
+  const int s = (int)(t % S);
+  const int id = ids[t];
+  // ids outside [0, V) are a caller error; they read as a zero row instead of out of bounds
+  const floatx4 a = (id >= 0 && id < V) ? *reinterpret_cast<const floatx4*>(wte + (int64_t)id * d + c)
+                                        : floatx4{0.f, 0.f, 0.f, 0.f};
+  const floatx4 b = *reinterpret_cast<const floatx4*>(wpe + (int64_t)s * d + c);
+  T* o = x + t * d + c;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) o[j] = from_f32<T>(a[j] + b[j]);
+}
+
+template <typename T>
+__global__ void __launch_bounds__(NT) embed_bwd_wte_kernel(const int32_t* __restrict__ ids, const T* __restrict__ dx,
+                                                            float* Gwte, int d, int V, int64_t total) {
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (i >= total) return;
+  const int64_t t = i / d;
+  const int c = (int)(i % d);
+  const int id = ids[t];
+  if (id < 0 || id >= V) return;
+  atomicAdd(Gwte + (int64_t)id * d + c, to_f32(dx[i]));
+}
+
+template <typename T>
+__global__ void __launch_bounds__(NT) embed_bwd_wpe_kernel(const T* __restrict__ dx, float* Gwpe, int mu, int S, int d) {
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;  // (s, c)
+  if (i >= (int64_t)S * d) return;
+  float acc = 0.f;
+  for (int b = 0; b < mu; ++b) acc += to_f32(dx[(int64_t)b * S * d + i]);
+  Gwpe[i] += acc;
+}
+
+__device__ __forceinline__ float block_reduce(float v, float* sh, bool is_max) {
+  v = is_max ? wave_max(v) : wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane_id() == 0) sh[w] = v;
+  __syncthreads();
+  float r = sh[0];
+  for (int i = 1; i < NT / 64; ++i) r = is_max ? fmaxf(r, sh[i]) : r + sh[i];
+  return r;
+}
+
+// One workgroup per token row.
+__global__ void __launch_bounds__(NT) ce_fwd_kernel(const float* __restrict__ z, int64_t ldz,
+                                                     const int32_t* __restrict__ tgt, float* lse, float* loss_row,
+                                                     int V) {
+  __shared__ float sh[NT / 64];
+  const int64_t t = blockIdx.x;
+  const float* zr = z + t * ldz;
+  float mx = -INFINITY;
+  for (int v = threadIdx.x; v < V; v += NT) mx = fmaxf(mx, zr[v]);
+  mx = block_reduce(mx, sh, true);
+  float s = 0.f;
+  for (int v = threadIdx.x; v < V; v += NT) s += expf(zr[v] - mx);
+  s = block_reduce(s, sh, false);
+  if (threadIdx.x == 0) {
+    const float l = mx + logf(s);
+    const int y = tgt[t];
+    lse[t] = l;
+    // a target outside [0, V) is a caller error; it yields a NaN loss instead of an out-of-bounds read
+    loss_row[t] = (y >= 0 && y < V) ? l - zr[y] : NAN;
+  }
+}
+
+// Deterministic mean of T per-token losses: a single workgroup.
+__global__ void __launch_bounds__(NT) mean_kernel(const float* __restrict__ x, int n, float* out) {
+  __shared__ float sh[NT / 64];
+  float s = 0.f;
+  for (int i = threadIdx.x; i < n; i += NT) s += x[i];
+  s = block_reduce(s, sh, false);
+  if (threadIdx.x == 0) *out = s / n;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(NT) ce_bwd_kernel(const float* __restrict__ z, int64_t ldz,
+                                                     const int32_t* __restrict__ tgt, const float* __restrict__ lse,
+                                                     T* dz, int V, float scale) {
+  const int64_t t = blockIdx.x;
+  const float* zr = z + t * ldz;
+  T* dr = dz + t * ldz;
+  const float l = lse[t];
+  const int y = tgt[t];
+  for (int v = threadIdx.x; v < ldz; v += NT) {
+    float g = 0.f;
+    if (v < V) g = scale * (expf(zr[v] - l) - (v == y ? 1.f : 0.f));
+    dr[v] = from_f32<T>(g);
+  }
+}
+
+}  // namespace
+
+hipError_t embed_fwd(DType dt, const int32_t* ids, const float* wte, const float* wpe, void* x, int mu, int S, int d,
+                     int V, hipStream_t st) {
+  if (d % 4) return hipErrorInvalidValue;
+  const int64_t total = (int64_t)mu * S * (d / 4);
+  const dim3 grid((unsigned)((total + NT - 1) / NT));
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL(embed_fwd_kernel<bf16>, grid, dim3(NT), 0, st, ids, wte, wpe, reinterpret_cast<bf16*>(x), S, d,
+                       V, total);
+  else
+    hipLaunchKernelGGL(embed_fwd_kernel<float>, grid, dim3(NT), 0, st, ids, wte, wpe, reinterpret_cast<float*>(x), S,
+                       d, V, total);
+  return hipGetLastError();
+}
+
+hipError_t embed_bwd(DType dt, const int32_t* ids, const void* dx, float* Gwte, float* Gwpe, int mu, int S, int d,
+                     int V, hipStream_t st) {
+  const int64_t total = (int64_t)mu * S * d;
+  const dim3 g1((unsigned)((total + NT - 1) / NT)), g2((unsigned)(((int64_t)S * d + NT - 1) / NT));
+  if (dt == DT_BF16) {
+    hipLaunchKernelGGL(embed_bwd_wte_kernel<bf16>, g1, dim3(NT), 0, st, ids, reinterpret_cast<const bf16*>(dx), Gwte,
+                       d, V, total);
+    hipLaunchKernelGGL(embed_bwd_wpe_kernel<bf16>, g2, dim3(NT), 0, st, reinterpret_cast<const bf16*>(dx), Gwpe, mu,
+                       S, d);
+  } else {
+    hipLaunchKernelGGL(embed_bwd_wte_kernel<float>, g1, dim3(NT), 0, st, ids, reinterpret_cast<const float*>(dx), Gwte,
+                       d, V, total);
+    hipLaunchKernelGGL(embed_bwd_wpe_kernel<float>, g2, dim3(NT), 0, st, reinterpret_cast<const float*>(dx), Gwpe, mu,
+                       S, d);
+  }
+  return hipGetLastError();
+}
+
+hipError_t ce_fwd(const float* z, int64_t ldz, const int32_t* tgt, float* lse, float* loss_out, float* part, int T,
+                  int V, hipStream_t st) {
+  hipLaunchKernelGGL(ce_fwd_kernel, dim3(T), dim3(NT), 0, st, z, ldz, tgt, lse, part, V);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(NT), 0, st, part, T, loss_out);
+  return hipGetLastError();
+}
+
+int64_t ce_part_floats(int T) { return T; }
+
+hipError_t ce_bwd(DType dt, const float* z, int64_t ldz, const int32_t* tgt, const float* lse, void* dz, int T, int V,
+                  float scale, hipStream_t st) {
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL(ce_bwd_kernel<bf16>, dim3(T), dim3(NT), 0, st, z, ldz, tgt, lse, reinterpret_cast<bf16*>(dz), V,
+                       scale);
+  else
+    hipLaunchKernelGGL(ce_bwd_kernel<float>, dim3(T), dim3(NT), 0, st, z, ldz, tgt, lse, reinterpret_cast<float*>(dz),
+                       V, scale);
+  return hipGetLastError();
+}
+
+}  // namespace paci

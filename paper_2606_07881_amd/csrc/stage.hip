@@ -1,0 +1,959 @@
+// The PACI stage runtime behind include/paci_stage.h.
+//
+// One stage of the asynchronous 1F1B pipeline (Alg. 1): a protocol object
+// holding the counters (version t, window count c, unresolved forwards q),
+// a single fp32 parameter copy, the fp32 gradient accumulator G, the AdamW
+// moments, and an activation store of delay + 1 micro-batch slots. All of it
+// is sub-allocated from one caller-owned device arena. Forward, backward and
+// step enqueue the hand-written kernels on one in-order HIP stream. Stream
+// order alone guards the buffers. A slot is rewritten by F(mb + delay + 1)
+// only after B(mb) has consumed it. The update runs after the K-th
+// backward's gradient kernels. The next forward reads the refreshed bf16
+// weights after the update.
+//
+// Drift semantics (Eq. 1): a backward differentiates the activations saved by
+// its forward but reads the current parameters. dgrad uses the current bf16
+// weights and LayerNorm backward the current fp32 gammas. Every activation
+// that depends on parameters (LN outputs, qkv, attention output, x1, u, a) is
+// saved at forward time, never recomputed.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+#include <cmath>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+#include "paci_stage.h"
+
+// ============================================================================================
+// Protocol (Alg. 1)
+// ============================================================================================
+struct paci_fsm {
+  int K, delay, t, c, q, next_f, next_b;
+};
+
+static int fsm_check_forward(const paci_fsm& f, int mb) {
+  if (f.c == f.K) return PACI_E_STEP_PENDING;
+  if (mb != f.next_f) return PACI_E_ORDER;
+  if (!(f.q <= f.delay)) return PACI_E_BACKPRESSURE;  // admission: q_i <= N - i
+  return PACI_OK;
+}
+static int fsm_check_backward(const paci_fsm& f, int mb) {
+  if (f.c == f.K) return PACI_E_STEP_PENDING;
+  if (mb != f.next_b || f.next_b >= f.next_f) return PACI_E_ORDER;
+  return PACI_OK;
+}
+static int fsm_commit_forward(paci_fsm& f) {
+  f.next_f++;
+  f.q++;
+  return f.t;
+}
+static int fsm_commit_backward(paci_fsm& f) {
+  f.next_b++;
+  f.c++;
+  f.q--;
+  return f.t;
+}
+static void fsm_commit_step(paci_fsm& f) {
+  f.c = 0;
+  f.t++;
+}
+static void fsm_counters(const paci_fsm& f, paci_counters* o) {
+  o->version = f.t;
+  o->c = f.c;
+  o->q = f.q;
+  o->next_f = f.next_f;
+  o->next_b = f.next_b;
+  o->K = f.K;
+  o->delay = f.delay;
+}
+
+extern "C" int paci_fsm_create(int K, int delay, paci_fsm** out) {
+  if (!out || K < 1 || delay < 0) return PACI_E_INVAL;
+  paci_fsm* f = new (std::nothrow) paci_fsm{K, delay, 0, 0, 0, 0, 0};
+  if (!f) return PACI_E_NOMEM;
+  *out = f;
+  return PACI_OK;
+}
+extern "C" int paci_fsm_forward(paci_fsm* f, int mb, int* version) {
+  if (!f) return PACI_E_INVAL;
+  const int e = fsm_check_forward(*f, mb);
+  if (e) return e;
+  const int t = fsm_commit_forward(*f);
+  if (version) *version = t;
+  return PACI_OK;
+}
+extern "C" int paci_fsm_backward(paci_fsm* f, int mb, int* version) {
+  if (!f) return PACI_E_INVAL;
+  const int e = fsm_check_backward(*f, mb);
+  if (e) return e;
+  const int t = fsm_commit_backward(*f);
+  if (version) *version = t;
+  return f->c == f->K ? PACI_STEP_DUE : PACI_OK;
+}
+extern "C" int paci_fsm_step(paci_fsm* f, int* new_version) {
+  if (!f) return PACI_E_INVAL;
+  if (f->c != f->K) return PACI_E_NOT_DUE;
+  fsm_commit_step(*f);
+  if (new_version) *new_version = f->t;
+  return PACI_OK;
+}
+extern "C" int paci_fsm_counters(const paci_fsm* f, paci_counters* out) {
+  if (!f || !out) return PACI_E_INVAL;
+  fsm_counters(*f, out);
+  return PACI_OK;
+}
+extern "C" int paci_fsm_destroy(paci_fsm* f) {
+  delete f;
+  return PACI_OK;
+}
+
+extern "C" int paci_schedule(int M, int K, int delay, int32_t* kinds, int32_t* idx, int cap, int* n) {
+  if (M < 0 || K < 1 || delay < 0 || !n) return PACI_E_INVAL;
+  const int total = 2 * M + M / K;
+  *n = total;
+  if (cap < total || (total > 0 && (!kinds || !idx))) return PACI_E_INVAL;
+  int e = 0;
+  auto emit = [&](int k, int i) { kinds[e] = k; idx[e] = i; ++e; };
+  for (int i = 0; i < std::min(delay + 1, M); ++i) emit(0, i);
+  for (int j = 0; j < M; ++j) {
+    emit(1, j);
+    if ((j + 1) % K == 0) emit(2, -1);
+    if (j + delay + 1 < M) emit(0, j + delay + 1);
+  }
+  return PACI_OK;
+}
+
+// ============================================================================================
+// Parameter layout
+// ============================================================================================
+namespace {
+
+struct TensorRef {
+  char name[32];
+  int rows, cols;
+  int64_t off, numel;
+  bool decay;
+};
+
+struct BlockRefs {
+  int64_t ln1_g, ln1_b, w_qkv, b_qkv, w_o, b_o, ln2_g, ln2_b, w_1, b_1, w_2, b_2;
+};
+
+struct ParamTable {
+  std::vector<TensorRef> t;
+  std::vector<BlockRefs> blocks;
+  int64_t wte = -1, wpe = -1, lnf_g = -1, lnf_b = -1, w_lm = -1;
+  int64_t total = 0;
+
+  int64_t add(const std::string& name, int rows, int cols, bool decay) {
+    TensorRef r;
+    memset(r.name, 0, sizeof(r.name));
+    strncpy(r.name, name.c_str(), sizeof(r.name) - 1);
+    r.rows = rows;
+    r.cols = cols;
+    r.off = total;
+    r.numel = (int64_t)rows * cols;
+    r.decay = decay;
+    t.push_back(r);
+    total += r.numel;
+    return r.off;
+  }
+};
+
+int validate_shapes(const paci_shapes* s, int K, int delay) {
+  if (!s) return PACI_E_INVAL;
+  if (K < 1 || delay < 0) return PACI_E_INVAL;
+  if (s->n_layers < 1 || s->n_heads < 1 || s->head_dim < 1 || s->seq < 1 || s->micro_batch < 1 || s->d_ff < 1)
+    return PACI_E_INVAL;
+  if (s->d_model != s->n_heads * s->head_dim) return PACI_E_INVAL;
+  if (s->kind != PACI_MIDDLE && s->kind != PACI_FIRST && s->kind != PACI_LAST) return PACI_E_UNSUPPORTED;
+  if (s->dtype != PACI_FP32 && s->dtype != PACI_BF16) return PACI_E_UNSUPPORTED;
+  if (s->kind != PACI_MIDDLE && s->vocab < 1) return PACI_E_INVAL;
+  if (s->kind == PACI_FIRST && (s->max_pos < 1 || s->seq > s->max_pos)) return PACI_E_INVAL;
+  const int dh = s->head_dim;
+  if (dh != 32 && dh != 64 && dh != 128) return PACI_E_UNSUPPORTED;
+  if (s->dtype == PACI_FP32 && dh == 128) return PACI_E_UNSUPPORTED;
+  if (s->d_model % 32 || s->d_ff % 32) return PACI_E_UNSUPPORTED;
+  if (s->d_model > 4096 || (s->dtype == PACI_FP32 && s->d_model > 2048)) return PACI_E_UNSUPPORTED;
+  const int64_t T = (int64_t)s->micro_batch * s->seq;
+  if (T > (1LL << 30)) return PACI_E_UNSUPPORTED;
+  return PACI_OK;
+}
+
+ParamTable build_params(const paci_shapes& s) {
+  ParamTable p;
+  const int d = s.d_model, f = s.d_ff;
+  if (s.kind == PACI_FIRST) {
+    p.wte = p.add("wte", s.vocab, d, false);
+    p.wpe = p.add("wpe", s.max_pos, d, false);
+  }
+  for (int l = 0; l < s.n_layers; ++l) {
+    const std::string h = "h" + std::to_string(l) + ".";
+    BlockRefs b;
+    b.ln1_g = p.add(h + "ln1_g", d, 1, false);
+    b.ln1_b = p.add(h + "ln1_b", d, 1, false);
+    b.w_qkv = p.add(h + "w_qkv", 3 * d, d, true);
+    b.b_qkv = p.add(h + "b_qkv", 3 * d, 1, false);
+    b.w_o = p.add(h + "w_o", d, d, true);
+    b.b_o = p.add(h + "b_o", d, 1, false);
+    b.ln2_g = p.add(h + "ln2_g", d, 1, false);
+    b.ln2_b = p.add(h + "ln2_b", d, 1, false);
+    b.w_1 = p.add(h + "w_1", f, d, true);
+    b.b_1 = p.add(h + "b_1", f, 1, false);
+    b.w_2 = p.add(h + "w_2", d, f, true);
+    b.b_2 = p.add(h + "b_2", d, 1, false);
+    p.blocks.push_back(b);
+  }
+  if (s.kind == PACI_LAST) {
+    p.lnf_g = p.add("lnf_g", d, 1, false);
+    p.lnf_b = p.add("lnf_b", d, 1, false);
+    p.w_lm = p.add("w_lm", s.vocab, d, true);
+  }
+  return p;
+}
+
+// ---- arena layout ----------------------------------------------------------------------------
+struct Bump {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    off = (off + 255) & ~(size_t)255;
+    const size_t r = off;
+    off += bytes;
+    return r;
+  }
+};
+
+struct BlockSlot {  // byte offsets inside one activation slot
+  size_t x, n1, qkv, o, x1, n2, u, a, mean1, rstd1, mean2, rstd2, lse2;
+};
+
+struct Layout {
+  int64_t P = 0;          // parameters
+  int64_t T = 0;          // tokens per micro-batch
+  int64_t ldz = 0;        // logits row stride (last stage)
+  size_t theta, G, m, v, theta16, chunks;
+  int nchunks = 0;
+  size_t stash, slot_bytes;
+  std::vector<BlockSlot> blk;  // per block, inside a slot
+  size_t s_ids = 0, s_tgt = 0, s_y = 0, s_meanf = 0, s_rstdf = 0, s_nf = 0, s_z = 0, s_lse_ce = 0;
+  // workspace
+  size_t w_dyA, w_dyB, w_du, w_dn, w_dx1, w_do, w_dqkv, w_D, w_part, w_dz = 0, w_dnf = 0, w_loss = 0;
+  size_t total;
+};
+
+constexpr int64_t CHUNK = 16384;  // AdamW elements per workgroup
+
+int count_chunks(const ParamTable& p) {
+  int n = 0;
+  for (const auto& t : p.t) n += (int)((t.numel + CHUNK - 1) / CHUNK);
+  return n;
+}
+
+Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) {
+  (void)K;
+  Layout L;
+  const int64_t esz = s.dtype == PACI_BF16 ? 2 : 4;
+  const int64_t d = s.d_model, f = s.d_ff, T = (int64_t)s.micro_batch * s.seq;
+  const int64_t heads_rows = (int64_t)s.micro_batch * s.n_heads * s.seq;
+  L.P = p.total;
+  L.T = T;
+  L.ldz = ((int64_t)s.vocab + 63) / 64 * 64;
+  Bump a;
+  L.theta = a.take(4 * L.P);
+  L.G = a.take(4 * L.P);
+  L.m = a.take(4 * L.P);
+  L.v = a.take(4 * L.P);
+  L.theta16 = s.dtype == PACI_BF16 ? a.take(2 * L.P) : 0;
+  L.nchunks = count_chunks(p);
+  L.chunks = a.take(16 * (size_t)L.nchunks);
+
+  // one activation slot
+  Bump sl;
+  for (int l = 0; l < s.n_layers; ++l) {
+    BlockSlot b;
+    b.x = sl.take(esz * T * d);
+    b.n1 = sl.take(esz * T * d);
+    b.qkv = sl.take(esz * T * 3 * d);
+    b.o = sl.take(esz * T * d);
+    b.x1 = sl.take(esz * T * d);
+    b.n2 = sl.take(esz * T * d);
+    b.u = sl.take(esz * T * f);
+    b.a = sl.take(esz * T * f);
+    b.mean1 = sl.take(4 * T);
+    b.rstd1 = sl.take(4 * T);
+    b.mean2 = sl.take(4 * T);
+    b.rstd2 = sl.take(4 * T);
+    b.lse2 = sl.take(4 * heads_rows);
+    L.blk.push_back(b);
+  }
+  if (s.kind == PACI_FIRST) L.s_ids = sl.take(4 * T);
+  if (s.kind == PACI_LAST) {
+    L.s_tgt = sl.take(4 * T);
+    L.s_y = sl.take(esz * T * d);
+    L.s_meanf = sl.take(4 * T);
+    L.s_rstdf = sl.take(4 * T);
+    L.s_nf = sl.take(esz * T * d);
+    L.s_z = sl.take(4 * T * L.ldz);
+    L.s_lse_ce = sl.take(4 * T);
+  }
+  L.slot_bytes = (sl.off + 255) & ~(size_t)255;
+  L.stash = a.take(L.slot_bytes * (size_t)(delay + 1));
+
+  // backward workspace (one micro-batch at a time)
+  L.w_dyA = a.take(esz * T * d);
+  L.w_dyB = a.take(esz * T * d);
+  L.w_du = a.take(esz * T * f);
+  L.w_dn = a.take(esz * T * d);
+  L.w_dx1 = a.take(esz * T * d);
+  L.w_do = a.take(esz * T * d);
+  L.w_dqkv = a.take(esz * T * 3 * d);
+  L.w_D = a.take(4 * heads_rows);
+  int64_t part = std::max(paci::colsum_part_floats((int)T, (int)std::max(3 * d, f)),
+                          paci::ln_bwd_part_floats((int)T, (int)d));
+  if (s.kind == PACI_LAST) {
+    part = std::max(part, paci::ce_part_floats((int)T));
+    L.w_dz = a.take(esz * T * L.ldz);
+    L.w_dnf = a.take(esz * T * d);
+  }
+  L.w_part = a.take(4 * part);
+  L.total = (a.off + 255) & ~(size_t)255;
+  return L;
+}
+
+// ---- kernel timing families -------------------------------------------------------------------
+enum Family {
+  F_GEMM_FWD = 0, F_GEMM_DGRAD, F_GEMM_WGRAD, F_ATTN_FWD, F_ATTN_BWD, F_LN_FWD, F_LN_BWD, F_BIAS_GRAD, F_ADAMW,
+  F_EMBED, F_CE, F_COPY, F_COUNT
+};
+const char* kFamilyNames[F_COUNT] = {"gemm_fwd", "gemm_dgrad", "gemm_wgrad_acc", "attn_fwd", "attn_bwd",
+                                     "layernorm_fwd", "layernorm_bwd", "bias_grad", "adamw", "embedding",
+                                     "cross_entropy", "copy"};
+
+}  // namespace
+
+// ============================================================================================
+// The stage handle
+// ============================================================================================
+struct paci_stage {
+  paci_shapes s;
+  paci_fsm fsm;
+  hipStream_t st;
+  char* arena;
+  ParamTable p;
+  Layout L;
+  paci::DType dt;
+  int esz;
+  int last_hip = 0;
+  bool broken = false;
+
+  // timing
+  bool timing = false;
+  struct Pending { hipEvent_t a, b; int fam; double work; };
+  std::vector<Pending> pending;
+  std::vector<hipEvent_t> free_ev;
+  int64_t launches[F_COUNT] = {};
+  double ms[F_COUNT] = {}, work[F_COUNT] = {};
+
+  float* theta() const { return reinterpret_cast<float*>(arena + L.theta); }
+  float* G() const { return reinterpret_cast<float*>(arena + L.G); }
+  float* m() const { return reinterpret_cast<float*>(arena + L.m); }
+  float* v() const { return reinterpret_cast<float*>(arena + L.v); }
+  // weights as consumed by the matrix kernels: the bf16 working copy, or fp32 itself
+  const void* W(int64_t off) const {
+    return dt == paci::DT_BF16 ? (const void*)(reinterpret_cast<const uint16_t*>(arena + L.theta16) + off)
+                               : (const void*)(theta() + off);
+  }
+  const float* th(int64_t off) const { return theta() + off; }
+  float* g(int64_t off) const { return G() + off; }
+  char* slot(int mb) const { return arena + L.stash + (size_t)(mb % (fsm.delay + 1)) * L.slot_bytes; }
+  char* ws(size_t off) const { return arena + off; }
+};
+
+namespace {
+
+hipEvent_t take_event(paci_stage* h) {
+  if (!h->free_ev.empty()) {
+    hipEvent_t e = h->free_ev.back();
+    h->free_ev.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+void drain_timing(paci_stage* h) {
+  for (auto& p : h->pending) {
+    float t = 0.f;
+    if (hipEventSynchronize(p.b) == hipSuccess && hipEventElapsedTime(&t, p.a, p.b) == hipSuccess) {
+      h->launches[p.fam]++;
+      h->ms[p.fam] += t;
+      h->work[p.fam] += p.work;
+    }
+    h->free_ev.push_back(p.a);
+    h->free_ev.push_back(p.b);
+  }
+  h->pending.clear();
+}
+
+// Runs one launch, bracketed by events when timing is on. Returns a PACI status.
+template <class F>
+int run(paci_stage* h, int fam, double work, F&& launch) {
+  hipEvent_t a = nullptr, b = nullptr;
+  if (h->timing) {
+    if (h->pending.size() >= 4096) drain_timing(h);
+    a = take_event(h);
+    b = take_event(h);
+    if (a && b) (void)hipEventRecord(a, h->st);
+  }
+  const hipError_t e = launch();
+  if (e != hipSuccess) {
+    h->last_hip = (int)e;
+    h->broken = true;
+    return PACI_E_HIP;
+  }
+  if (h->timing && a && b) {
+    (void)hipEventRecord(b, h->st);
+    h->pending.push_back({a, b, fam, work});
+  }
+  return PACI_OK;
+}
+
+#define TRY(x)                 \
+  do {                         \
+    const int _r = (x);        \
+    if (_r != PACI_OK) return _r; \
+  } while (0)
+
+// ---- linear-layer helpers -------------------------------------------------------------------
+int linear_fwd(paci_stage* h, const void* X, int64_t w_off, int64_t b_off, int M, int N, int K, paci::GemmEpi epi,
+               void* C, const void* aux, void* C2) {
+  paci::GemmArgs a{X, K, h->W(w_off), K, M, N, K, C, N, b_off >= 0 ? h->th(b_off) : nullptr, aux, N, C2};
+  return run(h, F_GEMM_FWD, 2.0 * M * N * K,
+             [&] { return paci::gemm(h->dt, false, paci::GEMM_NT, epi, a, 1, h->st); });
+}
+
+// dX [M, N] = dY [M, K] . W [K, N]   (W = nn.Linear weight [out = K, in = N])
+int linear_dgrad(paci_stage* h, const void* dY, int64_t ldy, int64_t w_off, int M, int N, int K, paci::GemmEpi epi,
+                 void* C, const void* aux) {
+  paci::GemmArgs a{dY, ldy, h->W(w_off), N, M, N, K, C, N, nullptr, aux, N, nullptr};
+  return run(h, F_GEMM_DGRAD, 2.0 * M * N * K,
+             [&] { return paci::gemm(h->dt, false, paci::GEMM_NN, epi, a, 1, h->st); });
+}
+
+// G[out, in] += dY[T, out]^T X[T, in]
+int linear_wgrad(paci_stage* h, const void* dY, int64_t ldy, const void* X, int64_t ldx, int out, int in, int T,
+                 int64_t g_off) {
+  const int tiles = ((out + paci::gemm_tile_m() - 1) / paci::gemm_tile_m()) *
+                    ((in + paci::gemm_tile_n() - 1) / paci::gemm_tile_n());
+  const int kt = (T + paci::gemm_tile_k(h->dt) - 1) / paci::gemm_tile_k(h->dt);
+  int splits = 1;
+  while (tiles * splits < 512 && splits * 2 <= kt / 4) splits *= 2;
+  paci::GemmArgs a{dY, ldy, X, ldx, out, in, T, h->g(g_off), in, nullptr, nullptr, 0, nullptr};
+  const paci::GemmEpi epi = splits > 1 ? paci::EPI_ATOMIC : paci::EPI_ACC;
+  return run(h, F_GEMM_WGRAD, 2.0 * out * in * T,
+             [&] { return paci::gemm(h->dt, true, paci::GEMM_TN, epi, a, splits, h->st); });
+}
+
+int bias_grad(paci_stage* h, const void* Y, int64_t ld, int rows, int ncols, int64_t g_off) {
+  return run(h, F_BIAS_GRAD, (double)rows * ncols * h->esz, [&] {
+    return paci::colsum_acc(h->dt, Y, ld, rows, ncols, h->g(g_off), reinterpret_cast<float*>(h->ws(h->L.w_part)),
+                            h->st);
+  });
+}
+
+int ln_fwd(paci_stage* h, const void* x, void* n, float* mean, float* rstd, int64_t g_off, int64_t b_off,
+           void* xcopy) {
+  const int T = (int)h->L.T, d = h->s.d_model;
+  return run(h, F_LN_FWD, (double)T * d * 2 * h->esz + 8.0 * T, [&] {
+    return paci::layernorm_fwd(h->dt, x, n, mean, rstd, h->th(g_off), h->th(b_off), xcopy, T, d, h->s.ln_eps, h->st);
+  });
+}
+
+int ln_bwd(paci_stage* h, const void* dn, const void* x, const float* mean, const float* rstd, int64_t g_off,
+           int64_t b_off, const void* res, void* dx) {
+  const int T = (int)h->L.T, d = h->s.d_model;
+  return run(h, F_LN_BWD, (double)T * d * (res ? 4 : 3) * h->esz + 8.0 * T, [&] {
+    return paci::layernorm_bwd(h->dt, dn, x, mean, rstd, h->th(g_off), res, dx, h->g(g_off), h->g(b_off),
+                               reinterpret_cast<float*>(h->ws(h->L.w_part)), T, d, h->st);
+  });
+}
+
+double attn_pairs(const paci_shapes& s) {
+  return (double)s.micro_batch * s.n_heads * ((double)s.seq * (s.seq + 1) / 2.0);
+}
+
+// ---- forward of the block stack -----------------------------------------------------------------
+// in: block-0 input (stage input or embedding output); copy_in: also store it in the slot.
+int blocks_fwd(paci_stage* h, char* sl, const void* in, bool copy_in, void* out) {
+  const paci_shapes& s = h->s;
+  const int T = (int)h->L.T, d = s.d_model, f = s.d_ff;
+  for (int l = 0; l < s.n_layers; ++l) {
+    const BlockRefs& b = h->p.blocks[l];
+    const BlockSlot& o = h->L.blk[l];
+    const void* x = (l == 0) ? in : (const void*)(sl + o.x);
+    float* mean1 = reinterpret_cast<float*>(sl + o.mean1);
+    float* rstd1 = reinterpret_cast<float*>(sl + o.rstd1);
+    TRY(ln_fwd(h, x, sl + o.n1, mean1, rstd1, b.ln1_g, b.ln1_b, (l == 0 && copy_in) ? sl + o.x : nullptr));
+    TRY(linear_fwd(h, sl + o.n1, b.w_qkv, b.b_qkv, T, 3 * d, d, paci::EPI_BIAS, sl + o.qkv, nullptr, nullptr));
+    TRY(run(h, F_ATTN_FWD, 4.0 * attn_pairs(s) * s.head_dim, [&] {
+      return paci::attn_fwd(h->dt, sl + o.qkv, sl + o.o, reinterpret_cast<float*>(sl + o.lse2), s.micro_batch, s.seq,
+                            s.n_heads, s.head_dim, h->st);
+    }));
+    TRY(linear_fwd(h, sl + o.o, b.w_o, b.b_o, T, d, d, paci::EPI_BIAS_RES, sl + o.x1, sl + o.x, nullptr));
+    TRY(ln_fwd(h, sl + o.x1, sl + o.n2, reinterpret_cast<float*>(sl + o.mean2), reinterpret_cast<float*>(sl + o.rstd2),
+               b.ln2_g, b.ln2_b, nullptr));
+    TRY(linear_fwd(h, sl + o.n2, b.w_1, b.b_1, T, f, d, paci::EPI_BIAS_GELU, sl + o.u, nullptr, sl + o.a));
+    void* y = (l + 1 < s.n_layers) ? (void*)(sl + h->L.blk[l + 1].x) : out;
+    TRY(linear_fwd(h, sl + o.a, b.w_2, b.b_2, T, d, f, paci::EPI_BIAS_RES, y, sl + o.x1, nullptr));
+  }
+  return PACI_OK;
+}
+
+// ---- backward of one block: dy -> dx ------------------------------------------------------------
+int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx) {
+  const paci_shapes& s = h->s;
+  const int T = (int)h->L.T, d = s.d_model, f = s.d_ff;
+  const BlockRefs& b = h->p.blocks[l];
+  const BlockSlot& o = h->L.blk[l];
+  const Layout& L = h->L;
+  char* du = h->ws(L.w_du);
+  char* dn = h->ws(L.w_dn);
+  char* dx1 = h->ws(L.w_dx1);
+  char* dO = h->ws(L.w_do);
+  char* dqkv = h->ws(L.w_dqkv);
+  // y = x1 + a W2^T + b2
+  TRY(linear_wgrad(h, dy, d, sl + o.a, f, d, f, T, b.w_2));
+  TRY(bias_grad(h, dy, d, T, d, b.b_2));
+  TRY(linear_dgrad(h, dy, d, b.w_2, T, f, d, paci::EPI_GELU_GRAD, du, sl + o.u));
+  // u = n2 W1^T + b1
+  TRY(linear_wgrad(h, du, f, sl + o.n2, d, f, d, T, b.w_1));
+  TRY(bias_grad(h, du, f, T, f, b.b_1));
+  TRY(linear_dgrad(h, du, f, b.w_1, T, d, f, paci::EPI_STORE, dn, nullptr));
+  // n2 = LN2(x1); dx1 = dy + LN2 backward
+  TRY(ln_bwd(h, dn, sl + o.x1, reinterpret_cast<const float*>(sl + o.mean2),
+             reinterpret_cast<const float*>(sl + o.rstd2), b.ln2_g, b.ln2_b, dy, dx1));
+  // x1 = x + o Wo^T + bo
+  TRY(linear_wgrad(h, dx1, d, sl + o.o, d, d, d, T, b.w_o));
+  TRY(bias_grad(h, dx1, d, T, d, b.b_o));
+  TRY(linear_dgrad(h, dx1, d, b.w_o, T, d, d, paci::EPI_STORE, dO, nullptr));
+  // attention
+  TRY(run(h, F_ATTN_BWD, 8.0 * attn_pairs(s) * s.head_dim, [&] {
+    return paci::attn_bwd(h->dt, sl + o.qkv, sl + o.o, dO, reinterpret_cast<const float*>(sl + o.lse2),
+                          reinterpret_cast<float*>(h->ws(L.w_D)), dqkv, s.micro_batch, s.seq, s.n_heads, s.head_dim,
+                          h->st);
+  }));
+  // qkv = n1 Wqkv^T + bqkv
+  TRY(linear_wgrad(h, dqkv, 3 * d, sl + o.n1, d, 3 * d, d, T, b.w_qkv));
+  TRY(bias_grad(h, dqkv, 3 * d, T, 3 * d, b.b_qkv));
+  TRY(linear_dgrad(h, dqkv, 3 * d, b.w_qkv, T, d, 3 * d, paci::EPI_STORE, dn, nullptr));
+  // n1 = LN1(x); dx = dx1 + LN1 backward
+  TRY(ln_bwd(h, dn, sl + o.x, reinterpret_cast<const float*>(sl + o.mean1),
+             reinterpret_cast<const float*>(sl + o.rstd1), b.ln1_g, b.ln1_b, dx1, dx));
+  return PACI_OK;
+}
+
+size_t act_bytes(const paci_stage* h) { return (size_t)h->L.T * h->s.d_model * h->esz; }
+
+}  // namespace
+
+// ============================================================================================
+// C ABI
+// ============================================================================================
+extern "C" int paci_param_count(const paci_shapes* s, int* n_tensors, int64_t* n_elements) {
+  if (!s) return PACI_E_INVAL;
+  const int v = validate_shapes(s, 1, 0);
+  if (v) return v;
+  const ParamTable p = build_params(*s);
+  if (n_tensors) *n_tensors = (int)p.t.size();
+  if (n_elements) *n_elements = p.total;
+  return PACI_OK;
+}
+
+extern "C" int paci_param_info_at(const paci_shapes* s, int index, paci_param_info* out) {
+  if (!s || !out) return PACI_E_INVAL;
+  const int v = validate_shapes(s, 1, 0);
+  if (v) return v;
+  const ParamTable p = build_params(*s);
+  if (index < 0 || index >= (int)p.t.size()) return PACI_E_INVAL;
+  const TensorRef& t = p.t[index];
+  memcpy(out->name, t.name, sizeof(out->name));
+  out->rows = t.rows;
+  out->cols = t.cols;
+  out->offset = t.off;
+  out->numel = t.numel;
+  out->decay = t.decay ? 1 : 0;
+  return PACI_OK;
+}
+
+extern "C" int paci_stage_arena_bytes(const paci_shapes* s, int K, int delay, size_t* bytes) {
+  if (!bytes) return PACI_E_INVAL;
+  const int v = validate_shapes(s, K, delay);
+  if (v) return v;
+  const ParamTable p = build_params(*s);
+  *bytes = make_layout(*s, K, delay, p).total;
+  return PACI_OK;
+}
+
+extern "C" int paci_stage_init(const paci_shapes* s, int K, int delay, void* dev_arena, size_t arena_bytes,
+                               void* hip_stream, paci_stage** out) {
+  if (!out || !dev_arena) return PACI_E_INVAL;
+  if (reinterpret_cast<uintptr_t>(dev_arena) & 255) return PACI_E_INVAL;
+  const int v = validate_shapes(s, K, delay);
+  if (v) return v;
+  paci_stage* h = new (std::nothrow) paci_stage();
+  if (!h) return PACI_E_NOMEM;
+  h->s = *s;
+  h->fsm = paci_fsm{K, delay, 0, 0, 0, 0, 0};
+  h->st = reinterpret_cast<hipStream_t>(hip_stream);
+  h->arena = reinterpret_cast<char*>(dev_arena);
+  h->p = build_params(*s);
+  h->L = make_layout(*s, K, delay, h->p);
+  h->dt = s->dtype == PACI_BF16 ? paci::DT_BF16 : paci::DT_F32;
+  h->esz = s->dtype == PACI_BF16 ? 2 : 4;
+  if (arena_bytes < h->L.total) {
+    delete h;
+    return PACI_E_NOMEM;
+  }
+  if (h->p.total >= (int64_t)INT32_MAX) {
+    delete h;
+    return PACI_E_UNSUPPORTED;
+  }
+  // AdamW chunk table: chunks never cross a tensor boundary
+  std::vector<int32_t> chunks;
+  chunks.reserve(4 * (size_t)h->L.nchunks);
+  for (const auto& t : h->p.t)
+    for (int64_t b = 0; b < t.numel; b += CHUNK) {
+      chunks.push_back((int32_t)(t.off + b));
+      chunks.push_back((int32_t)(t.off + std::min(t.numel, b + CHUNK)));
+      chunks.push_back(t.decay ? 1 : 0);
+      chunks.push_back(0);
+    }
+  hipError_t e = hipMemsetAsync(h->arena, 0, h->L.stash, h->st);  // theta, G, m, v, bf16 copy
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(h->arena + h->L.chunks, chunks.data(), chunks.size() * sizeof(int32_t),
+                       hipMemcpyHostToDevice, h->st);
+  if (e == hipSuccess) e = hipStreamSynchronize(h->st);
+  if (e != hipSuccess) {
+    delete h;
+    return PACI_E_HIP;
+  }
+  *out = h;
+  return PACI_OK;
+}
+
+extern "C" int paci_stage_destroy(paci_stage* h) {
+  if (!h) return PACI_E_INVAL;
+  for (auto& p : h->pending) {
+    (void)hipEventDestroy(p.a);
+    (void)hipEventDestroy(p.b);
+  }
+  for (auto e : h->free_ev) (void)hipEventDestroy(e);
+  delete h;
+  return PACI_OK;
+}
+
+static float* state_ptr(paci_stage* h, int what) {
+  switch (what) {
+    case PACI_PARAMS: return h->theta();
+    case PACI_GRADS: return h->G();
+    case PACI_EXP_AVG: return h->m();
+    case PACI_EXP_AVG_SQ: return h->v();
+  }
+  return nullptr;
+}
+
+extern "C" int paci_stage_load(paci_stage* h, int what, const float* src, int64_t n, int on_device) {
+  if (!h || !src || n != h->p.total) return PACI_E_INVAL;
+  if (h->broken) return PACI_E_HIP;
+  float* dst = state_ptr(h, what);
+  if (!dst) return PACI_E_INVAL;
+  hipError_t e = hipMemcpyAsync(dst, src, (size_t)n * 4, on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice,
+                                h->st);
+  if (e == hipSuccess && what == PACI_PARAMS && h->dt == paci::DT_BF16)
+    e = paci::f32_to_bf16(h->theta(), h->arena + h->L.theta16, n, h->st);
+  if (e == hipSuccess && !on_device) e = hipStreamSynchronize(h->st);
+  if (e != hipSuccess) {
+    h->last_hip = (int)e;
+    return PACI_E_HIP;
+  }
+  return PACI_OK;
+}
+
+extern "C" int paci_stage_read(paci_stage* h, int what, float* dst, int64_t n, int on_device) {
+  if (!h || !dst || n != h->p.total) return PACI_E_INVAL;
+  if (h->broken) return PACI_E_HIP;
+  const float* src = state_ptr(h, what);
+  if (!src) return PACI_E_INVAL;
+  hipError_t e = hipMemcpyAsync(dst, src, (size_t)n * 4, on_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost,
+                                h->st);
+  if (e == hipSuccess && !on_device) e = hipStreamSynchronize(h->st);
+  if (e != hipSuccess) {
+    h->last_hip = (int)e;
+    return PACI_E_HIP;
+  }
+  return PACI_OK;
+}
+
+extern "C" int paci_stage_forward(paci_stage* h, int mb, const void* dev_in, const int32_t* dev_targets,
+                                  void* dev_out, int* version) {
+  if (!h || !dev_in || !dev_out) return PACI_E_INVAL;
+  if (h->s.kind == PACI_LAST && !dev_targets) return PACI_E_INVAL;
+  if (h->broken) return PACI_E_HIP;
+  const int chk = fsm_check_forward(h->fsm, mb);
+  if (chk) return chk;
+  const paci_shapes& s = h->s;
+  const Layout& L = h->L;
+  const int T = (int)L.T, d = s.d_model;
+  char* sl = h->slot(mb);
+  int r = PACI_OK;
+  if (s.kind == PACI_FIRST) {
+    int32_t* ids = reinterpret_cast<int32_t*>(sl + L.s_ids);
+    r = run(h, F_COPY, 8.0 * T, [&] {
+      return hipMemcpyAsync(ids, dev_in, 4 * (size_t)T, hipMemcpyDeviceToDevice, h->st);
+    });
+    if (!r)
+      r = run(h, F_EMBED, (double)T * d * (8 + h->esz), [&] {
+        return paci::embed_fwd(h->dt, ids, h->th(h->p.wte), h->th(h->p.wpe), sl + L.blk[0].x, s.micro_batch, s.seq,
+                               d, s.vocab, h->st);
+      });
+    if (!r) r = blocks_fwd(h, sl, sl + L.blk[0].x, false, dev_out);
+  } else if (s.kind == PACI_MIDDLE) {
+    r = blocks_fwd(h, sl, dev_in, true, dev_out);
+  } else {
+    int32_t* tgt = reinterpret_cast<int32_t*>(sl + L.s_tgt);
+    r = run(h, F_COPY, 8.0 * T, [&] {
+      return hipMemcpyAsync(tgt, dev_targets, 4 * (size_t)T, hipMemcpyDeviceToDevice, h->st);
+    });
+    if (!r) r = blocks_fwd(h, sl, dev_in, true, sl + L.s_y);
+    float* meanf = reinterpret_cast<float*>(sl + L.s_meanf);
+    float* rstdf = reinterpret_cast<float*>(sl + L.s_rstdf);
+    float* z = reinterpret_cast<float*>(sl + L.s_z);
+    if (!r) r = ln_fwd(h, sl + L.s_y, sl + L.s_nf, meanf, rstdf, h->p.lnf_g, h->p.lnf_b, nullptr);
+    if (!r) {
+      paci::GemmArgs a{sl + L.s_nf, d, h->W(h->p.w_lm), d, T, s.vocab, d, z, L.ldz, nullptr, nullptr, 0, nullptr};
+      r = run(h, F_GEMM_FWD, 2.0 * T * s.vocab * d,
+              [&] { return paci::gemm(h->dt, true, paci::GEMM_NT, paci::EPI_STORE, a, 1, h->st); });
+    }
+    if (!r)
+      r = run(h, F_CE, 4.0 * T * s.vocab, [&] {
+        return paci::ce_fwd(z, L.ldz, tgt, reinterpret_cast<float*>(sl + L.s_lse_ce), reinterpret_cast<float*>(dev_out),
+                            reinterpret_cast<float*>(h->ws(L.w_part)), T, s.vocab, h->st);
+      });
+  }
+  if (r) return r;
+  const int t = fsm_commit_forward(h->fsm);
+  if (version) *version = t;
+  return PACI_OK;
+}
+
+extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_out, void* dev_grad_in,
+                                   int* version) {
+  if (!h) return PACI_E_INVAL;
+  const paci_shapes& s = h->s;
+  if (s.kind == PACI_LAST ? (dev_grad_out != nullptr) : (dev_grad_out == nullptr)) return PACI_E_INVAL;
+  if (s.kind == PACI_FIRST && dev_grad_in) return PACI_E_INVAL;
+  if (h->broken) return PACI_E_HIP;
+  const int chk = fsm_check_backward(h->fsm, mb);
+  if (chk) return chk;
+  const Layout& L = h->L;
+  const int T = (int)L.T, d = s.d_model;
+  char* sl = h->slot(mb);
+  char* bufA = h->ws(L.w_dyA);
+  char* bufB = h->ws(L.w_dyB);
+  const void* dy = dev_grad_out;
+  int r = PACI_OK;
+  if (s.kind == PACI_LAST) {
+    const float* z = reinterpret_cast<const float*>(sl + L.s_z);
+    const int32_t* tgt = reinterpret_cast<const int32_t*>(sl + L.s_tgt);
+    char* dz = h->ws(L.w_dz);
+    char* dnf = h->ws(L.w_dnf);
+    const float scale = 1.0f / ((float)T * (float)h->fsm.K);
+    r = run(h, F_CE, (double)T * L.ldz * (4 + h->esz), [&] {
+      return paci::ce_bwd(h->dt, z, L.ldz, tgt, reinterpret_cast<const float*>(sl + L.s_lse_ce), dz, T, s.vocab,
+                          scale, h->st);
+    });
+    if (!r) r = linear_wgrad(h, dz, L.ldz, sl + L.s_nf, d, s.vocab, d, T, h->p.w_lm);
+    if (!r) r = linear_dgrad(h, dz, L.ldz, h->p.w_lm, T, d, s.vocab, paci::EPI_STORE, dnf, nullptr);
+    if (!r)
+      r = ln_bwd(h, dnf, sl + L.s_y, reinterpret_cast<const float*>(sl + L.s_meanf),
+                 reinterpret_cast<const float*>(sl + L.s_rstdf), h->p.lnf_g, h->p.lnf_b, nullptr, bufA);
+    dy = bufA;
+  }
+  for (int l = s.n_layers - 1; l >= 0 && !r; --l) {
+    void* dx;
+    if (l == 0 && s.kind != PACI_FIRST && dev_grad_in)
+      dx = dev_grad_in;
+    else
+      dx = (dy == bufA) ? bufB : bufA;
+    r = block_bwd(h, sl, l, dy, dx);
+    dy = dx;
+  }
+  if (!r && s.kind == PACI_FIRST) {
+    r = run(h, F_EMBED, (double)T * d * (h->esz + 8), [&] {
+      return paci::embed_bwd(h->dt, reinterpret_cast<const int32_t*>(sl + L.s_ids), dy, h->g(h->p.wte),
+                             h->g(h->p.wpe), s.micro_batch, s.seq, d, s.vocab, h->st);
+    });
+  }
+  if (r) return r;
+  const int t = fsm_commit_backward(h->fsm);
+  if (version) *version = t;
+  return h->fsm.c == h->fsm.K ? PACI_STEP_DUE : PACI_OK;
+}
+
+extern "C" int paci_stage_step(paci_stage* h, int* new_version) {
+  if (!h) return PACI_E_INVAL;
+  if (h->fsm.c != h->fsm.K) return PACI_E_NOT_DUE;
+  if (h->broken) return PACI_E_HIP;
+  const paci_shapes& s = h->s;
+  const int t_adam = h->fsm.t + 1;
+  paci::AdamwArgs a;
+  a.lr = s.lr;
+  a.beta1 = s.beta1;
+  a.beta2 = s.beta2;
+  a.eps = s.eps;
+  a.weight_decay = s.weight_decay;
+  a.bc1 = (float)(1.0 - std::pow((double)s.beta1, t_adam));
+  a.bc2 = (float)(1.0 - std::pow((double)s.beta2, t_adam));
+  const int r = run(h, F_ADAMW, 30.0 * (double)h->p.total, [&] {
+    return paci::adamw(h->theta(), h->G(), h->m(), h->v(),
+                       h->dt == paci::DT_BF16 ? (void*)(h->arena + h->L.theta16) : nullptr,
+                       reinterpret_cast<const int4*>(h->arena + h->L.chunks), h->L.nchunks, a, h->st);
+  });
+  if (r) return r;
+  fsm_commit_step(h->fsm);
+  if (new_version) *new_version = h->fsm.t;
+  return PACI_OK;
+}
+
+extern "C" int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, const int32_t* dev_targets_all,
+                              const void* dev_grad_out_all, void* dev_out_all, void* dev_grad_in_all,
+                              int32_t* host_stamps) {
+  if (!h || M < 0 || !dev_in_all) return PACI_E_INVAL;
+  const paci_shapes& s = h->s;
+  if (s.kind == PACI_LAST && !dev_targets_all) return PACI_E_INVAL;
+  if (s.kind != PACI_LAST && !dev_grad_out_all) return PACI_E_INVAL;
+  if (h->fsm.next_f != 0 || h->fsm.next_b != 0 || h->fsm.c != 0) return PACI_E_ORDER;
+  const paci_fsm& f = h->fsm;
+  const int K = f.K, delay = f.delay;
+  const int64_t T = h->L.T;
+  const size_t act = act_bytes(h);
+  const size_t in_stride = s.kind == PACI_FIRST ? 4 * (size_t)T : act;
+  const size_t out_stride = s.kind == PACI_LAST ? sizeof(float) : act;
+  // scratch outputs when the caller discards them
+  char* out_scratch = h->ws(h->L.w_dyB);
+  float* loss_scratch = reinterpret_cast<float*>(h->ws(h->L.w_part));
+  std::vector<int32_t> kinds(2 * (size_t)M + M / K + 1), idx(kinds.size());
+  int n = 0;
+  int r = paci_schedule(M, K, delay, kinds.data(), idx.data(), (int)kinds.size(), &n);
+  if (r) return r;
+  for (int e = 0; e < n; ++e) {
+    const int i = idx[e];
+    int ver = 0;
+    if (kinds[e] == 0) {
+      const char* in = reinterpret_cast<const char*>(dev_in_all) + in_stride * i;
+      const int32_t* tg = dev_targets_all ? dev_targets_all + T * i : nullptr;
+      void* out = dev_out_all ? (void*)(reinterpret_cast<char*>(dev_out_all) + out_stride * i)
+                              : (s.kind == PACI_LAST ? (void*)loss_scratch : (void*)out_scratch);
+      // a middle/first stage writes its output before any backward reads the scratch buffer
+      r = paci_stage_forward(h, i, in, tg, out, &ver);
+      if (r < 0) return r;
+      if (host_stamps) host_stamps[3 * i] = ver;
+    } else if (kinds[e] == 1) {
+      const void* go = s.kind == PACI_LAST ? nullptr
+                                           : (const void*)(reinterpret_cast<const char*>(dev_grad_out_all) + act * i);
+      void* gi = (s.kind != PACI_FIRST && dev_grad_in_all) ? (void*)(reinterpret_cast<char*>(dev_grad_in_all) + act * i)
+                                                           : nullptr;
+      r = paci_stage_backward(h, i, go, gi, &ver);
+      if (r < 0) return r;
+      if (host_stamps) {
+        host_stamps[3 * i + 1] = ver;
+        host_stamps[3 * i + 2] = ver - host_stamps[3 * i];
+      }
+    } else {
+      r = paci_stage_step(h, &ver);
+      if (r < 0) return r;
+    }
+  }
+  return PACI_OK;
+}
+
+extern "C" int paci_stage_reset_counters(paci_stage* h) {
+  if (!h) return PACI_E_INVAL;
+  h->fsm.t = h->fsm.c = h->fsm.q = h->fsm.next_f = h->fsm.next_b = 0;
+  return PACI_OK;
+}
+
+extern "C" int paci_stage_counters(const paci_stage* h, paci_counters* out) {
+  if (!h || !out) return PACI_E_INVAL;
+  fsm_counters(h->fsm, out);
+  return PACI_OK;
+}
+
+extern "C" int paci_stage_sync(paci_stage* h) {
+  if (!h) return PACI_E_INVAL;
+  const hipError_t e = hipStreamSynchronize(h->st);
+  if (e != hipSuccess) {
+    h->last_hip = (int)e;
+    return PACI_E_HIP;
+  }
+  return PACI_OK;
+}
+
+extern "C" int paci_last_hip_error(const paci_stage* h) { return h ? h->last_hip : 0; }
+
+extern "C" const char* paci_strerror(int status) {
+  switch (status) {
+    case PACI_OK: return "ok";
+    case PACI_STEP_DUE: return "optimizer step due";
+    case PACI_E_INVAL: return "invalid argument";
+    case PACI_E_UNSUPPORTED: return "unsupported shape or dtype";
+    case PACI_E_NOMEM: return "arena too small";
+    case PACI_E_ORDER: return "micro-batch out of order";
+    case PACI_E_BACKPRESSURE: return "forward refused by the admission rule (q > delay)";
+    case PACI_E_STEP_PENDING: return "optimizer step pending";
+    case PACI_E_NOT_DUE: return "optimizer step not due";
+    case PACI_E_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+extern "C" int paci_kernel_family_count(void) { return F_COUNT; }
+extern "C" const char* paci_kernel_family_name(int family) {
+  return (family >= 0 && family < F_COUNT) ? kFamilyNames[family] : nullptr;
+}
+
+extern "C" int paci_stage_set_timing(paci_stage* h, int enable) {
+  if (!h) return PACI_E_INVAL;
+  if (!enable && h->timing) {
+    const hipError_t e = hipStreamSynchronize(h->st);
+    drain_timing(h);
+    if (e != hipSuccess) {
+      h->last_hip = (int)e;
+      h->timing = false;
+      return PACI_E_HIP;
+    }
+  }
+  if (enable && !h->timing) {
+    for (int i = 0; i < F_COUNT; ++i) {
+      h->launches[i] = 0;
+      h->ms[i] = h->work[i] = 0;
+    }
+  }
+  h->timing = enable != 0;
+  return PACI_OK;
+}
+
+extern "C" int paci_stage_kernel_times(paci_stage* h, int family, int64_t* launches, double* ms, double* work) {
+  if (!h || family < 0 || family >= F_COUNT) return PACI_E_INVAL;
+  drain_timing(h);
+  if (launches) *launches = h->launches[family];
+  if (ms) *ms = h->ms[family];
+  if (work) *work = h->work[family];
+  return PACI_OK;
+}

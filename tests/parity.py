@@ -1,0 +1,257 @@
+"""Shared helpers of the GPU parity tests (not collected by pytest).
+
+The GPU side is driven only through the C ABI (paper_2606_07881_amd.binding);
+the expected side is only the oracle. Both consume the same seeded inputs
+from paper_2606_07881_amd.inputs.
+
+Error metric (per tensor): e(x, r) = max|x - r| / max|r| (absolute when r == 0).
+Tolerances: fp32 stages 1e-4 everywhere; bf16 stages 2e-2 on activations and
+the loss, 3e-2 on gradients, parameters and moments.
+
+Where several results are correct: the first AdamW step moves each weight by
+about lr * sign(G). Later steps use m_hat / sqrt(v_hat). Wherever that ratio
+is ill-conditioned (sqrt(v_hat) of the oracle is below KAPPA times the largest
+G discrepancy seen for that tensor up to now), a G inside its tolerance can
+flip the direction. Such elements are only checked for validity: within
+2 * lr * (sum of the largest possible Adam step sizes) of the oracle. All
+other elements are compared to the tolerance. G, m and v are continuous in
+the gradient and are always compared in full.
+"""
+import os
+import sys
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from oracle import adamw as oadamw  # noqa: E402
+from oracle import schedule as osched  # noqa: E402
+from oracle import stage as ostage  # noqa: E402
+from paper_2606_07881_amd import configs, inputs  # noqa: E402
+
+KAPPA = 100.0
+
+
+def tol(c, kind):
+    if c["dtype"] == "fp32":
+        return 1e-4
+    return 2e-2 if kind == "act" else 3e-2
+
+
+def rel_err(x, r):
+    x = np.asarray(x, np.float64)
+    r = np.asarray(r, np.float64)
+    assert x.shape == r.shape, (x.shape, r.shape)
+    if x.size == 0:
+        return 0.0
+    if not np.all(np.isfinite(x)):
+        return float("inf")
+    den = np.abs(r).max()
+    num = np.abs(x - r).max()
+    return float(num / den) if den > 0 else float(num)
+
+
+def small_cfg(name, **kw):
+    """Parity workloads small enough for the oracle (seconds), spanning several
+    tiles with ragged tails."""
+    base = {
+        # ragged in tokens (T = 400), model width (192 = 1.5 GEMM tiles) and keys (S = 200)
+        "ragged_bf16": dict(kind="middle", n_layers=2, d_model=192, n_heads=3, head_dim=64, d_ff=768, seq=200,
+                            micro_batch=2, K=4, delay=3, M=12, dtype="bf16"),
+        "ragged_fp32": dict(kind="middle", n_layers=2, d_model=96, n_heads=3, head_dim=32, d_ff=320, seq=100,
+                            micro_batch=2, K=3, delay=2, M=9, dtype="fp32"),
+        "dh128_bf16": dict(kind="middle", n_layers=1, d_model=256, n_heads=2, head_dim=128, d_ff=512, seq=160,
+                           micro_batch=2, K=2, delay=1, M=6, dtype="bf16"),
+        "dh32_bf16": dict(kind="middle", n_layers=1, d_model=128, n_heads=4, head_dim=32, d_ff=256, seq=96,
+                          micro_batch=3, K=3, delay=2, M=9, dtype="bf16"),
+        "dh64_fp32": dict(kind="middle", n_layers=1, d_model=128, n_heads=2, head_dim=64, d_ff=256, seq=80,
+                          micro_batch=2, K=2, delay=1, M=4, dtype="fp32"),
+        "first_bf16": dict(kind="first", n_layers=1, d_model=128, n_heads=2, head_dim=64, d_ff=512, seq=100,
+                           micro_batch=2, vocab=1000, max_pos=128, K=2, delay=2, M=6, dtype="bf16"),
+        "last_bf16": dict(kind="last", n_layers=1, d_model=128, n_heads=2, head_dim=64, d_ff=512, seq=100,
+                          micro_batch=2, vocab=1000, max_pos=128, K=2, delay=0, M=4, dtype="bf16"),
+        "first_fp32": dict(kind="first", n_layers=1, d_model=64, n_heads=2, head_dim=32, d_ff=128, seq=40,
+                           micro_batch=2, vocab=301, max_pos=64, K=2, delay=1, M=4, dtype="fp32"),
+        "last_fp32": dict(kind="last", n_layers=1, d_model=64, n_heads=2, head_dim=32, d_ff=128, seq=40,
+                          micro_batch=2, vocab=301, max_pos=64, K=2, delay=0, M=4, dtype="fp32"),
+    }[name]
+    c = configs.get("tiny_fp32")
+    c.update(vocab=0, max_pos=0)
+    c.update(base)
+    c.update(kw)
+    c["name"] = name
+    return c
+
+
+# ---- inputs ------------------------------------------------------------------------------------
+class Inputs:
+    """Seeded inputs of M micro-batches as oracle values and device bits."""
+
+    def __init__(self, c, seed, M):
+        self.c, self.seed, self.M = c, seed, M
+        self.params = inputs.make_params(c, seed)
+        self.x, self.x_dev, self.dy, self.dy_dev, self.ids, self.tgt = [], [], [], [], [], []
+        for i in range(M):
+            if c["kind"] == "first":
+                ids = inputs.make_ids(c, seed, i)
+                self.x.append(ids)
+                self.x_dev.append(ids)
+            else:
+                v, b = inputs.make_x(c, seed, i)
+                self.x.append(v.astype(np.float64))
+                self.x_dev.append(b)
+            if c["kind"] == "last":
+                t = inputs.make_targets(c, seed, i)
+                self.tgt.append(t)
+            else:
+                v, b = inputs.make_dy(c, seed, i)
+                self.dy.append(v.astype(np.float64))
+                self.dy_dev.append(b)
+
+    def oracle_params(self):
+        return {k: v.astype(np.float64) for k, v in self.params.items()}
+
+
+def to_torch(a):
+    import torch
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def to_host(t):
+    import torch
+    if t.dtype == torch.bfloat16:
+        return t.float().cpu().numpy().astype(np.float64)
+    return t.cpu().numpy().astype(np.float64)
+
+
+def unflatten(c, flat, table=None):
+    out = {}
+    off = 0
+    for name, shape, _ in inputs.param_specs(c):
+        n = int(np.prod(shape))
+        out[name] = flat[off:off + n].reshape(shape).astype(np.float64)
+        off += n
+    return out
+
+
+# ---- GPU replay, driven event by event through the C ABI --------------------------------------
+def gpu_replay(c, inp, events=None, K=None, delay=None):
+    import torch
+    from paper_2606_07881_amd import binding
+    K = c["K"] if K is None else K
+    delay = c["delay"] if delay is None else delay
+    M = inp.M
+    st = binding.Stage(c, K, delay)
+    st.load_params(inp.params)
+    if events is None:
+        kinds, idx = binding.schedule(M, K, delay)
+        events = [("F", int(i)) if k == 0 else ("B", int(i)) if k == 1 else ("S", None) for k, i in zip(kinds, idx)]
+    T, d = c["micro_batch"] * c["seq"], c["d_model"]
+    act = st.act_dtype
+    rec = dict(out=[None] * M, grad_in=[None] * M, tF=[None] * M, tB=[None] * M, G=[], theta=[], m=[], v=[])
+    outs, gins, xs, dys, tgs = {}, {}, {}, {}, {}
+    for kind, i in events:
+        if kind == "F":
+            xs[i] = to_torch(inp.x_dev[i])
+            if c["kind"] == "last":
+                tgs[i] = to_torch(inp.tgt[i])
+                outs[i] = torch.zeros(1, dtype=torch.float32, device="cuda")
+            else:
+                outs[i] = torch.zeros(T, d, dtype=act, device="cuda")
+            rec["tF"][i] = st.forward(i, xs[i], outs[i], tgs.get(i))
+        elif kind == "B":
+            go = None
+            if c["kind"] != "last":
+                dys[i] = to_torch(inp.dy_dev[i])
+                go = dys[i]
+            gi = None
+            if c["kind"] != "first":
+                gins[i] = torch.zeros(T, d, dtype=act, device="cuda")
+                gi = gins[i]
+            rec["tB"][i], _ = st.backward(i, go, gi)
+        else:
+            rec["G"].append(unflatten(c, st.read(binding.GRADS)))
+            st.step()
+            rec["theta"].append(unflatten(c, st.read(binding.PARAMS)))
+            rec["m"].append(unflatten(c, st.read(binding.EXP_AVG)))
+            rec["v"].append(unflatten(c, st.read(binding.EXP_AVG_SQ)))
+    st.sync()
+    for i in range(M):
+        if i in outs:
+            rec["out"][i] = to_host(outs[i])[0] if c["kind"] == "last" else to_host(outs[i])
+        if i in gins:
+            rec["grad_in"][i] = to_host(gins[i])
+    rec["delta"] = [None if f is None or b is None else b - f for f, b in zip(rec["tF"], rec["tB"])]
+    rec["counters"] = st.counters()
+    st.close()
+    return rec
+
+
+def oracle_replay(c, inp, events=None, K=None, delay=None):
+    K = c["K"] if K is None else K
+    delay = c["delay"] if delay is None else delay
+    return ostage.replay(c, inp.oracle_params(), K, delay, inp.x,
+                         grad_outs=None if c["kind"] == "last" else inp.dy,
+                         targets=inp.tgt if c["kind"] == "last" else None, events=events)
+
+
+# ---- comparison ----------------------------------------------------------------------------------
+def compare_replays(c, g, o, report=None):
+    """Asserts parity of a GPU replay ``g`` with an oracle replay ``o``; returns the error report."""
+    rep = {} if report is None else report
+    M = len(o["out"])
+    assert g["tF"] == o["tF"] and g["tB"] == o["tB"], "version stamps differ"
+    assert g["delta"] == o["delta"]
+    assert len(g["G"]) == len(o["G"]), "number of updates differs"
+    t_act, t_grad = tol(c, "act"), tol(c, "grad")
+    worst = dict(out=0.0, grad_in=0.0, G=0.0, theta=0.0, m=0.0, v=0.0)
+    for i in range(M):
+        if o["out"][i] is not None:
+            e = rel_err(np.atleast_1d(g["out"][i]), np.atleast_1d(o["out"][i]))
+            worst["out"] = max(worst["out"], e)
+            assert e <= t_act, f"output of micro-batch {i}: {e:.3e}"
+        if o["grad_in"][i] is not None:
+            e = rel_err(g["grad_in"][i], o["grad_in"][i])
+            worst["grad_in"] = max(worst["grad_in"], e)
+            assert e <= t_grad, f"input gradient of micro-batch {i}: {e:.3e}"
+    names = [n for n, _, _ in inputs.param_specs(c)]
+    lr, b1, b2 = c["lr"], c["beta1"], c["beta2"]
+    masked_any = {n: None for n in names}
+    gerr_max = {n: 0.0 for n in names}
+    n_masked = 0
+    n_total = 0
+    budget = 0.0
+    for s in range(len(o["G"])):
+        budget += 2.0 * lr * oadamw.direction_bound(s + 1, b1, b2)
+        for n in names:
+            gg, og = g["G"][s][n], o["G"][s][n]
+            e = rel_err(gg, og)
+            worst["G"] = max(worst["G"], e)
+            assert e <= t_grad, f"G[{n}] before update {s + 1}: {e:.3e}"
+            gerr_max[n] = max(gerr_max[n], float(np.abs(gg - og).max()))
+            for key in ("m", "v"):
+                e = rel_err(g[key][s][n], o[key][s][n])
+                worst[key] = max(worst[key], e)
+                assert e <= t_grad, f"{key}[{n}] after update {s + 1}: {e:.3e}"
+            vhat = o["v"][s][n] / (1.0 - b2 ** (s + 1))
+            amb = np.sqrt(vhat) < KAPPA * gerr_max[n]
+            masked_any[n] = amb if masked_any[n] is None else (masked_any[n] | amb)
+            th_g, th_o = g["theta"][s][n], o["theta"][s][n]
+            keep = ~masked_any[n]
+            den = np.abs(th_o).max()
+            if keep.any():
+                e = float(np.abs(th_g - th_o)[keep].max() / den) if den > 0 else float(np.abs(th_g - th_o)[keep].max())
+                worst["theta"] = max(worst["theta"], e)
+                assert e <= t_grad, f"theta[{n}] after update {s + 1}: {e:.3e}"
+            if masked_any[n].any():
+                dev = np.abs(th_g - th_o)[masked_any[n]].max()
+                assert dev <= budget + t_grad * den, f"theta[{n}] invalid at an ambiguous element: {dev:.3e}"
+            n_masked += int(masked_any[n].sum())
+            n_total += masked_any[n].size
+    rep.update(worst)
+    rep["ambiguous_fraction"] = n_masked / max(n_total, 1)
+    return rep

@@ -1,0 +1,149 @@
+"""GPU parity of the PACI stage against the oracle, through the C ABI only."""
+import numpy as np
+import pytest
+
+from parity import (Inputs, compare_replays, gpu_replay, oracle_replay, rel_err, small_cfg, to_host, to_torch,
+                    tol, unflatten)
+from oracle import schedule as osched
+from oracle import stage as ostage
+from paper_2606_07881_amd import configs, inputs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def binding():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    from paper_2606_07881_amd import binding as b
+    return b
+
+
+def _one_event_pair(binding, c, seed=0):
+    """F_0 then B_0 at version 0; returns GPU and oracle (out, grad_in, G)."""
+    import torch
+    inp = Inputs(c, seed, 1)
+    st = binding.Stage(c, K=2, delay=1)
+    st.load_params(inp.params)
+    T, d = c["micro_batch"] * c["seq"], c["d_model"]
+    x = to_torch(inp.x_dev[0])
+    tg = to_torch(inp.tgt[0]) if c["kind"] == "last" else None
+    out = torch.zeros(1, dtype=torch.float32, device="cuda") if c["kind"] == "last" else \
+        torch.zeros(T, d, dtype=st.act_dtype, device="cuda")
+    assert st.forward(0, x, out, tg) == 0
+    go = None if c["kind"] == "last" else to_torch(inp.dy_dev[0])
+    gi = None if c["kind"] == "first" else torch.zeros(T, d, dtype=st.act_dtype, device="cuda")
+    v, due = st.backward(0, go, gi)
+    assert v == 0 and not due
+    G = unflatten(c, st.read(binding.GRADS))
+    st.sync()
+    g_out = to_host(out)
+    g_in = None if gi is None else to_host(gi)
+    st.close()
+    theta = inp.oracle_params()
+    o_out, saved = ostage.stage_fwd(c, theta, inp.x[0], inp.tgt[0] if c["kind"] == "last" else None)
+    o_in, o_G = ostage.stage_bwd(c, theta, saved, None if c["kind"] == "last" else inp.dy[0], 2,
+                                 ids=inp.x[0] if c["kind"] == "first" else None)
+    return (g_out, g_in, G), (o_out, o_in, o_G)
+
+
+@pytest.mark.parametrize("name", ["tiny_fp32", "ragged_bf16", "ragged_fp32", "dh128_bf16", "dh32_bf16", "dh64_fp32",
+                                  "first_bf16", "last_bf16", "first_fp32", "last_fp32"])
+def test_first_forward_backward(binding, name):
+    c = configs.get("tiny_fp32") if name == "tiny_fp32" else small_cfg(name)
+    (g_out, g_in, G), (o_out, o_in, o_G) = _one_event_pair(binding, c)
+    e = rel_err(np.atleast_1d(g_out).ravel(), np.atleast_1d(o_out).ravel())
+    print(f"{name}: out {e:.2e}", flush=True)
+    assert e <= tol(c, "act")
+    if o_in is not None:
+        e = rel_err(g_in, o_in)
+        print(f"{name}: grad_in {e:.2e}", flush=True)
+        assert e <= tol(c, "grad")
+    worst = max(rel_err(G[n], o_G[n]) for n in o_G)
+    print(f"{name}: worst G {worst:.2e}", flush=True)
+    for n in o_G:
+        assert rel_err(G[n], o_G[n]) <= tol(c, "grad"), n
+
+
+@pytest.mark.parametrize("name", ["tiny_fp32", "ragged_bf16", "ragged_fp32", "dh128_bf16", "dh32_bf16",
+                                  "first_bf16", "last_bf16", "first_fp32", "last_fp32"])
+def test_replay_parity(binding, name):
+    """The whole asynchronous 1F1B replay: stamps bit-exact, every output, input
+    gradient, accumulated G and the state after every AdamW update."""
+    c = configs.get("tiny_fp32") if name == "tiny_fp32" else small_cfg(name)
+    inp = Inputs(c, 1, c["M"])
+    g = gpu_replay(c, inp)
+    o = oracle_replay(c, inp)
+    rep = compare_replays(c, g, o)
+    print(name, {k: (f"{v:.2e}" if isinstance(v, float) else v) for k, v in rep.items()}, flush=True)
+    assert g["counters"]["version"] == c["M"] // c["K"]
+
+
+def test_stage_run_equals_event_calls(binding):
+    """paci_stage_run (the schedule driver) against the same events issued one by one."""
+    import torch
+    c = small_cfg("ragged_bf16")
+    inp = Inputs(c, 2, c["M"])
+    g = gpu_replay(c, inp)
+    T, d, M = c["micro_batch"] * c["seq"], c["d_model"], c["M"]
+    st = binding.Stage(c)
+    st.load_params(inp.params)
+    x_all = torch.stack([to_torch(a) for a in inp.x_dev])
+    dy_all = torch.stack([to_torch(a) for a in inp.dy_dev])
+    out_all = torch.zeros(M, T, d, dtype=st.act_dtype, device="cuda")
+    gin_all = torch.zeros(M, T, d, dtype=st.act_dtype, device="cuda")
+    stamps = st.run(M, x_all, dy_all, out_all, gin_all)
+    st.sync()
+    tF, tB, dl = osched.closed_form_stamps(M, c["K"], c["delay"])
+    assert stamps[:, 0].tolist() == tF and stamps[:, 1].tolist() == tB and stamps[:, 2].tolist() == dl
+    for i in range(M):
+        assert rel_err(to_host(out_all[i]), g["out"][i]) <= 1e-2
+        assert rel_err(to_host(gin_all[i]), g["grad_in"][i]) <= 1e-2
+    theta = unflatten(c, st.read(binding.PARAMS))
+    for n in theta:
+        assert np.abs(theta[n] - g["theta"][-1][n]).max() <= 2 * c["lr"] * (M // c["K"]) + 1e-6
+    # a second replay needs fresh counters
+    with pytest.raises(binding.PaciError) as ei:
+        st.run(M, x_all, dy_all)
+    assert ei.value.code == binding.E_ORDER
+    st.reset_counters()
+    st.run(M, x_all, dy_all)
+    st.sync()
+    assert st.counters()["version"] == M // c["K"]
+    st.close()
+
+
+def test_protocol_errors_leave_state_unchanged(binding):
+    import torch
+    c = small_cfg("dh32_bf16")
+    inp = Inputs(c, 3, 4)
+    T, d = c["micro_batch"] * c["seq"], c["d_model"]
+    st = binding.Stage(c, K=2, delay=1)
+    st.load_params(inp.params)
+    xs = [to_torch(a) for a in inp.x_dev]
+    dys = [to_torch(a) for a in inp.dy_dev]
+    outs = [torch.zeros(T, d, dtype=st.act_dtype, device="cuda") for _ in range(4)]
+    assert st.try_forward(1, xs[1], outs[1]) == binding.E_ORDER
+    assert st.try_backward(0, dys[0]) == binding.E_ORDER
+    assert st.try_step() == binding.E_NOT_DUE
+    st.forward(0, xs[0], outs[0])
+    st.forward(1, xs[1], outs[1])
+    sentinel = torch.full((T, d), 7.0, dtype=st.act_dtype, device="cuda")
+    outs[2].copy_(sentinel)
+    before = st.counters()
+    assert st.try_forward(2, xs[2], outs[2]) == binding.E_BACKPRESSURE
+    assert st.counters() == before
+    st.sync()
+    assert torch.equal(outs[2], sentinel)          # no device work was enqueued
+    assert st.backward(0, dys[0]) == (0, False)
+    st.forward(2, xs[2], outs[2])
+    assert st.backward(1, dys[1]) == (0, True)
+    assert st.try_forward(3, xs[3], outs[3]) == binding.E_STEP_PENDING
+    assert st.try_backward(2, dys[2]) == binding.E_STEP_PENDING
+    assert st.step() == 1
+    assert st.counters()["c"] == 0
+    # null pointers are refused
+    assert st.try_forward(3, None, outs[3]) == binding.E_INVAL
+    assert st.try_backward(2, None) == binding.E_INVAL
+    st.close()
