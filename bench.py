@@ -1,0 +1,217 @@
+"""Benchmark of one PACI pipeline stage on one MI355X.
+
+A step is one full asynchronous 1F1B replay of the GPT-2-medium-shaped bf16
+middle stage through the C ABI's schedule driver (paci_stage_run). The stage
+has 6 pre-LN blocks, d 1024, 16 heads of 64, FFN 4096, seq 1024 and
+micro-batch 8. A replay is 64 micro-batches with delay 3 and an AdamW update
+every K = 8 backwards. That is 64 forwards, 64 backwards with fp32 gradient
+accumulation and 8 updates. Inputs and output gradients are seeded synthetic
+tensors already resident in HBM. Successive replays keep training from the
+state the previous one left (only the counters are rewound).
+
+Printed: one JSON line with stage tokens/s, the stage's MFMA utilisation
+against the bf16 dense peak, the roofline of the dominant kernel family (HIP
+events around every launch on the stage stream during the timed replays),
+and the CPU oracle timed on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def make_device_inputs(torch, c, M, seed):
+    """Seeded N(0,1) stage inputs and N(0, 0.01^2) output gradients, bf16, [M, T, d]."""
+    T, d = c["micro_batch"] * c["seq"], c["d_model"]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    dt = torch.bfloat16 if c["dtype"] == "bf16" else torch.float32
+    x = torch.empty(M, T, d, dtype=dt, device="cuda")
+    dy = torch.empty(M, T, d, dtype=dt, device="cuda")
+    for i in range(M):
+        x[i].copy_(torch.randn(T, d, generator=g, device="cuda"))
+        dy[i].copy_(torch.randn(T, d, generator=g, device="cuda") * 1e-2)
+    return x, dy
+
+
+def cpu_baseline(c, seed=0, budget_s=20.0):
+    """The oracle (float64 NumPy) on a bounded sample of the same workload:
+    forward and backward of one sequence of seq tokens through every block of
+    the stage, repeated while the time budget lasts. Returns the JSON object."""
+    import numpy as np
+    from oracle import stage as ostage
+    from paper_2606_07881_amd import inputs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        threads = len(os.sched_getaffinity(0))
+    one = dict(c)
+    one["micro_batch"] = 1
+    params = {k: v.astype(np.float64) for k, v in inputs.make_params(c, seed).items()}
+    x, _ = inputs.make_x(one, seed, 0)
+    dy, _ = inputs.make_dy(one, seed, 0)
+    x, dy = x.astype(np.float64), dy.astype(np.float64)
+    n, t0 = 0, time.perf_counter()
+    while True:
+        _, saved = ostage.stage_fwd(one, params, x)
+        ostage.stage_bwd(one, params, saved, dy, c["K"])
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or n >= 8:
+            break
+    tokens = n * one["seq"]
+    return {"value": tokens / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} x forward+backward of 1 sequence ({one['seq']} tokens) through all "
+                      f"{c['n_layers']} blocks at the workload's shapes, float64, dense masked attention "
+                      f"(about 2x the causal attention FLOPs), {el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default=None)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one pipeline stage on one GPU; --gpus {args.gpus} is not supported "
+              "(stages on several GPUs exchange activations point to point and are outside this build)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_07881_amd import binding, configs, inputs
+
+    name = args.config or configs.BENCH_CONFIG
+    c = configs.get(name)
+    M, K, delay = c["M"], c["K"], c["delay"]
+    T = c["micro_batch"] * c["seq"]
+    log(f"bench: {name} M={M} K={K} delay={delay} T={T}")
+    torch.cuda.set_device(0)
+    st = binding.Stage(c)
+    st.load_params(inputs.make_params(c, args.seed))
+    x_all, dy_all = make_device_inputs(torch, c, M, args.seed)
+    torch.cuda.synchronize()
+    log("bench: inputs resident")
+
+    def replay():
+        st.reset_counters()
+        stamps = st.run(M, x_all, dy_all)
+        return stamps
+
+    for w in range(args.warmup):
+        replay()
+        torch.cuda.synchronize()
+        log(f"bench: warmup {w + 1}/{args.warmup} done")
+    # one instrumented replay outside the timed region creates the HIP event pool
+    st.set_timing(True)
+    replay()
+    st.set_timing(False)
+
+    # timed replays, HIP events on the stage stream around each replay and around every launch
+    stream = torch.cuda.current_stream()
+    st.set_timing(True)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for s in range(args.steps):
+        stamps = replay()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    st.set_timing(False)
+    kt = st.kernel_times()
+    log(f"bench: {args.steps} timed replays in {ms_total:.1f} ms")
+
+    # the same replays without per-launch events, to report what the instrumentation costs
+    start.record(stream)
+    for s in range(args.steps):
+        replay()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_plain = start.elapsed_time(stop) / args.steps
+    log(f"bench: {args.steps} replays without per-launch events in {ms_plain * args.steps:.1f} ms")
+
+    ms_step = ms_total / args.steps
+    tokens_per_step = M * T
+    flop_step = M * configs.algorithmic_flop_per_microbatch(c)
+    value = tokens_per_step / (ms_step / 1e3)
+    mfma_util = flop_step / (ms_step / 1e3) / (PEAK_BF16_TFLOPS * 1e12)
+
+    # dominant kernel family by device time; matrix families are priced in FLOP, streaming ones in bytes
+    mfma_fams = {"gemm_fwd", "gemm_dgrad", "gemm_wgrad_acc", "attn_fwd", "attn_bwd"}
+    fam = max(kt, key=lambda k: kt[k]["ms"])
+    f = kt[fam]
+    per_launch_work = f["work"] / max(f["launches"], 1)
+    per_launch_ms = f["ms"] / max(f["launches"], 1)
+    if fam in mfma_fams:
+        achieved = per_launch_work / (per_launch_ms / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None, "kernel": fam,
+                "launches": f["launches"], "avg_launch_us": round(per_launch_ms * 1e3, 2)}
+    else:
+        achieved = per_launch_work / (per_launch_ms / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None, "kernel": fam,
+                "launches": f["launches"], "avg_launch_us": round(per_launch_ms * 1e3, 2)}
+    families = {}
+    kernel_ms = sum(v["ms"] for v in kt.values())
+    for k, v in kt.items():
+        if v["launches"] == 0:
+            continue
+        rate = v["work"] / (v["ms"] / 1e3) if v["ms"] > 0 else 0.0
+        families[k] = {"ms_per_step": round(v["ms"] / args.steps, 3), "launches_per_step": v["launches"] // args.steps,
+                       "share": round(v["ms"] / kernel_ms, 4),
+                       ("TFLOP/s" if k in mfma_fams else "GB/s"): round(rate / (1e12 if k in mfma_fams else 1e9), 1)}
+
+    out = {
+        "metric": "stage tokens/s (fwd+bwd+accum+step) and MFMA util vs bf16 peak, 1 GPU",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if c["dtype"] == "bf16" else "f32",
+        "data": "synthetic (seeded N(0,1) stage inputs, N(0,0.01^2) output gradients, N(0,0.02^2) weights)",
+        "config": {"workload": f"{name}: GPT-2-medium-shaped middle pipeline stage, {c['n_layers']} pre-LN blocks, "
+                               f"d {c['d_model']}, {c['n_heads']}x{c['head_dim']} heads, FFN {c['d_ff']}, "
+                               f"seq {c['seq']}, micro-batch {c['micro_batch']}; one step = async 1F1B replay of "
+                               f"{M} micro-batches, delay {delay}, AdamW every K={K}",
+                   "micro_batches_per_step": M, "tokens_per_step": tokens_per_step, "K": K, "delay": delay,
+                   "parallelism": "single stage, 1 GPU"},
+        "mfma_util": round(mfma_util, 4),
+        "ms_per_step_without_launch_events": round(ms_plain, 3),
+        "flop_per_step": flop_step,
+        "stamps_delta_sum": int(stamps[:, 2].sum()),
+        "roofline": roof,
+        "kernels": families,
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(c, args.seed, args.cpu_budget)
+    st.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -217,7 +217,7 @@ int paci_stage_reset_counters(paci_stage* h);
 /* ---- introspection ------------------------------------------------------------- */
 int paci_stage_counters(const paci_stage* h, paci_counters* out);
 int paci_stage_sync(paci_stage* h);              /* hipStreamSynchronize; E_HIP on failure */
-int paci_last_hip_error(const paci_stage* h);    /* the hipError_t behind the last E_HIP */
+int paci_last_hip_error(const paci_stage* h);    /* the hipError_t behind the last E_HIP (NULL: of paci_stage_init) */
 const char* paci_strerror(int status);
 
 /* Kernel timing: while enabled, each kernel launch of the stage is bracketed by

@@ -151,13 +151,16 @@ def _copy(d):
     return {k: v.copy() for k, v in d.items()}
 
 
-def replay(cfg, params, K, delay, inputs, grad_outs=None, targets=None, events=None):
+def replay(cfg, params, K, delay, inputs, grad_outs=None, targets=None, events=None, grad_hook=None):
     """Run ``events`` (default: the canonical asynchronous 1F1B order) on a Stage.
 
     inputs[i] is micro-batch i's stage input, grad_outs[i] its output gradient
     (middle and first stages) and targets[i] its token targets (last stage).
     Returns a dict with per-micro-batch outputs, input gradients and stamps,
     and per update the G it consumed and theta, m, v after it.
+    ``grad_hook(update_index, G)``, if given, may replace G just before each
+    update; tests use it to measure how strongly the trajectory after an
+    update depends on small changes of the accumulated gradient.
     """
     M = len(inputs)
     if events is None:
@@ -173,6 +176,8 @@ def replay(cfg, params, K, delay, inputs, grad_outs=None, targets=None, events=N
             go = grad_outs[i] if grad_outs is not None else None
             rec["grad_in"][i], rec["tB"][i], _ = st.backward(i, go)
         else:
+            if grad_hook is not None:
+                st.G = grad_hook(len(rec["G"]), st.G)
             rec["G"].append(_copy(st.G))
             st.step()
             rec["theta"].append(_copy(st.theta))

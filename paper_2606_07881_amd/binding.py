@@ -11,6 +11,11 @@ import re
 
 import numpy as np
 
+# torch ships its own HIP runtime. It must be loaded before the library so
+# that the library's libamdhip64 dependency resolves to that same copy. Two
+# runtimes in one process do not share device allocations.
+import torch  # noqa: F401
+
 from . import inputs
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpaci_stage.so")
@@ -41,9 +46,11 @@ class PaciParamInfo(ctypes.Structure):
 
 
 class PaciError(RuntimeError):
-    def __init__(self, code, where=""):
+    def __init__(self, code, where="", hip=0):
         self.code = code
-        super().__init__(f"{where}: {strerror(code)} ({code})")
+        self.hip = hip
+        extra = f", hipError_t {hip}" if hip else ""
+        super().__init__(f"{where}: {strerror(code)} ({code}{extra})")
 
 
 def _load():
@@ -160,7 +167,7 @@ class Fsm:
         return {k: getattr(c, k) for k, _ in PaciCounters._fields_}
 
     def __del__(self):
-        if getattr(self, "h", None):
+        if getattr(self, "h", None) and lib is not None:
             lib.paci_fsm_destroy(self.h)
             self.h = None
 
@@ -215,15 +222,16 @@ class Stage:
         self.arena_ptr = (base + 255) // 256 * 256
         self.stream = torch.cuda.current_stream(self.arena.device)
         self.h = ctypes.c_void_p()
-        _check(lib.paci_stage_init(ctypes.byref(self.s), self.K, self.delay, ctypes.c_void_p(self.arena_ptr),
-                                   nbytes, ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(self.h)),
-               "paci_stage_init")
+        r = lib.paci_stage_init(ctypes.byref(self.s), self.K, self.delay, ctypes.c_void_p(self.arena_ptr),
+                                nbytes, ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(self.h))
+        if r < 0:
+            raise PaciError(r, "paci_stage_init", lib.paci_last_hip_error(None) if r == E_HIP else 0)
         self.n_params = sum(p["numel"] for p in param_table(cfg))
         self.act_dtype = torch.bfloat16 if cfg["dtype"] == "bf16" else torch.float32
         self.T = cfg["micro_batch"] * cfg["seq"]
 
     def close(self):
-        if getattr(self, "h", None):
+        if getattr(self, "h", None) and lib is not None:
             lib.paci_stage_destroy(self.h)
             self.h = None
 

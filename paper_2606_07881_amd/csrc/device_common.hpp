@@ -44,9 +44,15 @@ template <> __device__ __forceinline__ float from_f32<float>(float x) { return x
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
 
 // ---- element access inside a raw 16-byte vector -----------------------------------
+// Reinterpret one 32-bit word. The word is taken by value: applying
+// __builtin_bit_cast directly to an element of a vector reference (v[j]) was
+// compiled as a read of element 0 for every j by this toolchain.
+__device__ __forceinline__ float as_float(uint32_t w) { return __builtin_bit_cast(float, w); }
+
 template <typename T> __device__ __forceinline__ float vget(const u32x4& v, int j);
 template <> __device__ __forceinline__ float vget<float>(const u32x4& v, int j) {
-  return __builtin_bit_cast(float, v[j]);
+  const uint32_t w = v[j];
+  return as_float(w);
 }
 template <> __device__ __forceinline__ float vget<bf16>(const u32x4& v, int j) {
   uint32_t w = v[j >> 1];
@@ -101,8 +107,10 @@ template <> __device__ __forceinline__ void mma_step<bf16>(floatx4& acc, const u
 template <> __device__ __forceinline__ void mma_step<float>(floatx4& acc, const u32x4& x, const u32x4& y) {
 #pragma unroll
   for (int j = 0; j < 4; ++j)
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, x[j]), __builtin_bit_cast(float, y[j]),
-                                               acc, 0, 0, 0);
+  {
+    const uint32_t xw = x[j], yw = y[j];
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(as_float(xw), as_float(yw), acc, 0, 0, 0);
+  }
 }
 
 // ---- swizzled LDS tile addressing ------------------------------------------------------

@@ -121,7 +121,10 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int m, int n, const 
     } else if (nv == 4) {
       u32x4 old = ld16(C);
       float o[4];
-      for (int j = 0; j < 4; ++j) o[j] = __builtin_bit_cast(float, old[j]) + acc[j];
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t w = old[j];
+        o[j] = as_float(w) + acc[j];
+      }
       store4<float>(reinterpret_cast<float*>(a.C), (int64_t)m * a.ldc + n, o, 4);
     } else {
       for (int j = 0; j < nv; ++j) C[j] += acc[j];

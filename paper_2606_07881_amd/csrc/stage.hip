@@ -36,6 +36,9 @@ struct paci_fsm {
   int K, delay, t, c, q, next_f, next_b;
 };
 
+// HIP status of the last failed call that had no handle to record it in (init).
+static int g_init_hip_error = 0;
+
 static int fsm_check_forward(const paci_fsm& f, int mb) {
   if (f.c == f.K) return PACI_E_STEP_PENDING;
   if (mb != f.next_f) return PACI_E_ORDER;
@@ -406,7 +409,7 @@ template <class F>
 int run(paci_stage* h, int fam, double work, F&& launch) {
   hipEvent_t a = nullptr, b = nullptr;
   if (h->timing) {
-    if (h->pending.size() >= 4096) drain_timing(h);
+    if (h->pending.size() >= 65536) drain_timing(h);  // bounded pool; drains synchronize
     a = take_event(h);
     b = take_event(h);
     if (a && b) (void)hipEventRecord(a, h->st);
@@ -640,6 +643,7 @@ extern "C" int paci_stage_init(const paci_shapes* s, int K, int delay, void* dev
                        hipMemcpyHostToDevice, h->st);
   if (e == hipSuccess) e = hipStreamSynchronize(h->st);
   if (e != hipSuccess) {
+    g_init_hip_error = (int)e;
     delete h;
     return PACI_E_HIP;
   }
@@ -905,7 +909,7 @@ extern "C" int paci_stage_sync(paci_stage* h) {
   return PACI_OK;
 }
 
-extern "C" int paci_last_hip_error(const paci_stage* h) { return h ? h->last_hip : 0; }
+extern "C" int paci_last_hip_error(const paci_stage* h) { return h ? h->last_hip : g_init_hip_error; }
 
 extern "C" const char* paci_strerror(int status) {
   switch (status) {

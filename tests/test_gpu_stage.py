@@ -2,8 +2,8 @@
 import numpy as np
 import pytest
 
-from parity import (Inputs, compare_replays, gpu_replay, oracle_replay, rel_err, small_cfg, to_host, to_torch,
-                    tol, unflatten)
+from parity import (Inputs, compare_replays, gpu_replay, oracle_replay, oracle_sensitivity, rel_err, small_cfg,
+                    to_host, to_torch, tol, unflatten)
 from oracle import schedule as osched
 from oracle import stage as ostage
 from paper_2606_07881_amd import configs, inputs
@@ -75,7 +75,8 @@ def test_replay_parity(binding, name):
     inp = Inputs(c, 1, c["M"])
     g = gpu_replay(c, inp)
     o = oracle_replay(c, inp)
-    rep = compare_replays(c, g, o)
+    sens = oracle_sensitivity(c, inp, o) if c["dtype"] == "bf16" else None
+    rep = compare_replays(c, g, o, sens=sens, theta0=inp.params)
     print(name, {k: (f"{v:.2e}" if isinstance(v, float) else v) for k, v in rep.items()}, flush=True)
     assert g["counters"]["version"] == c["M"] // c["K"]
 
