@@ -159,8 +159,9 @@ def replay(cfg, params, K, delay, inputs, grad_outs=None, targets=None, events=N
     Returns a dict with per-micro-batch outputs, input gradients and stamps,
     and per update the G it consumed and theta, m, v after it.
     ``grad_hook(update_index, G)``, if given, may replace G just before each
-    update; tests use it to measure how strongly the trajectory after an
-    update depends on small changes of the accumulated gradient.
+    update (the recorded G is the one before the hook); tests use it to
+    measure how strongly the trajectory after an update depends on small
+    changes of the accumulated gradient.
     """
     M = len(inputs)
     if events is None:
@@ -176,9 +177,9 @@ def replay(cfg, params, K, delay, inputs, grad_outs=None, targets=None, events=N
             go = grad_outs[i] if grad_outs is not None else None
             rec["grad_in"][i], rec["tB"][i], _ = st.backward(i, go)
         else:
-            if grad_hook is not None:
-                st.G = grad_hook(len(rec["G"]), st.G)
             rec["G"].append(_copy(st.G))
+            if grad_hook is not None:
+                st.G = grad_hook(len(rec["G"]) - 1, st.G)
             st.step()
             rec["theta"].append(_copy(st.theta))
             rec["m"].append(_copy(st.m))

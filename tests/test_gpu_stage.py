@@ -75,7 +75,7 @@ def test_replay_parity(binding, name):
     inp = Inputs(c, 1, c["M"])
     g = gpu_replay(c, inp)
     o = oracle_replay(c, inp)
-    sens = oracle_sensitivity(c, inp, o) if c["dtype"] == "bf16" else None
+    sens = oracle_sensitivity(c, inp, o)
     rep = compare_replays(c, g, o, sens=sens, theta0=inp.params)
     print(name, {k: (f"{v:.2e}" if isinstance(v, float) else v) for k, v in rep.items()}, flush=True)
     assert g["counters"]["version"] == c["M"] // c["K"]
