@@ -88,6 +88,9 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="first copy a 256 MiB device buffer 3 times (a kernel of known traffic, for scaling "
+                         "hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one pipeline stage on one GPU; --gpus {args.gpus} is not supported "
@@ -109,6 +112,14 @@ def main():
     x_all, dy_all = make_device_inputs(torch, c, M, args.seed)
     torch.cuda.synchronize()
     log("bench: inputs resident")
+    if args.copy_probe:
+        src = torch.ones(64 * 2 ** 20, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log("bench: copy probe done (3 x 256 MiB device-to-device)")
 
     def replay():
         st.reset_counters()

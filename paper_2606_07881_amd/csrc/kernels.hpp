@@ -54,16 +54,14 @@ hipError_t attn_bwd(DType dt, const void* qkv, const void* o, const void* dO, co
 hipError_t layernorm_fwd(DType dt, const void* x, void* n, float* mean, float* rstd, const float* gamma,
                          const float* beta, void* xcopy, int rows, int d, float eps, hipStream_t st);
 // dx = res + rstd * (g - mean(g) - xhat * mean(g * xhat)), g = dn * gamma (res optional);
-// Ggamma += sum_rows dn * xhat, Gbeta += sum_rows dn (through `part`, >= ln_bwd_part_floats).
+// Ggamma += sum_rows dn * xhat, Gbeta += sum_rows dn (fp32 atomics).
 hipError_t layernorm_bwd(DType dt, const void* dn, const void* x, const float* mean, const float* rstd,
-                         const float* gamma, const void* res, void* dx, float* Ggamma, float* Gbeta,
-                         float* part, int rows, int d, hipStream_t st);
-int64_t ln_bwd_part_floats(int rows, int d);
+                         const float* gamma, const void* res, void* dx, float* Ggamma, float* Gbeta, int rows, int d,
+                         hipStream_t st);
 
 // ---- column sums accumulated into fp32 (bias gradients) ---------------------------------
-// G[c] += sum_r Y[r*ld + c], c < ncols; `part` needs colsum_part_floats floats.
-hipError_t colsum_acc(DType dt, const void* Y, int64_t ld, int rows, int ncols, float* G, float* part, hipStream_t st);
-int64_t colsum_part_floats(int rows, int ncols);
+// G[c] += sum_r Y[r*ld + c], c < ncols (fp32 atomics).
+hipError_t colsum_acc(DType dt, const void* Y, int64_t ld, int rows, int ncols, float* G, hipStream_t st);
 
 // ---- first stage: token + position embedding ----------------------------------------------
 // x[b*S + s] = wte[ids[b*S + s]] + wpe[s] (fp32 tables, x in the stage dtype).

@@ -4,10 +4,10 @@
 // LayerNorm uses one wavefront per row. The row is held in registers as
 // 16-byte vectors (lane i owns vectors i, i + 64, ...), so each element is
 // read once. Mean and variance are two-pass in fp32 with wavefront
-// reductions. The backward also produces per-column partial sums of
-// dn * xhat and dn over the rows of its workgroup. A second small kernel
-// adds the partial rows into the fp32 gradient accumulator. The sum order is
-// fixed, so results are reproducible run to run.
+// reductions. The affine gradients (sum of dn * xhat and of dn over rows) and
+// the bias gradients are column reductions. A grid of (column slice, 64-row
+// slice) workgroups streams the rows coalesced and adds its partial sums into
+// the fp32 accumulator with atomics. The summation order is therefore free.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -15,8 +15,6 @@ namespace paci {
 namespace {
 
 constexpr int NT = 256;
-constexpr int LN_ROWS_PER_BLOCK = 32;   // backward: rows per workgroup (8 per wavefront)
-constexpr int CS_ROWS_PER_BLOCK = 64;   // column sums: rows per workgroup
 
 template <typename T> __device__ __forceinline__ u32x4 pack_vec(const float* f);
 template <> __device__ __forceinline__ u32x4 pack_vec<float>(const float* f) {
@@ -83,130 +81,128 @@ __global__ void __launch_bounds__(NT) ln_fwd_kernel(const T* __restrict__ x, T* 
 }
 
 // ------------------------------------------------------------------------------------------
-// Each wavefront handles rows w, w+4, ... of the block's LN_ROWS_PER_BLOCK rows;
-// partial column sums of the 4 wavefronts are combined through LDS and the
-// block writes one partial row of dgamma and one of dbeta.
+// dx for one row per wavefront (the affine gradients are a separate column pass).
 template <typename T, int MAXV>
 __global__ void __launch_bounds__(NT) ln_bwd_kernel(const T* __restrict__ dn, const T* __restrict__ x,
                                                      const float* __restrict__ mean, const float* __restrict__ rstd,
-                                                     const float* __restrict__ gamma, const T* res, T* dx,
-                                                     float* part_g, float* part_b, int rows, int d) {
+                                                     const float* __restrict__ gamma, const T* res, T* dx, int rows,
+                                                     int d) {
   constexpr int V = Vec<T>::V;
-  __shared__ float red[2][NT / 64][64 * V];
-  const int w = threadIdx.x >> 6, l = lane_id();
+  const int row = blockIdx.x * (NT / 64) + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int l = lane_id();
   const int nv = d / V;
-  float pg[MAXV][V], pb[MAXV][V];
-#pragma unroll
-  for (int i = 0; i < MAXV; ++i)
-#pragma unroll
-    for (int j = 0; j < V; ++j) pg[i][j] = pb[i][j] = 0.f;
-
-  const int r0 = blockIdx.x * LN_ROWS_PER_BLOCK;
-  for (int rr = w; rr < LN_ROWS_PER_BLOCK; rr += NT / 64) {
-    const int row = r0 + rr;
-    if (row >= rows) break;
-    const float mu = mean[row], rs = rstd[row];
-    const T* dnr = dn + (int64_t)row * d;
-    const T* xr = x + (int64_t)row * d;
-    u32x4 gv[MAXV], xv[MAXV];
-    float sg = 0.f, sgx = 0.f;
-#pragma unroll
-    for (int i = 0; i < MAXV; ++i) {
-      const int vi = l + 64 * i;
-      if (vi < nv) {
-        gv[i] = ld16(dnr + vi * V);
-        xv[i] = ld16(xr + vi * V);
-#pragma unroll
-        for (int j = 0; j < V; ++j) {
-          const int c = vi * V + j;
-          const float g = vget<T>(gv[i], j) * gamma[c];
-          const float xh = (vget<T>(xv[i], j) - mu) * rs;
-          sg += g;
-          sgx += g * xh;
-        }
-      }
-    }
-    const float mg = wave_sum(sg) / d, mgx = wave_sum(sgx) / d;
-#pragma unroll
-    for (int i = 0; i < MAXV; ++i) {
-      const int vi = l + 64 * i;
-      if (vi < nv) {
-        u32x4 rv = {0, 0, 0, 0};
-        if (res) rv = ld16(res + (int64_t)row * d + vi * V);
-        float o[V];
-#pragma unroll
-        for (int j = 0; j < V; ++j) {
-          const int c = vi * V + j;
-          const float dnv = vget<T>(gv[i], j);
-          const float xh = (vget<T>(xv[i], j) - mu) * rs;
-          const float g = dnv * gamma[c];
-          o[j] = rs * (g - mg - xh * mgx) + (res ? vget<T>(rv, j) : 0.f);
-          pg[i][j] += dnv * xh;
-          pb[i][j] += dnv;
-        }
-        st16(dx + (int64_t)row * d + vi * V, pack_vec<T>(o));
-      }
-    }
-  }
-  // combine the 4 wavefronts, one 64*V column slice at a time
+  const float mu = mean[row], rs = rstd[row];
+  const T* dnr = dn + (int64_t)row * d;
+  const T* xr = x + (int64_t)row * d;
+  u32x4 gv[MAXV], xv[MAXV];
+  float sg = 0.f, sgx = 0.f;
 #pragma unroll
   for (int i = 0; i < MAXV; ++i) {
-    __syncthreads();
+    const int vi = l + 64 * i;
+    if (vi < nv) {
+      gv[i] = ld16(dnr + vi * V);
+      xv[i] = ld16(xr + vi * V);
 #pragma unroll
-    for (int j = 0; j < V; ++j) {
-      red[0][w][l * V + j] = pg[i][j];
-      red[1][w][l * V + j] = pb[i][j];
-    }
-    __syncthreads();
-    for (int c = threadIdx.x; c < 64 * V; c += NT) {
-      const int col = i * 64 * V + c;
-      if (col < d) {
-        float a = 0.f, b = 0.f;
-#pragma unroll
-        for (int ww = 0; ww < NT / 64; ++ww) {
-          a += red[0][ww][c];
-          b += red[1][ww][c];
-        }
-        part_g[(int64_t)blockIdx.x * d + col] = a;
-        part_b[(int64_t)blockIdx.x * d + col] = b;
+      for (int j = 0; j < V; ++j) {
+        const int c = vi * V + j;
+        const float g = vget<T>(gv[i], j) * gamma[c];
+        const float xh = (vget<T>(xv[i], j) - mu) * rs;
+        sg += g;
+        sgx += g * xh;
       }
     }
   }
-}
-
-// G[c] += sum over nrows partial rows (row stride ncols); one thread per column.
-__global__ void __launch_bounds__(NT) colreduce_acc_kernel(const float* __restrict__ part, int nrows, int ncols,
-                                                            float* G) {
-  const int c = blockIdx.x * NT + threadIdx.x;
-  if (c >= ncols) return;
-  float s = 0.f;
-  for (int r = 0; r < nrows; ++r) s += part[(int64_t)r * ncols + c];
-  G[c] += s;
-}
-
-// Partial column sums: block (x, y) covers columns [x*NT*V, ...) and rows
-// [y*CS_ROWS_PER_BLOCK, ...); thread t owns one 16-byte column vector.
-template <typename T>
-__global__ void __launch_bounds__(NT) colsum_kernel(const T* __restrict__ Y, int64_t ld, int rows, int ncols,
-                                                     float* part) {
-  constexpr int V = Vec<T>::V;
-  const int cv = blockIdx.x * NT + threadIdx.x;
-  const int c0 = cv * V;
-  if (c0 >= ncols) return;
-  float acc[V];
+  const float mg = wave_sum(sg) / d, mgx = wave_sum(sgx) / d;
 #pragma unroll
-  for (int j = 0; j < V; ++j) acc[j] = 0.f;
-  const int r0 = blockIdx.y * CS_ROWS_PER_BLOCK;
-  const int r1 = min(rows, r0 + CS_ROWS_PER_BLOCK);
-  for (int r = r0; r < r1; ++r) {
-    const u32x4 v = ld16(Y + (int64_t)r * ld + c0);
+  for (int i = 0; i < MAXV; ++i) {
+    const int vi = l + 64 * i;
+    if (vi < nv) {
+      u32x4 rv = {0, 0, 0, 0};
+      if (res) rv = ld16(res + (int64_t)row * d + vi * V);
+      float o[V];
 #pragma unroll
-    for (int j = 0; j < V; ++j) acc[j] += vget<T>(v, j);
+      for (int j = 0; j < V; ++j) {
+        const int c = vi * V + j;
+        const float xh = (vget<T>(xv[i], j) - mu) * rs;
+        const float g = vget<T>(gv[i], j) * gamma[c];
+        o[j] = rs * (g - mg - xh * mgx) + (res ? vget<T>(rv, j) : 0.f);
+      }
+      st16(dx + (int64_t)row * d + vi * V, pack_vec<T>(o));
+    }
   }
-  float* pr = part + (int64_t)blockIdx.y * ncols + c0;
+}
+
+// Column sums accumulated into fp32 with atomics. A workgroup of 256 threads
+// is 8 row groups x 32 column vectors (16 bytes each). It covers
+// 32 * V columns and CS_ROWS = 64 rows. Each thread issues its 8 row loads
+// together, the 8 row groups are combined in LDS, and one thread per column
+// adds the workgroup's sum into G. That is T / 64 atomic adds per column.
+// With AFFINE, the sums are of dy * xhat and dy, where
+// xhat = (x - mean) * rstd (the LayerNorm affine gradients).
+constexpr int CS_THREADS = 256;
+constexpr int CS_COLV = 32;             // column vectors per workgroup
+constexpr int CS_RG = CS_THREADS / CS_COLV;
+constexpr int CS_RPT = 8;               // rows per thread
+constexpr int CS_ROWS = CS_RG * CS_RPT;
+template <typename T, bool AFFINE>
+__global__ void __launch_bounds__(CS_THREADS) colsum_atomic_kernel(const T* __restrict__ Y, int64_t ld, int rows,
+                                                                    int ncols, const T* __restrict__ x,
+                                                                    const float* __restrict__ mean,
+                                                                    const float* __restrict__ rstd, float* G,
+                                                                    float* G2) {
+  constexpr int V = Vec<T>::V;
+  __shared__ float red[AFFINE ? 2 : 1][CS_RG][CS_COLV * V];
+  const int cv = threadIdx.x % CS_COLV, rg = threadIdx.x / CS_COLV;
+  const int c0 = (blockIdx.x * CS_COLV + cv) * V;
+  const bool colok = c0 < ncols;
+  const int r0 = blockIdx.y * CS_ROWS + rg;
+  float a[V], b[V];
 #pragma unroll
-  for (int j = 0; j < V; ++j)
-    if (c0 + j < ncols) pr[j] = acc[j];
+  for (int j = 0; j < V; ++j) a[j] = b[j] = 0.f;
+  u32x4 yv[CS_RPT], xv[CS_RPT];
+#pragma unroll
+  for (int i = 0; i < CS_RPT; ++i) {
+    const int r = r0 + i * CS_RG;
+    const bool ok = colok && r < rows;
+    yv[i] = ok ? ld16(Y + (int64_t)r * ld + c0) : u32x4{0, 0, 0, 0};
+    if (AFFINE) xv[i] = ok ? ld16(x + (int64_t)r * ld + c0) : u32x4{0, 0, 0, 0};
+  }
+#pragma unroll
+  for (int i = 0; i < CS_RPT; ++i) {
+    const int r = r0 + i * CS_RG;
+    if (AFFINE) {
+      const bool ok = r < rows;
+      const float mu = ok ? mean[r] : 0.f, rs = ok ? rstd[r] : 0.f;
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const float g = vget<T>(yv[i], j);
+        a[j] += g * (vget<T>(xv[i], j) - mu) * rs;
+        b[j] += g;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < V; ++j) a[j] += vget<T>(yv[i], j);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    red[0][rg][cv * V + j] = a[j];
+    if (AFFINE) red[AFFINE ? 1 : 0][rg][cv * V + j] = b[j];
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < CS_COLV * V; c += CS_THREADS) {
+    const int col = blockIdx.x * CS_COLV * V + c;
+    if (col >= ncols) continue;
+    float sa = 0.f, sb = 0.f;
+#pragma unroll
+    for (int g = 0; g < CS_RG; ++g) {
+      sa += red[0][g][c];
+      if (AFFINE) sb += red[AFFINE ? 1 : 0][g][c];
+    }
+    atomicAdd(G + col, sa);
+    if (AFFINE) atomicAdd(G2 + col, sb);
+  }
 }
 
 template <typename T, int MAXV>
@@ -219,20 +215,16 @@ hipError_t ln_fwd_launch(const void* x, void* n, float* mean, float* rstd, const
 
 template <typename T, int MAXV>
 hipError_t ln_bwd_launch(const void* dn, const void* x, const float* mean, const float* rstd, const float* gamma,
-                         const void* res, void* dx, float* Gg, float* Gb, float* part, int rows, int d,
-                         hipStream_t st) {
-  const int nb = (rows + LN_ROWS_PER_BLOCK - 1) / LN_ROWS_PER_BLOCK;
-  float* pg = part;
-  float* pb = part + (int64_t)nb * d;
-  hipLaunchKernelGGL((ln_bwd_kernel<T, MAXV>), dim3(nb), dim3(NT), 0, st, reinterpret_cast<const T*>(dn),
+                         const void* res, void* dx, float* Gg, float* Gb, int rows, int d, hipStream_t st) {
+  hipLaunchKernelGGL((ln_bwd_kernel<T, MAXV>), dim3((rows + 3) / 4), dim3(NT), 0, st, reinterpret_cast<const T*>(dn),
                      reinterpret_cast<const T*>(x), mean, rstd, gamma, reinterpret_cast<const T*>(res),
-                     reinterpret_cast<T*>(dx), pg, pb, rows, d);
+                     reinterpret_cast<T*>(dx), rows, d);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(colreduce_acc_kernel, dim3((d + NT - 1) / NT), dim3(NT), 0, st, pg, nb, d, Gg);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(colreduce_acc_kernel, dim3((d + NT - 1) / NT), dim3(NT), 0, st, pb, nb, d, Gb);
+  constexpr int V = Vec<T>::V;
+  const dim3 grid((d / V + CS_COLV - 1) / CS_COLV, (rows + CS_ROWS - 1) / CS_ROWS);
+  hipLaunchKernelGGL((colsum_atomic_kernel<T, true>), grid, dim3(CS_THREADS), 0, st, reinterpret_cast<const T*>(dn),
+                     (int64_t)d, rows, d, reinterpret_cast<const T*>(x), mean, rstd, Gg, Gb);
   return hipGetLastError();
 }
 
@@ -255,12 +247,12 @@ hipError_t ln_fwd_t(const void* x, void* n, float* mean, float* rstd, const floa
 
 template <typename T>
 hipError_t ln_bwd_t(const void* dn, const void* x, const float* mean, const float* rstd, const float* gamma,
-                    const void* res, void* dx, float* Gg, float* Gb, float* part, int rows, int d, hipStream_t st) {
+                    const void* res, void* dx, float* Gg, float* Gb, int rows, int d, hipStream_t st) {
   const int mv = maxv_for<T>(d);
-  if (mv <= 1) return ln_bwd_launch<T, 1>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, part, rows, d, st);
-  if (mv <= 2) return ln_bwd_launch<T, 2>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, part, rows, d, st);
-  if (mv <= 4) return ln_bwd_launch<T, 4>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, part, rows, d, st);
-  if (mv <= 8) return ln_bwd_launch<T, 8>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, part, rows, d, st);
+  if (mv <= 1) return ln_bwd_launch<T, 1>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, rows, d, st);
+  if (mv <= 2) return ln_bwd_launch<T, 2>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, rows, d, st);
+  if (mv <= 4) return ln_bwd_launch<T, 4>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, rows, d, st);
+  if (mv <= 8) return ln_bwd_launch<T, 8>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, rows, d, st);
   return hipErrorInvalidValue;
 }
 
@@ -274,37 +266,24 @@ hipError_t layernorm_fwd(DType dt, const void* x, void* n, float* mean, float* r
 }
 
 hipError_t layernorm_bwd(DType dt, const void* dn, const void* x, const float* mean, const float* rstd,
-                         const float* gamma, const void* res, void* dx, float* Gg, float* Gb, float* part, int rows,
-                         int d, hipStream_t st) {
+                         const float* gamma, const void* res, void* dx, float* Gg, float* Gb, int rows, int d,
+                         hipStream_t st) {
   if (rows <= 0 || d <= 0 || d % 8) return hipErrorInvalidValue;
-  if (dt == DT_BF16) return ln_bwd_t<bf16>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, part, rows, d, st);
-  return ln_bwd_t<float>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, part, rows, d, st);
+  if (dt == DT_BF16) return ln_bwd_t<bf16>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, rows, d, st);
+  return ln_bwd_t<float>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, rows, d, st);
 }
 
-int64_t ln_bwd_part_floats(int rows, int d) {
-  return 2 * (int64_t)((rows + LN_ROWS_PER_BLOCK - 1) / LN_ROWS_PER_BLOCK) * d;
-}
-
-hipError_t colsum_acc(DType dt, const void* Y, int64_t ld, int rows, int ncols, float* G, float* part,
-                      hipStream_t st) {
+hipError_t colsum_acc(DType dt, const void* Y, int64_t ld, int rows, int ncols, float* G, hipStream_t st) {
   if (rows <= 0 || ncols <= 0 || ncols % 8 || ld % 8) return hipErrorInvalidValue;
   const int V = (dt == DT_BF16) ? 8 : 4;
-  const int nrb = (rows + CS_ROWS_PER_BLOCK - 1) / CS_ROWS_PER_BLOCK;
-  dim3 grid((ncols / V + NT - 1) / NT, nrb);
+  const dim3 grid((ncols / V + CS_COLV - 1) / CS_COLV, (rows + CS_ROWS - 1) / CS_ROWS);
   if (dt == DT_BF16)
-    hipLaunchKernelGGL(colsum_kernel<bf16>, grid, dim3(NT), 0, st, reinterpret_cast<const bf16*>(Y), ld, rows, ncols,
-                       part);
+    hipLaunchKernelGGL((colsum_atomic_kernel<bf16, false>), grid, dim3(CS_THREADS), 0, st,
+                       reinterpret_cast<const bf16*>(Y), ld, rows, ncols, nullptr, nullptr, nullptr, G, nullptr);
   else
-    hipLaunchKernelGGL(colsum_kernel<float>, grid, dim3(NT), 0, st, reinterpret_cast<const float*>(Y), ld, rows,
-                       ncols, part);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(colreduce_acc_kernel, dim3((ncols + NT - 1) / NT), dim3(NT), 0, st, part, nrb, ncols, G);
+    hipLaunchKernelGGL((colsum_atomic_kernel<float, false>), grid, dim3(CS_THREADS), 0, st,
+                       reinterpret_cast<const float*>(Y), ld, rows, ncols, nullptr, nullptr, nullptr, G, nullptr);
   return hipGetLastError();
-}
-
-int64_t colsum_part_floats(int rows, int ncols) {
-  return (int64_t)((rows + CS_ROWS_PER_BLOCK - 1) / CS_ROWS_PER_BLOCK) * ncols;
 }
 
 }  // namespace paci

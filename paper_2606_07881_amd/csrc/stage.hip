@@ -316,14 +316,14 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
   L.w_do = a.take(esz * T * d);
   L.w_dqkv = a.take(esz * T * 3 * d);
   L.w_D = a.take(4 * heads_rows);
-  int64_t part = std::max(paci::colsum_part_floats((int)T, (int)std::max(3 * d, f)),
-                          paci::ln_bwd_part_floats((int)T, (int)d));
+  int64_t part = 64;
   if (s.kind == PACI_LAST) {
     part = std::max(part, paci::ce_part_floats((int)T));
     L.w_dz = a.take(esz * T * L.ldz);
     L.w_dnf = a.take(esz * T * d);
   }
   L.w_part = a.take(4 * part);
+  L.w_loss = a.take(256);
   L.total = (a.off + 255) & ~(size_t)255;
   return L;
 }
@@ -465,8 +465,7 @@ int linear_wgrad(paci_stage* h, const void* dY, int64_t ldy, const void* X, int6
 
 int bias_grad(paci_stage* h, const void* Y, int64_t ld, int rows, int ncols, int64_t g_off) {
   return run(h, F_BIAS_GRAD, (double)rows * ncols * h->esz, [&] {
-    return paci::colsum_acc(h->dt, Y, ld, rows, ncols, h->g(g_off), reinterpret_cast<float*>(h->ws(h->L.w_part)),
-                            h->st);
+    return paci::colsum_acc(h->dt, Y, ld, rows, ncols, h->g(g_off), h->st);
   });
 }
 
@@ -481,9 +480,9 @@ int ln_fwd(paci_stage* h, const void* x, void* n, float* mean, float* rstd, int6
 int ln_bwd(paci_stage* h, const void* dn, const void* x, const float* mean, const float* rstd, int64_t g_off,
            int64_t b_off, const void* res, void* dx) {
   const int T = (int)h->L.T, d = h->s.d_model;
-  return run(h, F_LN_BWD, (double)T * d * (res ? 4 : 3) * h->esz + 8.0 * T, [&] {
-    return paci::layernorm_bwd(h->dt, dn, x, mean, rstd, h->th(g_off), res, dx, h->g(g_off), h->g(b_off),
-                               reinterpret_cast<float*>(h->ws(h->L.w_part)), T, d, h->st);
+  return run(h, F_LN_BWD, (double)T * d * (res ? 4 : 3) * h->esz + 8.0 * T, [&] {  // dx pass; the affine pass rereads dn, x
+    return paci::layernorm_bwd(h->dt, dn, x, mean, rstd, h->th(g_off), res, dx, h->g(g_off), h->g(b_off), T, d,
+                               h->st);
   });
 }
 
@@ -851,7 +850,7 @@ extern "C" int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, cons
   const size_t out_stride = s.kind == PACI_LAST ? sizeof(float) : act;
   // scratch outputs when the caller discards them
   char* out_scratch = h->ws(h->L.w_dyB);
-  float* loss_scratch = reinterpret_cast<float*>(h->ws(h->L.w_part));
+  float* loss_scratch = reinterpret_cast<float*>(h->ws(h->L.w_loss));
   std::vector<int32_t> kinds(2 * (size_t)M + M / K + 1), idx(kinds.size());
   int n = 0;
   int r = paci_schedule(M, K, delay, kinds.data(), idx.data(), (int)kinds.size(), &n);

@@ -17,9 +17,10 @@ What is compared, and how:
   and moments it writes equal the AdamW formula applied to the parameters,
   G and moments it read (1e-5);
 * parameters against the oracle after every update: elementwise wherever the
-  Adam direction m_hat / sqrt(v_hat) is well conditioned, i.e. sqrt(v_hat)
-  of the oracle exceeds KAPPA times the largest discrepancy of that element's
-  G seen so far. Elsewhere (the first update moves a weight by about
+  Adam step lr * m_hat / (sqrt(v_hat) + eps) is well conditioned, i.e.
+  sqrt(v_hat) + eps of the oracle exceeds 3 / tol times the largest
+  discrepancy of that element's G seen so far (so that discrepancy moves the
+  step by at most a third of the tolerance). Elsewhere (the first update moves a weight by about
   lr * sign(G), so a tiny G within its tolerance may flip it) several results
   are correct and the element is only checked for validity: within
   2 * lr * (sum of the largest possible Adam steps) of the oracle;
@@ -49,7 +50,6 @@ from oracle import schedule as osched  # noqa: E402
 from oracle import stage as ostage  # noqa: E402
 from paper_2606_07881_amd import configs, inputs  # noqa: E402
 
-KAPPA = 100.0
 SENS_RHO = {"bf16": 2.0 ** -8, "fp32": 2.0 ** -20}   # G perturbation relative to max|G|
 
 
@@ -321,7 +321,7 @@ def compare_replays(c, g, o, sens=None, theta0=None):
                 assert e <= 1e-5, f"AdamW update {s + 1} of {n} differs from the formula on its own state: {e:.3e}"
             # parameters against the oracle
             vhat = o["v"][s][n] / (1.0 - b2 ** (s + 1))
-            amb = np.sqrt(vhat) < KAPPA * gerr[n]
+            amb = np.sqrt(vhat) + c["eps"] < (3.0 / t_grad) * gerr[n]
             masked[n] = amb if masked[n] is None else (masked[n] | amb)
             th_g, th_o = g["theta"][s][n], o["theta"][s][n]
             keep = ~masked[n]
