@@ -125,6 +125,33 @@ template <int ROWS> __device__ __forceinline__ u32x4 lds_frag(const u32x4* tile,
   return tile[lds_slot<ROWS>(kv, row0 + (l & 15))];
 }
 
+// ---- MN-major bf16 tiles read with the LDS transpose instruction ----------------------
+// A bf16 operand stored with its rows (m or n) contiguous and the contracted
+// index k as the outer dimension is staged in LDS as [k][ROWS] (16-byte
+// chunks of 8 rows), with chunk c of line k stored at chunk c ^ ((k & 3) << 1).
+// ds_read_b64_tr_b16 gives each lane j of a 16-lane group 4 values
+// (element i from the 8 bytes addressed by lane 4i + j / 4, position j % 4).
+// If lane c addresses line kb + c / 4, rows r0 + 4 (c % 4) .. + 3, lane j
+// receives rows r0 + j of lines kb .. kb + 3. Two such reads (kb and kb + 4)
+// give the 8 contracted values an MFMA step wants, with no register transpose.
+template <int ROWS> __device__ __forceinline__ int trt_elem(int k, int r) {
+  return k * ROWS + ((((r >> 3) ^ ((k & 3) << 1))) << 3) + (r & 7);
+}
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+template <int ROWS> __device__ __forceinline__ u32x4 lds_frag_tr(const u32x4* tile, int s, int row0) {
+  const int l = lane_id();
+  const int g = l >> 4, c = l & 15;
+  const bf16* base = reinterpret_cast<const bf16*>(tile);
+  const int r = row0 + 4 * (c & 3);
+  const int k0 = s * 32 + 8 * g + (c >> 2);
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4*)(base + trt_elem<ROWS>(k0, r)));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4*)(base + trt_elem<ROWS>(k0 + 4, r)));
+  const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
+  return u32x4{a[0], a[1], b[0], b[1]};
+}
+
 // ---- wave reductions ---------------------------------------------------------------------
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

@@ -6,29 +6,44 @@
 // 16 x 16 tiles. The contracted dimension advances in 8-vector slices (64 bf16 or
 // 32 fp32 elements), double-buffered in LDS: the global loads of slice k+1 are
 // in flight while slice k is multiplied. Operands stored contracted-major
-// (K-major) are copied as 16-byte vectors. Operands stored the other way
-// (MN-major: the weight in dX = dY W, both activations in dW = dY^T X) are
-// loaded as V x V blocks and transposed in registers before the LDS write, so
-// every LDS fragment read is one 16-byte access.
+// (K-major) are copied as 16-byte vectors and read as one 16-byte fragment.
+// For bf16, operands stored the other way (MN-major: the weight in dX = dY W,
+// both activations in dW = dY^T X) are also copied as 16-byte vectors, into a
+// [k][rows] layout read with the gfx950 LDS transpose instruction. fp32
+// MN-major operands are transposed in registers (4 x 4 blocks).
 //
 // Tile order is XCD-aware: workgroup w runs on XCD w % 8, so each XCD gets a
 // contiguous range of tiles, walked in groups of 8 tile-rows to keep A and B
 // panels in that XCD's L2.
 #include "device_common.hpp"
+#include <cmath>
+
 #include "kernels.hpp"
 
 namespace paci {
 namespace {
 
-constexpr int BM = 128, BN = 128, WM = 64, WN = 64, NT = 256, KVN = 8, GROUP_M = 8;
+constexpr int KVN = 8, GROUP_M = 8;
+
+// Tile configuration: a BM x BN output tile per workgroup, WM x WN per wavefront.
+template <int BM_, int BN_, int WM_, int WN_>
+struct Tile {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
+  static constexpr int WAVES = (BM / WM) * (BN / WN);
+  static constexpr int NT = 64 * WAVES;
+};
 
 // Register-staged tile loader (global -> registers -> LDS).
-template <typename T, int ROWS, bool KMAJ>
+// K-major operands and MN-major bf16 operands are copied as 16-byte vectors
+// (MN-major bf16 into the [k][ROWS] transpose-read layout); MN-major fp32
+// operands are loaded as 4 x 4 blocks and transposed in registers.
+template <typename T, int ROWS, bool KMAJ, int NT>
 struct TileLoader {
   static constexpr int V = Vec<T>::V;
-  static constexpr int ITEMS = KMAJ ? ROWS * KVN : (ROWS / V) * KVN;
+  static constexpr bool TR = !KMAJ && sizeof(T) == 2;   // transpose-read layout
+  static constexpr int ITEMS = (KMAJ || TR) ? ROWS * KVN : (ROWS / V) * KVN;
   static constexpr int PT = (ITEMS + NT - 1) / NT;
-  static constexpr int NV = KMAJ ? 1 : V;
+  static constexpr int NV = (KMAJ || TR) ? 1 : V;
   u32x4 r[PT][NV];
 
   // rows [row0, row0+ROWS) of `rows_total`; contracted [k0, k0 + 8V) of k_end.
@@ -38,8 +53,8 @@ struct TileLoader {
     for (int p = 0; p < PT; ++p) {
       const int it = tid + p * NT;
       if ((ITEMS % NT) != 0 && it >= ITEMS) continue;
-      const int kv = it % KVN, rr = it / KVN;
       if (KMAJ) {
+        const int kv = it % KVN, rr = it / KVN;
         const int row = row0 + rr, k = k0 + kv * V;
         u32x4 v = {0, 0, 0, 0};
         if (row < rows_total && k < k_end) {
@@ -47,7 +62,18 @@ struct TileLoader {
           if (k + V > k_end) v = vmask_tail<T>(v, k_end - k);
         }
         r[p][0] = v;
+      } else if (TR) {
+        constexpr int CPL = ROWS / V;             // 16-byte chunks per contracted line
+        const int c = it % CPL, kk = it / CPL;
+        const int k = k0 + kk, rb = row0 + c * V;
+        u32x4 v = {0, 0, 0, 0};
+        if (k < k_end && rb < rows_total) {
+          v = ld16(src + (int64_t)k * ld + rb);
+          if (rb + V > rows_total) v = vmask_tail<T>(v, rows_total - rb);
+        }
+        r[p][0] = v;
       } else {
+        const int kv = it % KVN, rr = it / KVN;
         const int rb = row0 + rr * V;
 #pragma unroll
         for (int j = 0; j < V; ++j) {
@@ -68,10 +94,15 @@ struct TileLoader {
     for (int p = 0; p < PT; ++p) {
       const int it = tid + p * NT;
       if ((ITEMS % NT) != 0 && it >= ITEMS) continue;
-      const int kv = it % KVN, rr = it / KVN;
       if (KMAJ) {
+        const int kv = it % KVN, rr = it / KVN;
         tile[lds_slot<ROWS>(kv, rr)] = r[p][0];
+      } else if (TR) {
+        constexpr int CPL = ROWS / V;
+        const int c = it % CPL, kk = it / CPL;
+        st16(reinterpret_cast<bf16*>(tile) + trt_elem<ROWS>(kk, c * V), r[p][0]);
       } else {
+        const int kv = it % KVN, rr = it / KVN;
         u32x4 out[V];
         transpose_block<T>(r[p], out);
 #pragma unroll
@@ -79,18 +110,40 @@ struct TileLoader {
       }
     }
   }
+
+  // operand fragment of MFMA step s for the 16 rows starting at row0
+  __device__ __forceinline__ static u32x4 frag(const u32x4* tile, int s, int row0) {
+    if (TR) return lds_frag_tr<ROWS>(tile, s, row0);
+    return lds_frag<ROWS>(tile, s, row0);
+  }
 };
 
+// tanh(z) = 1 - 2 / (exp(2z) + 1), exact in form and saturating to +-1.
+__device__ __forceinline__ float tanh_f(float z) { return 1.0f - 2.0f / (__expf(2.0f * z) + 1.0f); }
 __device__ __forceinline__ float gelu_f(float u) {
   const float c = 0.7978845608028654f, a = 0.044715f;
-  return 0.5f * u * (1.0f + tanhf(c * (u + a * u * u * u)));
+  return 0.5f * u * (1.0f + tanh_f(c * (u + a * u * u * u)));
 }
 __device__ __forceinline__ float gelu_grad_f(float u) {
   const float c = 0.7978845608028654f, a = 0.044715f;
-  const float th = tanhf(c * (u + a * u * u * u));
+  const float th = tanh_f(c * (u + a * u * u * u));
   return 0.5f * (1.0f + th) + 0.5f * u * (1.0f - th * th) * c * (1.0f + 3.0f * a * u * u);
 }
 
+// Four consecutive elements [i, i+4) of a T array as floats (one 8- or 16-byte load).
+template <typename T> __device__ __forceinline__ void ld4f(const void* p, int64_t i, float* out) {
+  const T* q = reinterpret_cast<const T*>(p) + i;
+  if (sizeof(T) == 4) {
+    const u32x4 v = ld16(q);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) out[j] = vget<float>(v, j);
+  } else {
+    const u32x2 v = *reinterpret_cast<const u32x2*>(q);
+    const u32x4 w = {v[0], v[1], 0u, 0u};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) out[j] = vget<bf16>(w, j);
+  }
+}
 template <typename T> __device__ __forceinline__ float ldf(const void* p, int64_t i) {
   return to_f32(reinterpret_cast<const T*>(p)[i]);
 }
@@ -131,17 +184,32 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int m, int n, const 
     }
     return;
   }
-  float o[4];
+  float o[4], bias[4] = {0.f, 0.f, 0.f, 0.f}, aux[4] = {0.f, 0.f, 0.f, 0.f};
+  constexpr bool HAS_BIAS = EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU;
+  constexpr bool HAS_AUX = EPI == EPI_BIAS_RES || EPI == EPI_GELU_GRAD;
+  if (nv == 4) {
+    if (HAS_BIAS) {
+      const u32x4 b = ld16(a.bias + n);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bias[j] = vget<float>(b, j);
+    }
+    if (HAS_AUX) ld4f<T>(a.aux, (int64_t)m * a.ld_aux + n, aux);
+  } else {
+    for (int j = 0; j < nv; ++j) {
+      if (HAS_BIAS) bias[j] = a.bias[n + j];
+      if (HAS_AUX) aux[j] = ldf<T>(a.aux, (int64_t)m * a.ld_aux + n + j);
+    }
+  }
+#pragma unroll
   for (int j = 0; j < 4; ++j) {
-    float x = acc[j];
-    const int nn = n + (j < nv ? j : 0);
-    if (EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU) x += a.bias[nn];
-    if (EPI == EPI_BIAS_RES) x += ldf<T>(a.aux, (int64_t)m * a.ld_aux + nn);
-    if (EPI == EPI_GELU_GRAD) x *= gelu_grad_f(ldf<T>(a.aux, (int64_t)m * a.ld_aux + nn));
+    float x = acc[j] + bias[j];
+    if (EPI == EPI_BIAS_RES) x += aux[j];
+    if (EPI == EPI_GELU_GRAD) x *= gelu_grad_f(aux[j]);
     o[j] = x;
   }
   store4<TO>(reinterpret_cast<TO*>(a.C), (int64_t)m * a.ldc + n, o, nv);
   if (EPI == EPI_BIAS_GELU) {
+#pragma unroll
     for (int j = 0; j < 4; ++j) o[j] = gelu_f(o[j]);
     store4<TO>(reinterpret_cast<TO*>(a.C2), (int64_t)m * a.ldc + n, o, nv);
   }
@@ -159,8 +227,10 @@ __device__ __forceinline__ void tile_coords(int pid, int tiles_m, int tiles_n, i
   tn = in_group / gm;
 }
 
-template <typename T, typename TO, bool AK, bool BK, int EPI>
-__global__ void __launch_bounds__(NT, 2) gemm_kernel(GemmArgs a, int k_per_split) {
+template <typename T, typename TO, bool AK, bool BK, int EPI, class CF>
+__global__ void __launch_bounds__(CF::NT, 1) gemm_kernel(GemmArgs a, int k_per_split) {
+  constexpr int BM = CF::BM, BN = CF::BN, WM = CF::WM, WN = CF::WN, NT = CF::NT;
+  constexpr int WAVES_N = BN / WN;
   constexpr int V = Vec<T>::V;
   constexpr int BKE = KVN * V;
   __shared__ u32x4 smem[2][(BM + BN) * KVN];
@@ -172,14 +242,14 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(GemmArgs a, int k_per_split
   const int k_begin = blockIdx.y * k_per_split;
   const int k_end = min(a.K, k_begin + k_per_split);
   const int nk = (k_end - k_begin + BKE - 1) / BKE;
-  const int wm0 = (w >> 1) * WM, wn0 = (w & 1) * WN;
+  const int wm0 = (w / WAVES_N) * WM, wn0 = (w % WAVES_N) * WN;
 
   const T* A = reinterpret_cast<const T*>(a.A);
   const T* B = reinterpret_cast<const T*>(a.B);
-  TileLoader<T, BM, AK> la;
-  TileLoader<T, BN, BK> lb;
-  // When both operands are MN-major each uses half of the threads.
-  const int tid_b = (!AK && !BK) ? ((tid + NT / 2) % NT) : tid;
+  TileLoader<T, BM, AK, NT> la;
+  TileLoader<T, BN, BK, NT> lb;
+  // fp32 MN-major operands load V x V blocks on part of the threads; spread A and B apart
+  const int tid_b = (!AK && !BK && sizeof(T) == 4) ? ((tid + NT / 2) % NT) : tid;
 
   floatx4 acc[WM / 16][WN / 16];
 #pragma unroll
@@ -207,9 +277,9 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(GemmArgs a, int k_per_split
     for (int s = 0; s < 2; ++s) {
       u32x4 yf[WM / 16], xf[WN / 16];
 #pragma unroll
-      for (int i = 0; i < WM / 16; ++i) yf[i] = lds_frag<BM>(sa, s, wm0 + i * 16);
+      for (int i = 0; i < WM / 16; ++i) yf[i] = TileLoader<T, BM, AK, NT>::frag(sa, s, wm0 + i * 16);
 #pragma unroll
-      for (int j = 0; j < WN / 16; ++j) xf[j] = lds_frag<BN>(sb, s, wn0 + j * 16);
+      for (int j = 0; j < WN / 16; ++j) xf[j] = TileLoader<T, BN, BK, NT>::frag(sb, s, wn0 + j * 16);
 #pragma unroll
       for (int i = 0; i < WM / 16; ++i)
 #pragma unroll
@@ -229,15 +299,306 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(GemmArgs a, int k_per_split
       epilogue<T, TO, EPI>(a, m0 + wm0 + i * 16 + (l & 15), n0 + wn0 + j * 16 + 4 * (l >> 4), acc[i][j]);
 }
 
-template <typename T, typename TO, bool AK, bool BK, int EPI>
-hipError_t launch(const GemmArgs& a, int splits, hipStream_t st) {
-  constexpr int BKE = KVN * Vec<T>::V;
-  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+// ============================================================================================
+// bf16 pipelined kernel: direct-to-LDS loads into an NS-stage ring.
+//
+// Each 16-byte slot of a tile is filled by global_load_lds_dwordx4. A wave
+// instruction fills 64 consecutive slots, so the LDS layouts are chosen to be
+// wave-contiguous:
+//   K-major   [row][8 vectors of k], vector kv stored at kv ^ ((row >> 1) & 7);
+//             8 lanes fetch one 128-byte row segment, and a 16-row fragment
+//             read touches 16 distinct bank groups;
+//   MN-major  [k][rows] with 16-byte chunk c of line k at c ^ ((k & 3) << 1),
+//             read by ds_read_b64_tr_b16 (see lds_frag_tr).
+// Slots outside the operand (rows past M or N, k past K) are filled from a
+// zero page, so the ring never holds stale data and the k tail sums exactly.
+// The loads of tile kt + NS are issued right after the barrier that publishes
+// tile kt + 1, into the stage of tile kt, which every wave has read by then.
+// ============================================================================================
+template <int BM_, int BN_, int WM_, int WN_, int NS_>
+struct PipeTile {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NS = NS_;
+  static constexpr int WAVES = (BM / WM) * (BN / WN);
+  static constexpr int NT = 64 * WAVES;
+  static constexpr int SLOTS_A = BM * 8, SLOTS_B = BN * 8;       // 16-byte slots per tile
+  static constexpr int LA = SLOTS_A / NT, LB = SLOTS_B / NT;     // loads per thread per tile
+  static constexpr int STAGE_SLOTS = SLOTS_A + SLOTS_B;
+  static_assert(SLOTS_A % NT == 0 && SLOTS_B % NT == 0, "tile slots must split evenly over the threads");
+  // epilogue staging: PR rows of BN + 4 floats at a time, in the same LDS
+  static constexpr int LDC = BN + 4;
+  static constexpr int PR = (BM * LDC <= NS * STAGE_SLOTS * 4) ? BM : (BM > 128 ? 128 : BM);
+  static constexpr int SMEM_SLOTS = (NS * STAGE_SLOTS > PR * LDC / 4) ? NS * STAGE_SLOTS : PR * LDC / 4;
+  static_assert(BM % PR == 0 && PR % WM == 0 && (PR * LDC) % 4 == 0, "epilogue panels must align with wave rows");
+};
+
+__device__ __forceinline__ int kmaj_slot(int row, int kv) { return row * 8 + (kv ^ ((row >> 1) & 7)); }
+
+template <int ROWS> __device__ __forceinline__ u32x4 pipe_frag_k(const u32x4* tile, int s, int row0) {
+  const int l = lane_id();
+  const int row = row0 + (l & 15), kv = s * 4 + (l >> 4);
+  return tile[kmaj_slot(row, kv)];
+}
+
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// Wait until at most `newer` tiles of L loads each (issued after the awaited
+// one) are outstanding; the count must be an immediate, so the cases up to
+// MAXN are unrolled.
+template <int L, int MAXN> __device__ __forceinline__ void wait_loads(int newer) {
+  if constexpr (MAXN > 0) {
+    if (newer >= MAXN) {
+      wait_vmcnt<L * MAXN>();
+      return;
+    }
+    wait_loads<L, MAXN - 1>(newer);
+  } else {
+    (void)newer;
+    wait_vmcnt<0>();
+  }
+}
+// lgkmcnt(0), other counters left alone. Issued through the builtin, not inline
+// asm, so that the compiler's own wait insertion knows the reads are complete:
+// it then never has to cover the 16 LDS reads of two MFMA steps at once, which
+// the 4-bit LGKM counter cannot track, and which makes it wait for all of them.
+__device__ __forceinline__ void wait_lds_reads() {
+  __builtin_amdgcn_sched_barrier(0);   // keep MFMAs from being scheduled across the wait
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  __builtin_amdgcn_sched_barrier(0);
+}
+// Workgroup barrier without the memory fence __syncthreads() implies: the
+// fence would wait for every outstanding global load, including the tiles
+// prefetched for later iterations. Each wave has already waited for its own
+// loads of the tile about to be read (wait_loads) and for its LDS reads of the
+// stage about to be refilled (wait_lds_reads).
+__device__ __forceinline__ void barrier_no_fence() { asm volatile("s_barrier" ::: "memory"); }
+
+// One direct-to-LDS load: each lane's 16 bytes at g land at LDS byte address
+// lds + 16 * lane (the LDS address is wave-uniform, taken from M0). Issued as
+// inline asm so that the compiler does not track it: its wait insertion would
+// otherwise treat every later transpose read of LDS as a possible alias of the
+// transfer and wait for all loads in flight. The ring orders these transfers
+// explicitly (wait_loads, then a barrier, before a stage is read).
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+
+// Issue this thread's loads of one operand tile (ROWS rows x 64 contracted).
+// `tile` is the LDS byte address of the operand's part of the stage, `w` the
+// wave index (wave-uniform).
+template <int ROWS, bool KMAJ, int NT>
+__device__ __forceinline__ void pipe_fill(const bf16* src, int64_t ld, int row0, int rows_total, int k0, int k_end,
+                                          uint32_t tile, const void* zeros, int w, int l) {
+  constexpr int L = ROWS * 8 / NT;
+#pragma unroll
+  for (int p = 0; p < L; ++p) {
+    const int blk = p * (NT / 64) + w;        // wave-uniform block of 64 slots
+    const int slot = blk * 64 + l;
+    const void* g;
+    bool ok;
+    if (KMAJ) {
+      const int row = slot >> 3;
+      const int kv = (slot & 7) ^ ((row >> 1) & 7);
+      const int k = k0 + kv * 8;
+      ok = (row0 + row < rows_total) && (k < k_end);
+      g = src + (int64_t)(row0 + row) * ld + k;
+    } else {
+      constexpr int CPL = ROWS / 8;
+      const int line = slot / CPL;
+      const int c = (slot % CPL) ^ ((line & 3) << 1);
+      const int k = k0 + line, rb = row0 + c * 8;
+      ok = (k < k_end) && (rb < rows_total);
+      g = src + (int64_t)k * ld + rb;
+    }
+    dma16(ok ? g : zeros, tile + (uint32_t)(blk * 64 * 16));
+  }
+}
+
+// Epilogue through LDS. The accumulator tile goes to LDS as fp32 (row stride
+// BN + 4 floats, so the 16 rows a wave writes at once fall in distinct banks)
+// and is read back with consecutive lanes on consecutive columns: a wave then
+// covers whole 256-byte row segments with each store, and each atomic add
+// covers 64 consecutive floats. Tiles larger than the ring are done in row
+// panels of PR rows.
+template <typename TO, int EPI, class CF, int N_I, int N_J>
+__device__ __forceinline__ void staged_epilogue(const GemmArgs& a, float* cl, int m0, int n0, int wm0, int wn0,
+                                                const floatx4 (&acc)[N_I][N_J]) {
+  constexpr int BM = CF::BM, BN = CF::BN, NT = CF::NT, LDC = CF::LDC, PR = CF::PR;
+  const int tid = threadIdx.x, l = lane_id();
+#pragma unroll
+  for (int p = 0; p < BM / PR; ++p) {
+    __syncthreads();   // every wave is done with the ring (or with the previous panel)
+    if (wm0 >= p * PR && wm0 < (p + 1) * PR) {
+#pragma unroll
+      for (int i = 0; i < N_I; ++i)
+#pragma unroll
+        for (int j = 0; j < N_J; ++j)
+          *reinterpret_cast<floatx4*>(cl + (wm0 - p * PR + i * 16 + (l & 15)) * LDC + wn0 + j * 16 + 4 * (l >> 4)) =
+              acc[i][j];
+    }
+    __syncthreads();
+    const int mb = m0 + p * PR;
+    if constexpr (EPI == EPI_ATOMIC) {
+      float* C = reinterpret_cast<float*>(a.C);
+      for (int idx = tid; idx < PR * BN; idx += NT) {
+        const int r = idx / BN, c = idx % BN;
+        const int m = mb + r, n = n0 + c;
+        if (m < a.M && n < a.N) atomicAdd(C + (int64_t)m * a.ldc + n, cl[r * LDC + c]);
+      }
+    } else {
+      constexpr int CPR = BN / 4;   // 4-column units per row
+      for (int idx = tid; idx < PR * CPR; idx += NT) {
+        const int r = idx / CPR, c = (idx % CPR) * 4;
+        const floatx4 v = *reinterpret_cast<const floatx4*>(cl + r * LDC + c);
+        epilogue<bf16, TO, EPI>(a, mb + r, n0 + c, v);
+      }
+    }
+  }
+}
+
+template <typename TO, bool AK, bool BK, int EPI, class CF>
+__global__ void __launch_bounds__(CF::NT, 1) gemm_pipe_kernel(GemmArgs a, int k_per_split) {
+  constexpr int BM = CF::BM, BN = CF::BN, WM = CF::WM, WN = CF::WN, NT = CF::NT, NS = CF::NS;
+  constexpr int WAVES_N = BN / WN;
+  constexpr int BKE = 64;
+  constexpr int L = CF::LA + CF::LB;
+  __shared__ u32x4 smem[CF::SMEM_SLOTS];
+  const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
+  const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.N + BN - 1) / BN;
+  int tm, tn;
+  tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int k_begin = blockIdx.y * k_per_split;
+  const int k_end = min(a.K, k_begin + k_per_split);
+  const int nk = (k_end - k_begin + BKE - 1) / BKE;
+  const int wm0 = (w / WAVES_N) * WM, wn0 = (w % WAVES_N) * WN;
+  const bf16* A = reinterpret_cast<const bf16*>(a.A);
+  const bf16* B = reinterpret_cast<const bf16*>(a.B);
+
+  const uint32_t smem_lds = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) u32x4*)smem);
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  auto fill = [&](int kt) {
+    const uint32_t st = smem_lds + (uint32_t)((kt % NS) * CF::STAGE_SLOTS * 16);
+    const int k0 = k_begin + kt * BKE;
+    pipe_fill<BM, AK, NT>(A, a.lda, m0, a.M, k0, k_end, st, a.zeros, wu, l);
+    pipe_fill<BN, BK, NT>(B, a.ldb, n0, a.N, k0, k_end, st + CF::SLOTS_A * 16, a.zeros, wu, l);
+  };
+
+  floatx4 acc[WM / 16][WN / 16];
+#pragma unroll
+  for (int i = 0; i < WM / 16; ++i)
+#pragma unroll
+    for (int j = 0; j < WN / 16; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  // Fragments are double-buffered in registers: the LDS reads of the next
+  // MFMA step are issued before the MFMAs of the current one. The barrier that
+  // publishes tile kt + 1 sits between the two steps of tile kt; each wave
+  // first waits for its own reads of tile kt, so after the barrier the stage of
+  // tile kt is free and is refilled at once with tile kt + NS. Loads of a tile
+  // are thus issued NS - 1 tiles of MFMA work before they are needed.
+  u32x4 ya[WM / 16], xa[WN / 16], yb[WM / 16], xb[WN / 16];
+  auto read_step = [&](int kt, int s, u32x4* yf, u32x4* xf) {
+    const u32x4* sa = smem + (kt % NS) * CF::STAGE_SLOTS;
+    const u32x4* sb = sa + CF::SLOTS_A;
+#pragma unroll
+    for (int i = 0; i < WM / 16; ++i)
+      yf[i] = AK ? pipe_frag_k<BM>(sa, s, wm0 + i * 16) : lds_frag_tr<BM>(sa, s, wm0 + i * 16);
+#pragma unroll
+    for (int j = 0; j < WN / 16; ++j)
+      xf[j] = BK ? pipe_frag_k<BN>(sb, s, wn0 + j * 16) : lds_frag_tr<BN>(sb, s, wn0 + j * 16);
+  };
+  auto mma_all = [&](const u32x4* yf, const u32x4* xf) {
+#pragma unroll
+    for (int i = 0; i < WM / 16; ++i)
+#pragma unroll
+      for (int j = 0; j < WN / 16; ++j) mma_step<bf16>(acc[i][j], xf[j], yf[i]);
+  };
+
+#pragma unroll
+  for (int t = 0; t < NS; ++t)
+    if (t < nk) fill(t);
+  if (nk > 0) {
+    wait_loads<L, NS - 1>(min(nk - 1, NS - 1));
+    barrier_no_fence();
+    read_step(0, 0, ya, xa);
+  }
+  for (int kt = 0; kt < nk; ++kt) {
+    wait_lds_reads();   // reads of ya/xa, issued one MFMA step ago
+    read_step(kt, 1, yb, xb);
+    mma_all(ya, xa);
+    wait_lds_reads();     // reads of yb/xb: on every path, so no later join waits for more
+    if (kt + 1 < nk) {
+      // tiles kt + 2 .. kt + NS - 1 (those issued) may still be in flight
+      wait_loads<L, NS - 2>(min(nk - 1, kt + NS - 1) - (kt + 1));
+      barrier_no_fence();
+      if (kt + NS < nk) fill(kt + NS);
+      read_step(kt + 1, 0, ya, xa);
+    }
+    mma_all(yb, xb);
+  }
+  staged_epilogue<TO, EPI, CF>(a, reinterpret_cast<float*>(smem), m0, n0, wm0, wn0, acc);
+}
+
+// Tile configurations; the choice per call is made in launch().
+typedef Tile<128, 128, 64, 64> T128x128;
+
+int g_tile_override = -1;  // testing hook: force one configuration
+
+typedef PipeTile<256, 128, 64, 64, 3> P256x128;
+typedef PipeTile<128, 128, 64, 64, 4> P128x128;
+typedef PipeTile<128, 256, 64, 64, 3> P128x256;
+typedef PipeTile<256, 256, 64, 128, 2> P256x256w8;
+typedef PipeTile<256, 256, 128, 128, 2> P256x256w4;
+
+template <typename TO, bool AK, bool BK, int EPI, class CF>
+hipError_t launch_pipe(const GemmArgs& a, int splits, hipStream_t st) {
+  constexpr int BKE = 64;
+  const int tiles = ((a.M + CF::BM - 1) / CF::BM) * ((a.N + CF::BN - 1) / CF::BN);
   int kps = (a.K + splits - 1) / splits;
   kps = ((kps + BKE - 1) / BKE) * BKE;
   const int used = (a.K + kps - 1) / kps;
-  hipLaunchKernelGGL((gemm_kernel<T, TO, AK, BK, EPI>), dim3(tiles, used), dim3(NT), 0, st, a, kps);
+  hipLaunchKernelGGL((gemm_pipe_kernel<TO, AK, BK, EPI, CF>), dim3(tiles, used), dim3(CF::NT), 0, st, a, kps);
   return hipGetLastError();
+}
+
+template <typename T, typename TO, bool AK, bool BK, int EPI, class CF>
+hipError_t launch_cf(const GemmArgs& a, int splits, hipStream_t st) {
+  constexpr int BKE = KVN * Vec<T>::V;
+  const int tiles = ((a.M + CF::BM - 1) / CF::BM) * ((a.N + CF::BN - 1) / CF::BN);
+  int kps = (a.K + splits - 1) / splits;
+  kps = ((kps + BKE - 1) / BKE) * BKE;
+  const int used = (a.K + kps - 1) / kps;
+  hipLaunchKernelGGL((gemm_kernel<T, TO, AK, BK, EPI, CF>), dim3(tiles, used), dim3(CF::NT), 0, st, a, kps);
+  return hipGetLastError();
+}
+
+// The pipelined kernel moves whole 16-byte chunks of 8 elements from global
+// memory to LDS, so every chunk must be aligned and lie wholly inside or wholly
+// outside the operand: 16-byte aligned bases, leading dimensions and K (and the
+// contiguous M or N of an MN-major operand) multiples of 8. Other calls take
+// the register-staged kernel, which masks partial vectors.
+template <bool AK, bool BK>
+bool pipe_eligible(const GemmArgs& a) {
+  auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+  return a.zeros != nullptr && al16(a.A) && al16(a.B) && al16(a.zeros) && a.K % 8 == 0 && a.lda % 8 == 0 &&
+         a.ldb % 8 == 0 && (AK || a.M % 8 == 0) && (BK || a.N % 8 == 0);
+}
+
+template <typename T, typename TO, bool AK, bool BK, int EPI>
+hipError_t launch(const GemmArgs& a, int splits, hipStream_t st) {
+  if constexpr (sizeof(T) == 2) {
+    if (pipe_eligible<AK, BK>(a)) {
+      switch (g_tile_override) {
+        case 0: break;  // register-staged kernel, for comparison
+        case 11: return launch_pipe<TO, AK, BK, EPI, P128x128>(a, splits, st);
+        case 12: return launch_pipe<TO, AK, BK, EPI, P128x256>(a, splits, st);
+        case 13: return launch_pipe<TO, AK, BK, EPI, P256x256w8>(a, splits, st);
+        case 14: return launch_pipe<TO, AK, BK, EPI, P256x256w4>(a, splits, st);
+        default: return launch_pipe<TO, AK, BK, EPI, P256x128>(a, splits, st);
+      }
+    }
+  }
+  return launch_cf<T, TO, AK, BK, EPI, T128x128>(a, splits, st);
 }
 
 template <typename T, typename TO, bool AK, bool BK>
@@ -283,9 +644,40 @@ hipError_t by_layout(bool out_f32, GemmLayout lay, GemmEpi epi, const GemmArgs& 
 
 }  // namespace
 
-int gemm_tile_m() { return BM; }
-int gemm_tile_n() { return BN; }
-int gemm_tile_k(DType dt) { return KVN * (dt == DT_BF16 ? 8 : 4); }
+void gemm_set_tile_override(int cfg) { g_tile_override = cfg; }
+
+int gemm_acc_splits(DType dt, int M, int N, int K) {
+  // Split-K count for Cf32 += A^T B. Cost model, in microseconds: rounds of
+  // workgroups over the CUs times the k-tiles each runs (one k-tile of a tile
+  // at about 2.3 TFLOP/s per CU), plus the fp32 read-modify-write or atomic
+  // adds of the epilogue (about 2 ps per element and split).
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess && hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) ==
+                                                hipSuccess && n > 0)
+      cus = n;
+    else
+      cus = 256;
+  }
+  const bool pipe = dt == DT_BF16 && K % 8 == 0 && M % 8 == 0 && N % 8 == 0;
+  const int bm = pipe ? P256x128::BM : T128x128::BM, bn = pipe ? P256x128::BN : T128x128::BN;
+  const int bk = pipe ? 64 : KVN * (dt == DT_BF16 ? 8 : 4);
+  const double tiles = (double)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+  const int kt = (K + bk - 1) / bk;
+  const double t_k = 2.0 * bm * bn * bk / 2.3e6, t_e = 2e-6 * M * N;
+  int best = 1;
+  double best_t = 1e30;
+  for (int sp = 1; sp <= 16 && sp <= kt; sp *= 2) {
+    const double rounds = std::ceil(tiles * sp / cus);
+    const double t = rounds * std::ceil((double)kt / sp) * t_k + sp * t_e;
+    if (t < best_t * 0.97) {
+      best_t = t;
+      best = sp;
+    }
+  }
+  return best;
+}
 
 hipError_t gemm(DType dt, bool out_f32, GemmLayout lay, GemmEpi epi, const GemmArgs& a, int splits,
                 hipStream_t st) {

@@ -32,15 +32,20 @@ struct GemmArgs {
   const float* bias;
   const void* aux; int64_t ld_aux;
   void* C2;
+  const void* zeros;  // >= 16 bytes of device zeros (bf16 path: source of out-of-range tile slots)
 };
+// bf16 operands: K-major vectors that straddle K read the memory just past K,
+// which must hold zeros (true when K % 8 == 0, or for zero-padded rows).
 
 // dtype: element type of A, B, aux and of C/C2 unless out_f32 (then C is float).
 // splits > 1 is only valid with EPI_ATOMIC.
 hipError_t gemm(DType dt, bool out_f32, GemmLayout lay, GemmEpi epi, const GemmArgs& a, int splits, hipStream_t st);
 // Tile edge used by gemm(); callers size split-K against it.
-int gemm_tile_m();
-int gemm_tile_n();
-int gemm_tile_k(DType dt);
+// Split-K count the fp32-accumulating TN product (weight gradients) should use.
+int gemm_acc_splits(DType dt, int M, int N, int K);
+// Testing hook: force one kernel configuration for bf16 calls (0: register-staged 128x128;
+// direct-to-LDS pipelines 10: 256x128 x 3 stages (the default), 11: 128x128 x 4, 12: 128x256 x 3).
+void gemm_set_tile_override(int cfg);
 
 // ---- causal attention over the fused projection qkv [T, 3d] --------------------------
 // Forward: o [T, d]; lse2 [mu*H*S] = log2-sum-exp2 of the scaled scores in log2 units.

@@ -239,7 +239,7 @@ struct Layout {
   int64_t P = 0;          // parameters
   int64_t T = 0;          // tokens per micro-batch
   int64_t ldz = 0;        // logits row stride (last stage)
-  size_t theta, G, m, v, theta16, chunks;
+  size_t theta, G, m, v, theta16, chunks, zeros;
   int nchunks = 0;
   size_t stash, slot_bytes;
   std::vector<BlockSlot> blk;  // per block, inside a slot
@@ -274,6 +274,7 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
   L.theta16 = s.dtype == PACI_BF16 ? a.take(2 * L.P) : 0;
   L.nchunks = count_chunks(p);
   L.chunks = a.take(16 * (size_t)L.nchunks);
+  L.zeros = a.take(256);  // never written after init: source of out-of-range GEMM tile slots
 
   // one activation slot
   Bump sl;
@@ -436,7 +437,8 @@ int run(paci_stage* h, int fam, double work, F&& launch) {
 // ---- linear-layer helpers -------------------------------------------------------------------
 int linear_fwd(paci_stage* h, const void* X, int64_t w_off, int64_t b_off, int M, int N, int K, paci::GemmEpi epi,
                void* C, const void* aux, void* C2) {
-  paci::GemmArgs a{X, K, h->W(w_off), K, M, N, K, C, N, b_off >= 0 ? h->th(b_off) : nullptr, aux, N, C2};
+  paci::GemmArgs a{X, K, h->W(w_off), K, M, N, K, C, N, b_off >= 0 ? h->th(b_off) : nullptr, aux, N, C2,
+                   h->arena + h->L.zeros};
   return run(h, F_GEMM_FWD, 2.0 * M * N * K,
              [&] { return paci::gemm(h->dt, false, paci::GEMM_NT, epi, a, 1, h->st); });
 }
@@ -444,7 +446,7 @@ int linear_fwd(paci_stage* h, const void* X, int64_t w_off, int64_t b_off, int M
 // dX [M, N] = dY [M, K] . W [K, N]   (W = nn.Linear weight [out = K, in = N])
 int linear_dgrad(paci_stage* h, const void* dY, int64_t ldy, int64_t w_off, int M, int N, int K, paci::GemmEpi epi,
                  void* C, const void* aux) {
-  paci::GemmArgs a{dY, ldy, h->W(w_off), N, M, N, K, C, N, nullptr, aux, N, nullptr};
+  paci::GemmArgs a{dY, ldy, h->W(w_off), N, M, N, K, C, N, nullptr, aux, N, nullptr, h->arena + h->L.zeros};
   return run(h, F_GEMM_DGRAD, 2.0 * M * N * K,
              [&] { return paci::gemm(h->dt, false, paci::GEMM_NN, epi, a, 1, h->st); });
 }
@@ -452,12 +454,8 @@ int linear_dgrad(paci_stage* h, const void* dY, int64_t ldy, int64_t w_off, int 
 // G[out, in] += dY[T, out]^T X[T, in]
 int linear_wgrad(paci_stage* h, const void* dY, int64_t ldy, const void* X, int64_t ldx, int out, int in, int T,
                  int64_t g_off) {
-  const int tiles = ((out + paci::gemm_tile_m() - 1) / paci::gemm_tile_m()) *
-                    ((in + paci::gemm_tile_n() - 1) / paci::gemm_tile_n());
-  const int kt = (T + paci::gemm_tile_k(h->dt) - 1) / paci::gemm_tile_k(h->dt);
-  int splits = 1;
-  while (tiles * splits < 512 && splits * 2 <= kt / 4) splits *= 2;
-  paci::GemmArgs a{dY, ldy, X, ldx, out, in, T, h->g(g_off), in, nullptr, nullptr, 0, nullptr};
+  const int splits = paci::gemm_acc_splits(h->dt, out, in, T);
+  paci::GemmArgs a{dY, ldy, X, ldx, out, in, T, h->g(g_off), in, nullptr, nullptr, 0, nullptr, h->arena + h->L.zeros};
   const paci::GemmEpi epi = splits > 1 ? paci::EPI_ATOMIC : paci::EPI_ACC;
   return run(h, F_GEMM_WGRAD, 2.0 * out * in * T,
              [&] { return paci::gemm(h->dt, true, paci::GEMM_TN, epi, a, splits, h->st); });
@@ -739,7 +737,8 @@ extern "C" int paci_stage_forward(paci_stage* h, int mb, const void* dev_in, con
     float* z = reinterpret_cast<float*>(sl + L.s_z);
     if (!r) r = ln_fwd(h, sl + L.s_y, sl + L.s_nf, meanf, rstdf, h->p.lnf_g, h->p.lnf_b, nullptr);
     if (!r) {
-      paci::GemmArgs a{sl + L.s_nf, d, h->W(h->p.w_lm), d, T, s.vocab, d, z, L.ldz, nullptr, nullptr, 0, nullptr};
+      paci::GemmArgs a{sl + L.s_nf, d, h->W(h->p.w_lm), d, T, s.vocab, d, z, L.ldz, nullptr, nullptr, 0, nullptr,
+                       h->arena + h->L.zeros};
       r = run(h, F_GEMM_FWD, 2.0 * T * s.vocab * d,
               [&] { return paci::gemm(h->dt, true, paci::GEMM_NT, paci::EPI_STORE, a, 1, h->st); });
     }
