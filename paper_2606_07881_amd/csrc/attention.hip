@@ -19,6 +19,8 @@
 //          with the key in the lane, dV^T += dO^T P, dK^T += Q^T dS;
 //   dQ     (per 64 queries; 16 per wavefront):   S^T and dP^T with the query
 //          in the lane, dQ^T += K^T dS^T.
+#include <type_traits>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -124,6 +126,204 @@ __global__ void __launch_bounds__(NT) attn_fwd_kernel(const T* qkv, T* out, floa
       for (int r = 0; r < 4; ++r) op[c + r] = from_f32<T>(acc[t][r] * inv);
     }
     if ((l >> 4) == 0) lse2[(int64_t)bh * S + qrow] = m_run + log2f(l_run);
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+// bf16 kernels on an LDS ring. A block is 64 consecutive rows (keys or
+// queries) of one head, [64][dh] bf16, copied by direct-to-LDS loads into a
+// ring of NS stages so that the next blocks load while one is used. Row r's
+// 16-byte chunk c sits at chunk c ^ blk_swz(r): both fragment reads of 16
+// rows at one chunk (ds_read_b128) and transpose reads of 4 rows x 2 chunks
+// per 16 lanes (ds_read_b64_tr_b16) then hit distinct LDS banks.
+template <int CPR> __device__ __forceinline__ int blk_swz(int r) {
+  if constexpr (CPR == 4) return (r >> 2) & 3;
+  else if constexpr (CPR == 8) return (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
+  else return ((r & 7) << 1) | ((r >> 3) & 1);
+}
+template <int CPR> __device__ __forceinline__ int blk_slot(int r, int c) { return r * CPR + (c ^ blk_swz<CPR>(r)); }
+
+// MFMA operand: rows = block rows row0 + (l % 16), contracted = head dims of step s.
+template <int CPR> __device__ __forceinline__ u32x4 blk_frag(const u32x4* blk, int s, int row0) {
+  const int l = lane_id();
+  return blk[blk_slot<CPR>(row0 + (l & 15), s * 4 + (l >> 4))];
+}
+// MFMA operand: rows = head dims dh0 + (l % 16), contracted = the 32 block rows
+// of step s in StepPairPerm order (the order acc_to_frag gives accumulators).
+template <int CPR> __device__ __forceinline__ u32x4 blk_frag_tr(const u32x4* blk, int s, int dh0) {
+  const int l = lane_id(), g = l >> 4, c = l & 15;
+  const bf16* base = reinterpret_cast<const bf16*>(blk);
+  const int e = dh0 + 4 * (c & 3);
+  const int r_lo = s * 32 + 4 * g + (c >> 2), r_hi = r_lo + 16;
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4*)(base + blk_slot<CPR>(r_lo, e >> 3) * 8 + (e & 7)));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4*)(base + blk_slot<CPR>(r_hi, e >> 3) * 8 + (e & 7)));
+  const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
+  return u32x4{a[0], a[1], b[0], b[1]};
+}
+// Issue this thread's loads of one block (rows src[0..63], row stride ld) into
+// LDS byte address lds. Rows at or past rows_valid (>= 1) re-read the last
+// valid row; every consumer masks those rows out.
+template <int CPR, int NT>
+__device__ __forceinline__ void blk_fill(const bf16* src, int64_t ld, int rows_valid, uint32_t lds, int w, int l) {
+  constexpr int L = 64 * CPR / NT;
+  static_assert(L >= 1 && (64 * CPR) % NT == 0, "block slots must split evenly over the threads");
+#pragma unroll
+  for (int p = 0; p < L; ++p) {
+    const int blk = p * (NT / 64) + w;
+    const int slot = blk * 64 + l;
+    const int r = slot / CPR;
+    const int c = (slot % CPR) ^ blk_swz<CPR>(r);
+    const int rr = min(r, rows_valid - 1);
+    dma16(src + (int64_t)rr * ld + c * 8, lds + (uint32_t)(blk * 1024));
+  }
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)p);
+}
+
+// Forward, bf16: a workgroup takes 64 * QS * 4 queries, each wavefront 16 * QS
+// of them (QS sub-tiles of 16, the query in the lane as in the kernel above),
+// so every K and V fragment read from LDS feeds QS MFMAs. Key blocks are 64.
+template <int DH> struct FwdRing {
+  static constexpr int CPR = DH / 8, KS = DH / 32;
+  static constexpr int QS = DH <= 64 ? 4 : 2, WQ = 16 * QS, BQ = 4 * WQ;
+  static constexpr int NS = DH <= 64 ? 3 : 2;
+  static constexpr int BLK = 64 * CPR;          // 16-byte slots per block
+  static constexpr int L = 2 * BLK / NT;        // loads per thread per stage (K and V)
+};
+
+template <int DH>
+__global__ void __launch_bounds__(NT, 2) attn_fwd_ring_kernel(const bf16* qkv, bf16* out, float* lse2, int S, int H,
+                                                               int d, float scale_log2) {
+  using C = FwdRing<DH>;
+  constexpr int QS = C::QS, KS = C::KS, NS = C::NS, CPR = C::CPR;
+  __shared__ u32x4 ring[NS * 2 * C::BLK];
+  const int nqb = (S + C::BQ - 1) / C::BQ;
+  const int qb = nqb - 1 - blockIdx.y;
+  const int bh = blockIdx.x, b = bh / H, h = bh % H;
+  const int w = threadIdx.x >> 6, l = lane_id(), g = l >> 4;
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  const int64_t ld = 3 * (int64_t)d;
+  const bf16* Qp = qkv + (int64_t)b * S * ld + h * DH;
+  const bf16* Kp = Qp + d;
+  const bf16* Vp = Qp + 2 * d;
+  const int q0 = qb * C::BQ, qw0 = q0 + w * C::WQ;
+  const uint32_t ring_lds = lds_addr(ring);
+  const int nkb = min((q0 + C::BQ - 1) / BKV, (S - 1) / BKV) + 1;
+  const int my_last = (qw0 < S) ? min((qw0 + C::WQ - 1) / BKV, (S - 1) / BKV) : -1;
+
+  u32x4 qf[QS][KS];
+#pragma unroll
+  for (int qs = 0; qs < QS; ++qs) {
+    const int row = qw0 + 16 * qs + (l & 15);
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      qf[qs][s] = (row < S) ? ld16(Qp + (int64_t)row * ld + s * 32 + 8 * g) : u32x4{0, 0, 0, 0};
+  }
+  floatx4 acc[QS][DH / 16];
+  float m_run[QS], l_run[QS];
+#pragma unroll
+  for (int qs = 0; qs < QS; ++qs) {
+    m_run[qs] = -INFINITY;
+    l_run[qs] = 0.f;
+#pragma unroll
+    for (int t = 0; t < DH / 16; ++t) acc[qs][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  auto fill = [&](int kb) {
+    const uint32_t st = ring_lds + (uint32_t)((kb % NS) * 2 * C::BLK * 16);
+    const int k0 = kb * BKV;
+    blk_fill<CPR, NT>(Kp + (int64_t)k0 * ld, ld, S - k0, st, wu, l);
+    blk_fill<CPR, NT>(Vp + (int64_t)k0 * ld, ld, S - k0, st + C::BLK * 16, wu, l);
+  };
+#pragma unroll
+  for (int t = 0; t < NS - 1; ++t)
+    if (t < nkb) fill(t);
+  for (int kb = 0; kb < nkb; ++kb) {
+    wait_loads<C::L, NS - 2>(min(nkb - 1, kb + NS - 2) - kb);
+    wait_lds_reads();
+    barrier_no_fence();
+    if (kb + NS - 1 < nkb) fill(kb + NS - 1);   // into the stage of block kb - 1, read by now
+    if (kb > my_last) continue;
+    const u32x4* sK = ring + (kb % NS) * 2 * C::BLK;
+    const u32x4* sV = sK + C::BLK;
+    const int k0 = kb * BKV;
+
+    floatx4 sc[QS][4];
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+      u32x4 kf[KS];
+#pragma unroll
+      for (int s = 0; s < KS; ++s) kf[s] = blk_frag<CPR>(sK, s, kt * 16);
+#pragma unroll
+      for (int qs = 0; qs < QS; ++qs) {
+        sc[qs][kt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) mma_step<bf16>(sc[qs][kt], kf[s], qf[qs][s]);
+      }
+    }
+    u32x4 pf[QS][2];
+#pragma unroll
+    for (int qs = 0; qs < QS; ++qs) {
+      const int qrow = qw0 + 16 * qs + (l & 15);
+      if (k0 + BKV - 1 > qw0 + 16 * qs || k0 + BKV > S) {   // block crosses the diagonal or the end
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int key = k0 + kt * 16 + 4 * g + r;
+            if (key > qrow || key >= S) sc[qs][kt][r] = -INFINITY;
+          }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[qs][kt][r]);
+      mx = group4_max(mx);
+      const float m_new = fmaxf(m_run[qs], mx * scale_log2);
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      const float alpha = fast_exp2(m_run[qs] - m_use);
+      float rs = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = fast_exp2(fmaf(sc[qs][kt][r], scale_log2, -m_use));
+          sc[qs][kt][r] = p;
+          rs += p;
+        }
+      l_run[qs] = l_run[qs] * alpha + group4_sum(rs);
+      m_run[qs] = m_new;
+#pragma unroll
+      for (int t = 0; t < DH / 16; ++t) acc[qs][t] *= alpha;
+      pf[qs][0] = acc_to_frag<bf16>(sc[qs], 0);
+      pf[qs][1] = acc_to_frag<bf16>(sc[qs], 1);
+    }
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int t = 0; t < DH / 16; ++t) {
+        const u32x4 vf = blk_frag_tr<CPR>(sV, s, t * 16);
+#pragma unroll
+        for (int qs = 0; qs < QS; ++qs) mma_step<bf16>(acc[qs][t], vf, pf[qs][s]);
+      }
+  }
+#pragma unroll
+  for (int qs = 0; qs < QS; ++qs) {
+    const int qrow = qw0 + 16 * qs + (l & 15);
+    if (qrow < S) {
+      const float inv = 1.f / l_run[qs];
+      bf16* op = out + ((int64_t)b * S + qrow) * d + h * DH;
+#pragma unroll
+      for (int t = 0; t < DH / 16; ++t)
+        *reinterpret_cast<u32x2*>(op + t * 16 + 4 * g) =
+            u32x2{pack_bf16x2(acc[qs][t][0] * inv, acc[qs][t][1] * inv),
+                  pack_bf16x2(acc[qs][t][2] * inv, acc[qs][t][3] * inv)};
+      if (g == 0) lse2[(int64_t)bh * S + qrow] = m_run[qs] + log2f(l_run[qs]);
+    }
   }
 }
 
@@ -333,10 +533,337 @@ __global__ void __launch_bounds__(NT) attn_bwd_dq_kernel(const T* qkv, const T* 
   }
 }
 
+// ---------------------------------------------------------------------------------------
+// Backward, bf16. A pre-pass writes (lse2, D) pairs per query into a buffer
+// padded to 64 queries per head, so the kernels can copy them with the blocks.
+// Both kernels then recompute P from q, k and lse2 (no atomics):
+//   dK/dV  per 64 * SUB keys of a wavefront (K and V fragments in registers),
+//          streaming 64-query blocks of Q, dO and their pairs through the ring:
+//          S = Q K^T and dP = dO V^T with the key in the lane, then
+//          dV^T += dO^T P and dK^T += Q^T dS, dO^T and Q^T by transpose reads;
+//   dQ     per 64 * SUB queries (Q and dO fragments in registers), streaming
+//          64-key blocks of K and V: S^T, dP^T with the query in the lane, then
+//          dQ^T += K^T dS^T, K^T by transpose reads.
+template <int DH> struct BwdRing {
+  static constexpr int CPR = DH / 8, KST = DH / 32;
+  static constexpr int SUB = DH <= 64 ? 4 : 2, WR = 16 * SUB, BR = 4 * WR;
+  static constexpr int NS = DH <= 64 ? 3 : 2;
+  static constexpr int BLK = 64 * CPR;
+  static constexpr int PAIR_SLOTS = 32;            // 64 (lse2, D) pairs
+  static constexpr int STAGE = 2 * BLK + PAIR_SLOTS;
+  static constexpr int L = 2 * BLK / NT;           // block loads per thread per stage (wave 0 adds the pairs)
+};
+
+template <int DH>
+__global__ void __launch_bounds__(NT) attn_pairs_kernel(const bf16* o, const bf16* dO, const float* lse2, float* pairs,
+                                                         int S, int S_pad, int H, int d, int64_t rows) {
+  constexpr int LPR = DH / 8;
+  const int64_t gid = (int64_t)blockIdx.x * NT + threadIdx.x;
+  const int64_t row = gid / LPR;  // row = token * H + h
+  const int part = gid % LPR;
+  float sum = 0.f;
+  if (row < rows) {
+    const int64_t off = (row / H) * d + (row % H) * DH + part * 8;
+    const u32x4 a = ld16(o + off), g = ld16(dO + off);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sum += vget<bf16>(a, j) * vget<bf16>(g, j);
+  }
+#pragma unroll
+  for (int m = LPR / 2; m >= 1; m >>= 1) sum += __shfl_xor(sum, m, 64);
+  if (row < rows && part == 0) {
+    const int64_t tok = row / H, bq = tok / S, q = tok % S;
+    const int64_t bh = bq * H + row % H;
+    pairs[(bh * S_pad + q) * 2] = lse2[bh * S + q];
+    pairs[(bh * S_pad + q) * 2 + 1] = sum;
+  }
+  // queries S .. S_pad - 1 of every head: zeros, so that masked products (p = 0) stay finite
+  const int npad = S_pad - S;
+  const int64_t heads = rows / S;
+  if (npad > 0 && gid < heads * npad) {
+    const int64_t bh = gid / npad, q = S + gid % npad;
+    pairs[(bh * S_pad + q) * 2] = 0.f;
+    pairs[(bh * S_pad + q) * 2 + 1] = 0.f;
+  }
+}
+
+template <int DH>
+__global__ void __launch_bounds__(NT, 1) attn_dkdv_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
+                                                                bf16* dqkv, int S, int S_pad, int H, int d,
+                                                                float scale_log2, float scale) {
+  using C = BwdRing<DH>;
+  constexpr int SUB = C::SUB, KST = C::KST, NS = C::NS, CPR = C::CPR;
+  __shared__ u32x4 ring[NS * C::STAGE];
+  const int kb = blockIdx.y;                     // smallest keys first: they see the most queries
+  const int bh = blockIdx.x, b = bh / H, h = bh % H;
+  const int w = threadIdx.x >> 6, l = lane_id(), g = l >> 4;
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  const int64_t ld = 3 * (int64_t)d;
+  const bf16* Qp = qkv + (int64_t)b * S * ld + h * DH;
+  const bf16* Kp = Qp + d;
+  const bf16* Vp = Qp + 2 * d;
+  const bf16* dOp = dO + (int64_t)b * S * d + h * DH;
+  const float* Pp = pairs + (int64_t)bh * S_pad * 2;
+  const uint32_t ring_lds = lds_addr(ring);
+  const int k0 = kb * C::BR, kw0 = k0 + w * C::WR;
+  const int nqb = (S + 63) / 64, qb_first = k0 / 64, njobs = nqb - qb_first;
+  const int my_first = (kw0 < S) ? kw0 / 64 : nqb;
+
+  u32x4 kf[SUB][KST], vf[SUB][KST];
+#pragma unroll
+  for (int ks = 0; ks < SUB; ++ks) {
+    const int key = kw0 + 16 * ks + (l & 15);
+#pragma unroll
+    for (int st = 0; st < KST; ++st) {
+      kf[ks][st] = (key < S) ? ld16(Kp + (int64_t)key * ld + st * 32 + 8 * g) : u32x4{0, 0, 0, 0};
+      vf[ks][st] = (key < S) ? ld16(Vp + (int64_t)key * ld + st * 32 + 8 * g) : u32x4{0, 0, 0, 0};
+    }
+  }
+  floatx4 adk[SUB][DH / 16], adv[SUB][DH / 16];
+#pragma unroll
+  for (int ks = 0; ks < SUB; ++ks)
+#pragma unroll
+    for (int t = 0; t < DH / 16; ++t) adk[ks][t] = adv[ks][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  auto fill = [&](int j) {
+    const uint32_t st = ring_lds + (uint32_t)((j % NS) * C::STAGE * 16);
+    const int q0 = (qb_first + j) * 64;
+    blk_fill<CPR, NT>(Qp + (int64_t)q0 * ld, ld, S - q0, st, wu, l);
+    blk_fill<CPR, NT>(dOp + (int64_t)q0 * d, d, S - q0, st + C::BLK * 16, wu, l);
+    if (wu == 0 && l < C::PAIR_SLOTS) dma16(Pp + (int64_t)q0 * 2 + l * 4, st + 2 * C::BLK * 16);
+  };
+#pragma unroll
+  for (int t = 0; t < NS - 1; ++t)
+    if (t < njobs) fill(t);
+  for (int j = 0; j < njobs; ++j) {
+    wait_loads<C::L, NS - 2>(min(njobs - 1, j + NS - 2) - j);
+    wait_lds_reads();
+    barrier_no_fence();
+    if (j + NS - 1 < njobs) fill(j + NS - 1);
+    const int qb = qb_first + j;
+    if (qb < my_first) continue;
+    const u32x4* sQ = ring + (j % NS) * C::STAGE;
+    const u32x4* sdO = sQ + C::BLK;
+    const float* sP = reinterpret_cast<const float*>(sQ + 2 * C::BLK);
+    const int q0 = qb * 64;
+    const bool edge = (q0 < kw0 + C::WR - 1) || (q0 + 64 > S) || (kw0 + C::WR > S);
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {   // 32 queries: tiles 2s and 2s + 1
+      floatx4 sc[SUB][2], dp[SUB][2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        u32x4 qfr[KST], gfr[KST];
+#pragma unroll
+        for (int st = 0; st < KST; ++st) {
+          qfr[st] = blk_frag<CPR>(sQ, st, (2 * s + u) * 16);
+          gfr[st] = blk_frag<CPR>(sdO, st, (2 * s + u) * 16);
+        }
+#pragma unroll
+        for (int ks = 0; ks < SUB; ++ks) {
+          sc[ks][u] = dp[ks][u] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int st = 0; st < KST; ++st) {
+            mma_step<bf16>(sc[ks][u], qfr[st], kf[ks][st]);
+            mma_step<bf16>(dp[ks][u], gfr[st], vf[ks][st]);
+          }
+        }
+      }
+      // P = 2^(s * scale * log2 e - lse2), dS = P (dP - D); masked entries get P = 0
+      auto softmax = [&](auto masked) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int qi = (2 * s + u) * 16 + 4 * g + r;
+            const float lq = sP[2 * qi], Dq = sP[2 * qi + 1];
+#pragma unroll
+            for (int ks = 0; ks < SUB; ++ks) {
+              float x = fmaf(sc[ks][u][r], scale_log2, -lq);
+              if constexpr (decltype(masked)::value) {
+                const int key = kw0 + 16 * ks + (l & 15);
+                x = (key <= q0 + qi && q0 + qi < S && key < S) ? x : -INFINITY;
+              }
+              const float p = fast_exp2(x);
+              sc[ks][u][r] = p;
+              dp[ks][u][r] = p * (dp[ks][u][r] - Dq);
+            }
+          }
+      };
+      if (edge) softmax(std::true_type());
+      else softmax(std::false_type());
+      u32x4 pfr[SUB], dsf[SUB];
+#pragma unroll
+      for (int ks = 0; ks < SUB; ++ks) {
+        pfr[ks] = acc_to_frag<bf16>(sc[ks], 0);
+        dsf[ks] = acc_to_frag<bf16>(dp[ks], 0);
+      }
+#pragma unroll
+      for (int t = 0; t < DH / 16; ++t) {
+        const u32x4 gt = blk_frag_tr<CPR>(sdO, s, t * 16), qt = blk_frag_tr<CPR>(sQ, s, t * 16);
+#pragma unroll
+        for (int ks = 0; ks < SUB; ++ks) {
+          mma_step<bf16>(adv[ks][t], gt, pfr[ks]);
+          mma_step<bf16>(adk[ks][t], qt, dsf[ks]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int ks = 0; ks < SUB; ++ks) {
+    const int key = kw0 + 16 * ks + (l & 15);
+    if (key < S) {
+      bf16* dk = dqkv + ((int64_t)b * S + key) * ld + d + h * DH;
+      bf16* dv = dk + d;
+#pragma unroll
+      for (int t = 0; t < DH / 16; ++t) {
+        *reinterpret_cast<u32x2*>(dk + t * 16 + 4 * g) =
+            u32x2{pack_bf16x2(adk[ks][t][0] * scale, adk[ks][t][1] * scale),
+                  pack_bf16x2(adk[ks][t][2] * scale, adk[ks][t][3] * scale)};
+        *reinterpret_cast<u32x2*>(dv + t * 16 + 4 * g) =
+            u32x2{pack_bf16x2(adv[ks][t][0], adv[ks][t][1]), pack_bf16x2(adv[ks][t][2], adv[ks][t][3])};
+      }
+    }
+  }
+}
+
+template <int DH>
+__global__ void __launch_bounds__(NT, 1) attn_dq_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
+                                                              bf16* dqkv, int S, int S_pad, int H, int d,
+                                                              float scale_log2, float scale) {
+  using C = BwdRing<DH>;
+  constexpr int SUB = C::SUB, KST = C::KST, NS = C::NS, CPR = C::CPR;
+  __shared__ u32x4 ring[NS * 2 * C::BLK];
+  const int nqb = (S + C::BR - 1) / C::BR;
+  const int qb = nqb - 1 - blockIdx.y;           // largest queries first: they see the most keys
+  const int bh = blockIdx.x, b = bh / H, h = bh % H;
+  const int w = threadIdx.x >> 6, l = lane_id(), g = l >> 4;
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  const int64_t ld = 3 * (int64_t)d;
+  const bf16* Qp = qkv + (int64_t)b * S * ld + h * DH;
+  const bf16* Kp = Qp + d;
+  const bf16* Vp = Qp + 2 * d;
+  const bf16* dOp = dO + (int64_t)b * S * d + h * DH;
+  const float* Pp = pairs + (int64_t)bh * S_pad * 2;
+  const uint32_t ring_lds = lds_addr(ring);
+  const int q0 = qb * C::BR, qw0 = q0 + w * C::WR;
+  const int nkb = min((q0 + C::BR - 1) / BKV, (S - 1) / BKV) + 1;
+  const int my_last = (qw0 < S) ? min((qw0 + C::WR - 1) / BKV, (S - 1) / BKV) : -1;
+
+  u32x4 qf[SUB][KST], gf[SUB][KST];
+  float lq[SUB], Dq[SUB];
+#pragma unroll
+  for (int qs = 0; qs < SUB; ++qs) {
+    const int q = qw0 + 16 * qs + (l & 15);
+    const bool ok = q < S;
+#pragma unroll
+    for (int st = 0; st < KST; ++st) {
+      qf[qs][st] = ok ? ld16(Qp + (int64_t)q * ld + st * 32 + 8 * g) : u32x4{0, 0, 0, 0};
+      gf[qs][st] = ok ? ld16(dOp + (int64_t)q * d + st * 32 + 8 * g) : u32x4{0, 0, 0, 0};
+    }
+    lq[qs] = ok ? Pp[2 * q] : 0.f;
+    Dq[qs] = ok ? Pp[2 * q + 1] : 0.f;
+  }
+  floatx4 adq[SUB][DH / 16];
+#pragma unroll
+  for (int qs = 0; qs < SUB; ++qs)
+#pragma unroll
+    for (int t = 0; t < DH / 16; ++t) adq[qs][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  auto fill = [&](int kb) {
+    const uint32_t st = ring_lds + (uint32_t)((kb % NS) * 2 * C::BLK * 16);
+    const int k0 = kb * BKV;
+    blk_fill<CPR, NT>(Kp + (int64_t)k0 * ld, ld, S - k0, st, wu, l);
+    blk_fill<CPR, NT>(Vp + (int64_t)k0 * ld, ld, S - k0, st + C::BLK * 16, wu, l);
+  };
+#pragma unroll
+  for (int t = 0; t < NS - 1; ++t)
+    if (t < nkb) fill(t);
+  for (int kb = 0; kb < nkb; ++kb) {
+    wait_loads<C::L, NS - 2>(min(nkb - 1, kb + NS - 2) - kb);
+    wait_lds_reads();
+    barrier_no_fence();
+    if (kb + NS - 1 < nkb) fill(kb + NS - 1);
+    if (kb > my_last) continue;
+    const u32x4* sK = ring + (kb % NS) * 2 * C::BLK;
+    const u32x4* sV = sK + C::BLK;
+    const int k0 = kb * BKV;
+    const bool edge = (k0 + BKV - 1 > qw0) || (k0 + BKV > S) || (qw0 + C::WR > S);
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {   // 32 keys: tiles 2s and 2s + 1
+      floatx4 sc[SUB][2], dp[SUB][2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        u32x4 kfr[KST], vfr[KST];
+#pragma unroll
+        for (int st = 0; st < KST; ++st) {
+          kfr[st] = blk_frag<CPR>(sK, st, (2 * s + u) * 16);
+          vfr[st] = blk_frag<CPR>(sV, st, (2 * s + u) * 16);
+        }
+#pragma unroll
+        for (int qs = 0; qs < SUB; ++qs) {
+          sc[qs][u] = dp[qs][u] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int st = 0; st < KST; ++st) {
+            mma_step<bf16>(sc[qs][u], kfr[st], qf[qs][st]);
+            mma_step<bf16>(dp[qs][u], vfr[st], gf[qs][st]);
+          }
+        }
+      }
+      auto softmax = [&](auto masked) {
+#pragma unroll
+        for (int qs = 0; qs < SUB; ++qs) {
+          const int q = qw0 + 16 * qs + (l & 15);
+#pragma unroll
+          for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              float x = fmaf(sc[qs][u][r], scale_log2, -lq[qs]);
+              if constexpr (decltype(masked)::value) {
+                const int key = k0 + (2 * s + u) * 16 + 4 * g + r;
+                x = (key <= q && key < S && q < S) ? x : -INFINITY;
+              }
+              const float p = fast_exp2(x);
+              dp[qs][u][r] = p * (dp[qs][u][r] - Dq[qs]);
+            }
+        }
+      };
+      if (edge) softmax(std::true_type());
+      else softmax(std::false_type());
+      u32x4 dsf[SUB];
+#pragma unroll
+      for (int qs = 0; qs < SUB; ++qs) dsf[qs] = acc_to_frag<bf16>(dp[qs], 0);
+#pragma unroll
+      for (int t = 0; t < DH / 16; ++t) {
+        const u32x4 kt = blk_frag_tr<CPR>(sK, s, t * 16);
+#pragma unroll
+        for (int qs = 0; qs < SUB; ++qs) mma_step<bf16>(adq[qs][t], kt, dsf[qs]);
+      }
+    }
+  }
+#pragma unroll
+  for (int qs = 0; qs < SUB; ++qs) {
+    const int q = qw0 + 16 * qs + (l & 15);
+    if (q < S) {
+      bf16* dq = dqkv + ((int64_t)b * S + q) * ld + h * DH;
+#pragma unroll
+      for (int t = 0; t < DH / 16; ++t)
+        *reinterpret_cast<u32x2*>(dq + t * 16 + 4 * g) =
+            u32x2{pack_bf16x2(adq[qs][t][0] * scale, adq[qs][t][1] * scale),
+                  pack_bf16x2(adq[qs][t][2] * scale, adq[qs][t][3] * scale)};
+    }
+  }
+}
+
 template <typename T, int DH>
 hipError_t fwd_launch(const void* qkv, void* o, float* lse2, int mu, int S, int H, hipStream_t st) {
   const int d = H * DH;
   const float scale_log2 = LOG2E / sqrtf((float)DH);
+  if constexpr (sizeof(T) == 2) {
+    using C = FwdRing<DH>;
+    dim3 grid(mu * H, (S + C::BQ - 1) / C::BQ);   // x fastest: every head's heaviest query block first
+    hipLaunchKernelGGL((attn_fwd_ring_kernel<DH>), grid, dim3(NT), 0, st, reinterpret_cast<const bf16*>(qkv),
+                       reinterpret_cast<bf16*>(o), lse2, S, H, d, scale_log2);
+    return hipGetLastError();
+  }
   dim3 grid((S + 63) / 64, mu * H);
   hipLaunchKernelGGL((attn_fwd_kernel<T, DH>), grid, dim3(NT), 0, st, reinterpret_cast<const T*>(qkv),
                      reinterpret_cast<T*>(o), lse2, S, H, d, scale_log2);
@@ -349,6 +876,28 @@ hipError_t bwd_launch(const void* qkv, const void* o, const void* dO, const floa
   const int d = H * DH;
   const float scale = 1.f / sqrtf((float)DH);
   const float scale_log2 = LOG2E * scale;
+  if constexpr (sizeof(T) == 2) {
+    using C = BwdRing<DH>;
+    const int S_pad = (S + 63) / 64 * 64;
+    const int64_t rows = (int64_t)mu * S * H;
+    const int64_t threads = rows * (DH / 8);
+    const bf16* q = reinterpret_cast<const bf16*>(qkv);
+    const bf16* g = reinterpret_cast<const bf16*>(dO);
+    bf16* dq = reinterpret_cast<bf16*>(dqkv);
+    const int64_t pad_threads = (int64_t)mu * H * (S_pad - S);
+    const int64_t grid_threads = threads > pad_threads ? threads : pad_threads;
+    hipLaunchKernelGGL((attn_pairs_kernel<DH>), dim3((unsigned)((grid_threads + NT - 1) / NT)), dim3(NT), 0, st,
+                       reinterpret_cast<const bf16*>(o), g, lse2, Dbuf, S, S_pad, H, d, rows);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((attn_dkdv_ring_kernel<DH>), dim3(mu * H, (S + C::BR - 1) / C::BR), dim3(NT), 0, st, q, g,
+                       Dbuf, dq, S, S_pad, H, d, scale_log2, scale);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((attn_dq_ring_kernel<DH>), dim3(mu * H, (S + C::BR - 1) / C::BR), dim3(NT), 0, st, q, g, Dbuf,
+                       dq, S, S_pad, H, d, scale_log2, scale);
+    return hipGetLastError();
+  }
   constexpr int LPR = DH / Vec<T>::V;
   const int64_t rows = (int64_t)mu * S * H;
   const int64_t threads = rows * LPR;
@@ -399,6 +948,11 @@ hipError_t attn_fwd(DType dt, const void* qkv, void* o, float* lse2, int mu, int
   if (mu <= 0 || S <= 0 || H <= 0) return hipErrorInvalidValue;
   if (dt == DT_BF16) return fwd_dh<bf16>(qkv, o, lse2, mu, S, H, dh, st);
   return fwd_dh<float>(qkv, o, lse2, mu, S, H, dh, st);
+}
+
+int64_t attn_bwd_workspace_floats(DType dt, int mu, int S, int H) {
+  if (dt == DT_BF16) return 2 * (int64_t)mu * H * ((S + 63) / 64 * 64);
+  return (int64_t)mu * H * S;
 }
 
 hipError_t attn_bwd(DType dt, const void* qkv, const void* o, const void* dO, const float* lse2, float* Dbuf,

@@ -339,49 +339,6 @@ template <int ROWS> __device__ __forceinline__ u32x4 pipe_frag_k(const u32x4* ti
   return tile[kmaj_slot(row, kv)];
 }
 
-template <int N> __device__ __forceinline__ void wait_vmcnt() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-// Wait until at most `newer` tiles of L loads each (issued after the awaited
-// one) are outstanding; the count must be an immediate, so the cases up to
-// MAXN are unrolled.
-template <int L, int MAXN> __device__ __forceinline__ void wait_loads(int newer) {
-  if constexpr (MAXN > 0) {
-    if (newer >= MAXN) {
-      wait_vmcnt<L * MAXN>();
-      return;
-    }
-    wait_loads<L, MAXN - 1>(newer);
-  } else {
-    (void)newer;
-    wait_vmcnt<0>();
-  }
-}
-// lgkmcnt(0), other counters left alone. Issued through the builtin, not inline
-// asm, so that the compiler's own wait insertion knows the reads are complete:
-// it then never has to cover the 16 LDS reads of two MFMA steps at once, which
-// the 4-bit LGKM counter cannot track, and which makes it wait for all of them.
-__device__ __forceinline__ void wait_lds_reads() {
-  __builtin_amdgcn_sched_barrier(0);   // keep MFMAs from being scheduled across the wait
-  __builtin_amdgcn_s_waitcnt(0xC07F);
-  __builtin_amdgcn_sched_barrier(0);
-}
-// Workgroup barrier without the memory fence __syncthreads() implies: the
-// fence would wait for every outstanding global load, including the tiles
-// prefetched for later iterations. Each wave has already waited for its own
-// loads of the tile about to be read (wait_loads) and for its LDS reads of the
-// stage about to be refilled (wait_lds_reads).
-__device__ __forceinline__ void barrier_no_fence() { asm volatile("s_barrier" ::: "memory"); }
-
-// One direct-to-LDS load: each lane's 16 bytes at g land at LDS byte address
-// lds + 16 * lane (the LDS address is wave-uniform, taken from M0). Issued as
-// inline asm so that the compiler does not track it: its wait insertion would
-// otherwise treat every later transpose read of LDS as a possible alias of the
-// transfer and wait for all loads in flight. The ring orders these transfers
-// explicitly (wait_loads, then a barrier, before a stage is read).
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
-}
 
 // Issue this thread's loads of one operand tile (ROWS rows x 64 contracted).
 // `tile` is the LDS byte address of the operand's part of the stage, `w` the

@@ -51,6 +51,8 @@ void gemm_set_tile_override(int cfg);
 // Forward: o [T, d]; lse2 [mu*H*S] = log2-sum-exp2 of the scaled scores in log2 units.
 hipError_t attn_fwd(DType dt, const void* qkv, void* o, float* lse2, int mu, int S, int H, int dh, hipStream_t st);
 // Backward: D = rowsum(dO * O) per (b, h, query), then dK, dV and dQ into dqkv [T, 3d].
+// Dbuf is workspace of attn_bwd_workspace_floats() floats.
+int64_t attn_bwd_workspace_floats(DType dt, int mu, int S, int H);
 hipError_t attn_bwd(DType dt, const void* qkv, const void* o, const void* dO, const float* lse2, float* Dbuf,
                     void* dqkv, int mu, int S, int H, int dh, hipStream_t st);
 

@@ -316,7 +316,8 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
   L.w_dx1 = a.take(esz * T * d);
   L.w_do = a.take(esz * T * d);
   L.w_dqkv = a.take(esz * T * 3 * d);
-  L.w_D = a.take(4 * heads_rows);
+  L.w_D = a.take(4 * (size_t)paci::attn_bwd_workspace_floats(s.dtype == PACI_BF16 ? paci::DT_BF16 : paci::DT_F32,
+                                                              s.micro_batch, s.seq, s.n_heads));
   int64_t part = 64;
   if (s.kind == PACI_LAST) {
     part = std::max(part, paci::ce_part_floats((int)T));
