@@ -119,7 +119,10 @@ struct TileLoader {
 };
 
 // tanh(z) = 1 - 2 / (exp(2z) + 1), exact in form and saturating to +-1.
-__device__ __forceinline__ float tanh_f(float z) { return 1.0f - 2.0f / (__expf(2.0f * z) + 1.0f); }
+// tanh z = 1 - 2 / (e^(2z) + 1), with the hardware exp2 and reciprocal (about 1 ulp each)
+__device__ __forceinline__ float tanh_f(float z) {
+  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(fast_exp2(2.8853900817779268f * z) + 1.0f);
+}
 __device__ __forceinline__ float gelu_f(float u) {
   const float c = 0.7978845608028654f, a = 0.044715f;
   return 0.5f * u * (1.0f + tanh_f(c * (u + a * u * u * u)));
@@ -371,6 +374,124 @@ __device__ __forceinline__ void pipe_fill(const bf16* src, int64_t ld, int row0,
   }
 }
 
+// Output pass of the staged epilogue (every mode but the atomic one). A unit
+// is one 16-byte store: 8 bf16 or 4 fp32 columns. Each thread keeps the same
+// unit column for all its rows, so the bias is loaded once; the aux rows of
+// all passes are loaded before any store, so their latencies overlap.
+template <typename TO, int EPI, int BN, int PR, int NT>
+__device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, int mb, int n0, int tid) {
+  constexpr int U = 16 / sizeof(TO), UPR = BN / U, RPI = NT / UPR, P = PR / RPI;
+  static_assert(NT % UPR == 0 && PR % RPI == 0, "units must tile the panel");
+  constexpr int LDC = BN + 4;
+  constexpr bool HAS_BIAS = EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU;
+  constexpr bool HAS_AUX = EPI == EPI_BIAS_RES || EPI == EPI_GELU_GRAD;   // aux holds bf16 here
+  const int cu = tid % UPR, r0 = tid / UPR;
+  const int n = n0 + cu * U;
+  if (n >= a.N) return;
+  const int nv = min(U, a.N - n);
+  auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+  const bool vec = nv == U && a.ldc % U == 0 && al16(a.C) && (EPI != EPI_BIAS_GELU || al16(a.C2)) &&
+                   (!HAS_AUX || (a.ld_aux % 8 == 0 && al16(a.aux))) && (!HAS_BIAS || al16(a.bias));
+  float bias[U];
+#pragma unroll
+  for (int j = 0; j < U; ++j) bias[j] = (HAS_BIAS && j < nv) ? a.bias[n + j] : 0.f;
+  float aux[P][U];
+  if constexpr (HAS_AUX) {
+    const bf16* ap = reinterpret_cast<const bf16*>(a.aux);
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const int m = mb + r0 + p * RPI;
+      if (m < a.M) {
+        const int64_t off = (int64_t)m * a.ld_aux + n;
+        if (vec) {
+#pragma unroll
+          for (int h = 0; h < U / 8 + (U < 8 ? 1 : 0); ++h) {
+            if constexpr (U >= 8) {
+              const u32x4 w = ld16(ap + off + 8 * h);
+#pragma unroll
+              for (int j = 0; j < 8; ++j) aux[p][8 * h + j] = vget<bf16>(w, j);
+            } else {
+              const u32x2 w = *reinterpret_cast<const u32x2*>(ap + off);
+#pragma unroll
+              for (int j = 0; j < U; ++j) {
+                const uint32_t word = w[j >> 1];
+                aux[p][j] = as_float((j & 1) ? (word & 0xffff0000u) : (word << 16));
+              }
+            }
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < U; ++j) aux[p][j] = j < nv ? (float)ap[off + j] : 0.f;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    const int r = r0 + p * RPI, m = mb + r;
+    if (m >= a.M) continue;
+    float o[U];
+#pragma unroll
+    for (int q = 0; q < U / 4; ++q) {
+      const floatx4 v = *reinterpret_cast<const floatx4*>(cl + r * LDC + cu * U + 4 * q);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[4 * q + j] = v[j];
+    }
+    const int64_t off = (int64_t)m * a.ldc + n;
+    if constexpr (EPI == EPI_ACC) {
+      float* C = reinterpret_cast<float*>(a.C);
+      if (vec) {
+        const u32x4 old = ld16(C + off);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] += as_float(old[j]);
+      } else {
+#pragma unroll
+        for (int j = 0; j < U; ++j)
+          if (j < nv) o[j] += C[off + j];
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        float x = o[j] + bias[j];
+        if constexpr (EPI == EPI_BIAS_RES) x += aux[p][j];
+        if constexpr (EPI == EPI_GELU_GRAD) x *= gelu_grad_f(aux[p][j]);
+        o[j] = x;
+      }
+    }
+    TO* C = reinterpret_cast<TO*>(a.C);
+    if (vec) {
+      if constexpr (sizeof(TO) == 2) {
+        st16(C + off, u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
+                            pack_bf16x2(o[6], o[7])});
+      } else {
+        st16(C + off, u32x4{__builtin_bit_cast(uint32_t, o[0]), __builtin_bit_cast(uint32_t, o[1]),
+                            __builtin_bit_cast(uint32_t, o[2]), __builtin_bit_cast(uint32_t, o[3])});
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (j < nv) C[off + j] = from_f32<TO>(o[j]);
+    }
+    if constexpr (EPI == EPI_BIAS_GELU) {
+      TO* C2 = reinterpret_cast<TO*>(a.C2);
+#pragma unroll
+      for (int j = 0; j < U; ++j) o[j] = gelu_f(o[j]);
+      if (vec) {
+        if constexpr (sizeof(TO) == 2)
+          st16(C2 + off, u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
+                               pack_bf16x2(o[6], o[7])});
+        else
+          st16(C2 + off, u32x4{__builtin_bit_cast(uint32_t, o[0]), __builtin_bit_cast(uint32_t, o[1]),
+                               __builtin_bit_cast(uint32_t, o[2]), __builtin_bit_cast(uint32_t, o[3])});
+      } else {
+#pragma unroll
+        for (int j = 0; j < U; ++j)
+          if (j < nv) C2[off + j] = from_f32<TO>(o[j]);
+      }
+    }
+  }
+}
+
 // Epilogue through LDS. The accumulator tile goes to LDS as fp32 (row stride
 // BN + 4 floats, so the 16 rows a wave writes at once fall in distinct banks)
 // and is read back with consecutive lanes on consecutive columns: a wave then
@@ -403,13 +524,20 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, float* cl, in
         if (m < a.M && n < a.N) atomicAdd(C + (int64_t)m * a.ldc + n, cl[r * LDC + c]);
       }
     } else {
-      constexpr int CPR = BN / 4;   // 4-column units per row
-      for (int idx = tid; idx < PR * CPR; idx += NT) {
-        const int r = idx / CPR, c = (idx % CPR) * 4;
-        const floatx4 v = *reinterpret_cast<const floatx4*>(cl + r * LDC + c);
-        epilogue<bf16, TO, EPI>(a, mb + r, n0 + c, v);
-      }
+      staged_out<TO, EPI, BN, PR, NT>(a, cl, mb, n0, tid);
     }
+  }
+}
+
+// Scheduling pattern for one MFMA step: NREAD LDS reads (of the next step)
+// spread evenly between NMFMA independent MFMAs (of this step).
+template <int NREAD, int NMFMA>
+__device__ __forceinline__ void interleave_reads() {
+  constexpr int PER = NMFMA / NREAD > 0 ? NMFMA / NREAD : 1;
+#pragma unroll
+  for (int i = 0; i < NREAD; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one DS read
+    __builtin_amdgcn_sched_group_barrier(0x008, PER, 0); // PER MFMAs
   }
 }
 
@@ -471,28 +599,30 @@ __global__ void __launch_bounds__(CF::NT, 1) gemm_pipe_kernel(GemmArgs a, int k_
       for (int j = 0; j < WN / 16; ++j) mma_step<bf16>(acc[i][j], xf[j], yf[i]);
   };
 
+  // The loop body has no branches: fills past the last tile read the zero page
+  // and the reads after the last tile are discarded. Within each MFMA step the
+  // scheduler spreads the LDS reads of the next step between the MFMAs.
+  constexpr int NRI = (AK ? 1 : 2) * (WM / 16) + (BK ? 1 : 2) * (WN / 16);   // LDS read instructions per step
+  constexpr int NM = (WM / 16) * (WN / 16);                                 // MFMAs per step
 #pragma unroll
-  for (int t = 0; t < NS; ++t)
-    if (t < nk) fill(t);
-  if (nk > 0) {
-    wait_loads<L, NS - 1>(min(nk - 1, NS - 1));
-    barrier_no_fence();
-    read_step(0, 0, ya, xa);
-  }
+  for (int t = 0; t < NS; ++t) fill(t);
+  wait_vmcnt<L * (NS - 1)>();
+  barrier_no_fence();
+  read_step(0, 0, ya, xa);
   for (int kt = 0; kt < nk; ++kt) {
-    wait_lds_reads();   // reads of ya/xa, issued one MFMA step ago
+    wait_lds_reads();     // reads of ya/xa, issued one MFMA step ago
     read_step(kt, 1, yb, xb);
     mma_all(ya, xa);
-    wait_lds_reads();     // reads of yb/xb: on every path, so no later join waits for more
-    if (kt + 1 < nk) {
-      // tiles kt + 2 .. kt + NS - 1 (those issued) may still be in flight
-      wait_loads<L, NS - 2>(min(nk - 1, kt + NS - 1) - (kt + 1));
-      barrier_no_fence();
-      if (kt + NS < nk) fill(kt + NS);
-      read_step(kt + 1, 0, ya, xa);
-    }
+    interleave_reads<NRI, NM>();
+    wait_lds_reads();     // reads of yb/xb
+    wait_vmcnt<L * (NS - 2)>();   // tile kt + 1 has landed; kt + 2 .. kt + NS - 1 may be in flight
+    barrier_no_fence();
+    fill(kt + NS);                // into the stage of tile kt, which every wave has read
+    read_step(kt + 1, 0, ya, xa);
     mma_all(yb, xb);
+    interleave_reads<NRI, NM>();
   }
+  wait_vmcnt<0>();   // the fills past the last tile, before the ring is reused
   staged_epilogue<TO, EPI, CF>(a, reinterpret_cast<float*>(smem), m0, n0, wm0, wn0, acc);
 }
 
@@ -504,8 +634,6 @@ int g_tile_override = -1;  // testing hook: force one configuration
 typedef PipeTile<256, 128, 64, 64, 3> P256x128;
 typedef PipeTile<128, 128, 64, 64, 4> P128x128;
 typedef PipeTile<128, 256, 64, 64, 3> P128x256;
-typedef PipeTile<256, 256, 64, 128, 2> P256x256w8;
-typedef PipeTile<256, 256, 128, 128, 2> P256x256w4;
 
 template <typename TO, bool AK, bool BK, int EPI, class CF>
 hipError_t launch_pipe(const GemmArgs& a, int splits, hipStream_t st) {
@@ -549,8 +677,6 @@ hipError_t launch(const GemmArgs& a, int splits, hipStream_t st) {
         case 0: break;  // register-staged kernel, for comparison
         case 11: return launch_pipe<TO, AK, BK, EPI, P128x128>(a, splits, st);
         case 12: return launch_pipe<TO, AK, BK, EPI, P128x256>(a, splits, st);
-        case 13: return launch_pipe<TO, AK, BK, EPI, P256x256w8>(a, splits, st);
-        case 14: return launch_pipe<TO, AK, BK, EPI, P256x256w4>(a, splits, st);
         default: return launch_pipe<TO, AK, BK, EPI, P256x128>(a, splits, st);
       }
     }
