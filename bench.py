@@ -27,6 +27,7 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_gpt2m_mid_bf16.md")
 
 
 def log(msg):
@@ -135,13 +136,17 @@ def main():
     # the timed region: K plain replays on the stage stream
     stream = torch.cuda.current_stream()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     start.record(stream)
+    marks[0].record(stream)
     for s in range(args.steps):
         stamps = replay()
+        marks[s + 1].record(stream)
     stop.record(stream)
     torch.cuda.synchronize()
     ms_total = start.elapsed_time(stop)
+    per_replay = sorted(marks[s].elapsed_time(marks[s + 1]) for s in range(args.steps))
     log(f"bench: {args.steps} timed replays in {ms_total:.1f} ms")
 
     # after the timed region: the same number of replays with HIP events around every
@@ -166,6 +171,12 @@ def main():
     value = tokens_per_step / (ms_step / 1e3)
     mfma_util = flop_step / (ms_step / 1e3) / (PEAK_BF16_TFLOPS * 1e12)
 
+    # HBM bytes per launch from the committed counter summary, while the kernel sources are unchanged
+    from paper_2606_07881_amd import profile_summary
+    rec = profile_summary.read_record(TRAFFIC_PROFILE)
+    traffic_ok = (rec is not None and name == configs.BENCH_CONFIG
+                  and rec.get("sources_sha256") == profile_summary.sources_sha256())
+
     # dominant kernel family by device time; matrix families are priced in FLOP, streaming ones in bytes
     mfma_fams = {"gemm_fwd", "gemm_dgrad", "gemm_wgrad_acc", "attn_fwd", "attn_bwd"}
     fam = max(kt, key=lambda k: kt[k]["ms"])
@@ -182,6 +193,12 @@ def main():
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None, "kernel": fam,
                 "launches": f["launches"], "avg_launch_us": round(per_launch_ms * 1e3, 2)}
+    if traffic_ok and fam in rec["bytes_per_launch"]:
+        roof["traffic"] = rec["bytes_per_launch"][fam]
+        roof["traffic_unit"] = "bytes per launch (HBM, FETCH_SIZE + WRITE_SIZE scaled by a copy kernel)"
+        roof["traffic_source"] = os.path.relpath(TRAFFIC_PROFILE, ROOT)
+    else:
+        roof["traffic_source"] = "none: counters were taken on other kernel sources or another workload"
     families = {}
     kernel_ms = sum(v["ms"] for v in kt.values())
     for k, v in kt.items():
@@ -212,6 +229,8 @@ def main():
                    "micro_batches_per_step": M, "tokens_per_step": tokens_per_step, "K": K, "delay": delay,
                    "parallelism": "single stage, 1 GPU"},
         "mfma_util": round(mfma_util, 4),
+        "ms_per_step_median": round(per_replay[len(per_replay) // 2], 3),
+        "ms_per_step_min_max": [round(per_replay[0], 3), round(per_replay[-1], 3)],
         "ms_per_step_with_launch_events": round(ms_instr, 3),
         "flop_per_step": flop_step,
         "stamps_delta_sum": int(stamps[:, 2].sum()),

@@ -1,7 +1,8 @@
 """Builds libpaci_stage.so (the HIP stage library) for gfx950 with hipcc.
 
-Every translation unit under csrc/ is compiled in parallel into _build/ and
-linked in place next to this file, where the binding loads it. Run as
+Every translation unit of the library under csrc/ is compiled in parallel into
+_build/ and linked in place next to this file, where the binding loads it.
+stage_bench (a native driver used for profiling) is linked against it. Run as
 ``python -m paper_2606_07881_amd.build`` or call ``build()``.
 """
 import concurrent.futures
@@ -16,7 +17,9 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libpaci_stage.so")
+EXE = os.path.join(HERE, "stage_bench")
 SOURCES = ["gemm.hip", "attention.hip", "rowwise.hip", "optim.hip", "stage.hip"]
+TOOLS = ["stage_bench.hip"]
 
 ARCH = "gfx950"
 FLAGS = [
@@ -47,17 +50,26 @@ def _compile(src):
 
 def build(verbose=False):
     os.makedirs(BUILD, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        results = list(ex.map(_compile, SOURCES))
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(SOURCES) + len(TOOLS))) as ex:
+        results = list(ex.map(_compile, SOURCES + TOOLS))
     for obj, err in results:
         if verbose and err.strip():
             print(err, file=sys.stderr)
+    tools = results[len(SOURCES):]
+    results = results[:len(SOURCES)]
     tmp = LIB + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + [o for o, _ in results]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stdout + r.stderr)
     os.replace(tmp, LIB)
+    tmp = EXE + ".tmp"
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-o", tmp, tools[0][0], "-L", HERE, "-lpaci_stage",
+           "-Wl,-rpath,$ORIGIN"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("link of stage_bench failed:\n" + r.stdout + r.stderr)
+    os.replace(tmp, EXE)
     return LIB
 
 

@@ -261,7 +261,9 @@ template <> struct AccPerm<bf16> { typedef StepPairPerm type; };
 // inline asm so that the compiler does not track it: its wait insertion would
 // otherwise treat every later transpose read of LDS as a possible alias of the
 // transfer and wait for all loads in flight. The ring orders these transfers
-// explicitly (wait_loads, then a barrier, before a stage is read).
+// explicitly (wait_loads, then a barrier, before a stage is read). M0 is set
+// inside the asm; the kernels that use it (GEMM, attention) have no compiler-
+// generated M0 use for the asm to disturb.
 __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
 }
