@@ -318,9 +318,10 @@ __global__ void __launch_bounds__(CF::NT, 1) gemm_kernel(GemmArgs a, int k_per_s
 // The loads of tile kt + NS are issued right after the barrier that publishes
 // tile kt + 1, into the stage of tile kt, which every wave has read by then.
 // ============================================================================================
-template <int BM_, int BN_, int WM_, int WN_, int NS_>
+template <int BM_, int BN_, int WM_, int WN_, int NS_, int OCC_ = 1>
 struct PipeTile {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NS = NS_;
+  static constexpr int OCC = OCC_;   // wavefronts per SIMD the register budget must allow
   static constexpr int WAVES = (BM / WM) * (BN / WN);
   static constexpr int NT = 64 * WAVES;
   static constexpr int SLOTS_A = BM * 8, SLOTS_B = BN * 8;       // 16-byte slots per tile
@@ -542,7 +543,7 @@ __device__ __forceinline__ void interleave_reads() {
 }
 
 template <typename TO, bool AK, bool BK, int EPI, class CF>
-__global__ void __launch_bounds__(CF::NT, 1) gemm_pipe_kernel(GemmArgs a, int k_per_split) {
+__global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, int k_per_split) {
   constexpr int BM = CF::BM, BN = CF::BN, WM = CF::WM, WN = CF::WN, NT = CF::NT, NS = CF::NS;
   constexpr int WAVES_N = BN / WN;
   constexpr int BKE = 64;
@@ -634,6 +635,7 @@ int g_tile_override = -1;  // testing hook: force one configuration
 typedef PipeTile<256, 128, 64, 64, 3> P256x128;
 typedef PipeTile<128, 128, 64, 64, 4> P128x128;
 typedef PipeTile<128, 256, 64, 64, 3> P128x256;
+typedef PipeTile<128, 128, 64, 64, 2, 2> P128x128o2;   // two workgroups per CU
 
 template <typename TO, bool AK, bool BK, int EPI, class CF>
 hipError_t launch_pipe(const GemmArgs& a, int splits, hipStream_t st) {
@@ -644,6 +646,19 @@ hipError_t launch_pipe(const GemmArgs& a, int splits, hipStream_t st) {
   const int used = (a.K + kps - 1) / kps;
   hipLaunchKernelGGL((gemm_pipe_kernel<TO, AK, BK, EPI, CF>), dim3(tiles, used), dim3(CF::NT), 0, st, a, kps);
   return hipGetLastError();
+}
+
+int cu_count() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess && hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) ==
+                                                hipSuccess && n > 0)
+      cus = n;
+    else
+      cus = 256;
+  }
+  return cus;
 }
 
 template <typename T, typename TO, bool AK, bool BK, int EPI, class CF>
@@ -677,7 +692,15 @@ hipError_t launch(const GemmArgs& a, int splits, hipStream_t st) {
         case 0: break;  // register-staged kernel, for comparison
         case 11: return launch_pipe<TO, AK, BK, EPI, P128x128>(a, splits, st);
         case 12: return launch_pipe<TO, AK, BK, EPI, P128x256>(a, splits, st);
-        default: return launch_pipe<TO, AK, BK, EPI, P256x128>(a, splits, st);
+        case 10: return launch_pipe<TO, AK, BK, EPI, P256x128>(a, splits, st);
+        case 13: return launch_pipe<TO, AK, BK, EPI, P128x128o2>(a, splits, st);
+        default:
+          // weight gradients (both operands MN-major): 128 x 128 tiles, two
+          // workgroups per CU, so one's epilogue overlaps the other's loop;
+          // forward and dgrad: 256 x 128 tiles, which re-read the weights
+          // half as often (measured faster inside the stage)
+          if constexpr (!AK) return launch_pipe<TO, AK, BK, EPI, P128x128o2>(a, splits, st);
+          else return launch_pipe<TO, AK, BK, EPI, P256x128>(a, splits, st);
       }
     }
   }
@@ -731,24 +754,18 @@ void gemm_set_tile_override(int cfg) { g_tile_override = cfg; }
 
 int gemm_acc_splits(DType dt, int M, int N, int K) {
   // Split-K count for Cf32 += A^T B. Cost model, in microseconds: rounds of
-  // workgroups over the CUs times the k-tiles each runs (one k-tile of a tile
-  // at about 2.3 TFLOP/s per CU), plus the fp32 read-modify-write or atomic
-  // adds of the epilogue (about 2 ps per element and split).
-  static int cus = 0;
-  if (cus == 0) {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) == hipSuccess && hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) ==
-                                                hipSuccess && n > 0)
-      cus = n;
-    else
-      cus = 256;
-  }
+  // workgroups over the resident slots (CUs x workgroups per CU) times the
+  // k-tiles each runs (about 2.3 TFLOP/s per CU, shared by its workgroups),
+  // plus the fp32 read-modify-write or atomic adds of the epilogue (about
+  // 2 ps per element and split).
   const bool pipe = dt == DT_BF16 && K % 8 == 0 && M % 8 == 0 && N % 8 == 0;
-  const int bm = pipe ? P256x128::BM : T128x128::BM, bn = pipe ? P256x128::BN : T128x128::BN;
+  const int bm = pipe ? P128x128o2::BM : T128x128::BM, bn = pipe ? P128x128o2::BN : T128x128::BN;
   const int bk = pipe ? 64 : KVN * (dt == DT_BF16 ? 8 : 4);
+  const int occ = pipe ? P128x128o2::OCC : 1;   // workgroups resident per CU
+  const int cus = cu_count() * occ;
   const double tiles = (double)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
   const int kt = (K + bk - 1) / bk;
-  const double t_k = 2.0 * bm * bn * bk / 2.3e6, t_e = 2e-6 * M * N;
+  const double t_k = 2.0 * bm * bn * bk / (2.3e6 / occ), t_e = 2e-6 * M * N;
   int best = 1;
   double best_t = 1e30;
   for (int sp = 1; sp <= 16 && sp <= kt; sp *= 2) {
