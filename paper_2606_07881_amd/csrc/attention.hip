@@ -188,14 +188,15 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // so every K and V fragment read from LDS feeds QS MFMAs. Key blocks are 64.
 template <int DH> struct FwdRing {
   static constexpr int CPR = DH / 8, KS = DH / 32;
-  static constexpr int QS = DH <= 64 ? 4 : 2, WQ = 16 * QS, BQ = 4 * WQ;
+  static constexpr int QS = DH == 32 ? 4 : (DH == 64 ? 2 : 1), WAVES = DH == 32 ? 4 : 8, NTF = 64 * WAVES;
+  static constexpr int WQ = 16 * QS, BQ = WAVES * WQ;
   static constexpr int NS = DH <= 64 ? 3 : 2;
   static constexpr int BLK = 64 * CPR;          // 16-byte slots per block
-  static constexpr int L = 2 * BLK / NT;        // loads per thread per stage (K and V)
+  static constexpr int L = 2 * BLK / NTF;       // loads per thread per stage (K and V)
 };
 
 template <int DH>
-__global__ void __launch_bounds__(NT, 2) attn_fwd_ring_kernel(const bf16* qkv, bf16* out, float* lse2, int S, int H,
+__global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(const bf16* qkv, bf16* out, float* lse2, int S, int H,
                                                                int d, float scale_log2) {
   using C = FwdRing<DH>;
   constexpr int QS = C::QS, KS = C::KS, NS = C::NS, CPR = C::CPR;
@@ -235,8 +236,8 @@ __global__ void __launch_bounds__(NT, 2) attn_fwd_ring_kernel(const bf16* qkv, b
   auto fill = [&](int kb) {
     const uint32_t st = ring_lds + (uint32_t)((kb % NS) * 2 * C::BLK * 16);
     const int k0 = kb * BKV;
-    blk_fill<CPR, NT>(Kp + (int64_t)k0 * ld, ld, S - k0, st, wu, l);
-    blk_fill<CPR, NT>(Vp + (int64_t)k0 * ld, ld, S - k0, st + C::BLK * 16, wu, l);
+    blk_fill<CPR, C::NTF>(Kp + (int64_t)k0 * ld, ld, S - k0, st, wu, l);
+    blk_fill<CPR, C::NTF>(Vp + (int64_t)k0 * ld, ld, S - k0, st + C::BLK * 16, wu, l);
   };
 #pragma unroll
   for (int t = 0; t < NS - 1; ++t)
@@ -544,14 +545,17 @@ __global__ void __launch_bounds__(NT) attn_bwd_dq_kernel(const T* qkv, const T* 
 //   dQ     per 64 * SUB queries (Q and dO fragments in registers), streaming
 //          64-key blocks of K and V: S^T, dP^T with the query in the lane, then
 //          dQ^T += K^T dS^T, K^T by transpose reads.
+// head_dim 64: 8 wavefronts of 32 rows (two per SIMD, so one's softmax VALU work
+// overlaps the other's MFMAs); 128: 8 of 16 rows; 32: 4 of 64 rows.
 template <int DH> struct BwdRing {
   static constexpr int CPR = DH / 8, KST = DH / 32;
-  static constexpr int SUB = DH <= 64 ? 4 : 2, WR = 16 * SUB, BR = 4 * WR;
+  static constexpr int SUB = DH == 32 ? 4 : (DH == 64 ? 2 : 1), WAVES = DH == 32 ? 4 : 8, NTB = 64 * WAVES;
+  static constexpr int WR = 16 * SUB, BR = WAVES * WR;
   static constexpr int NS = DH <= 64 ? 3 : 2;
   static constexpr int BLK = 64 * CPR;
   static constexpr int PAIR_SLOTS = 32;            // 64 (lse2, D) pairs
   static constexpr int STAGE = 2 * BLK + PAIR_SLOTS;
-  static constexpr int L = 2 * BLK / NT;           // block loads per thread per stage (wave 0 adds the pairs)
+  static constexpr int L = 2 * BLK / NTB;          // block loads per thread per stage (wave 0 adds the pairs)
 };
 
 template <int DH>
@@ -587,7 +591,7 @@ __global__ void __launch_bounds__(NT) attn_pairs_kernel(const bf16* o, const bf1
 }
 
 template <int DH>
-__global__ void __launch_bounds__(NT, 1) attn_dkdv_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
+__global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn_dkdv_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
                                                                 bf16* dqkv, int S, int S_pad, int H, int d,
                                                                 float scale_log2, float scale) {
   using C = BwdRing<DH>;
@@ -627,8 +631,8 @@ __global__ void __launch_bounds__(NT, 1) attn_dkdv_ring_kernel(const bf16* qkv, 
   auto fill = [&](int j) {
     const uint32_t st = ring_lds + (uint32_t)((j % NS) * C::STAGE * 16);
     const int q0 = (qb_first + j) * 64;
-    blk_fill<CPR, NT>(Qp + (int64_t)q0 * ld, ld, S - q0, st, wu, l);
-    blk_fill<CPR, NT>(dOp + (int64_t)q0 * d, d, S - q0, st + C::BLK * 16, wu, l);
+    blk_fill<CPR, C::NTB>(Qp + (int64_t)q0 * ld, ld, S - q0, st, wu, l);
+    blk_fill<CPR, C::NTB>(dOp + (int64_t)q0 * d, d, S - q0, st + C::BLK * 16, wu, l);
     if (wu == 0 && l < C::PAIR_SLOTS) dma16(Pp + (int64_t)q0 * 2 + l * 4, st + 2 * C::BLK * 16);
   };
 #pragma unroll
@@ -726,7 +730,7 @@ __global__ void __launch_bounds__(NT, 1) attn_dkdv_ring_kernel(const bf16* qkv, 
 }
 
 template <int DH>
-__global__ void __launch_bounds__(NT, 1) attn_dq_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
+__global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn_dq_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
                                                               bf16* dqkv, int S, int S_pad, int H, int d,
                                                               float scale_log2, float scale) {
   using C = BwdRing<DH>;
@@ -771,8 +775,8 @@ __global__ void __launch_bounds__(NT, 1) attn_dq_ring_kernel(const bf16* qkv, co
   auto fill = [&](int kb) {
     const uint32_t st = ring_lds + (uint32_t)((kb % NS) * 2 * C::BLK * 16);
     const int k0 = kb * BKV;
-    blk_fill<CPR, NT>(Kp + (int64_t)k0 * ld, ld, S - k0, st, wu, l);
-    blk_fill<CPR, NT>(Vp + (int64_t)k0 * ld, ld, S - k0, st + C::BLK * 16, wu, l);
+    blk_fill<CPR, C::NTB>(Kp + (int64_t)k0 * ld, ld, S - k0, st, wu, l);
+    blk_fill<CPR, C::NTB>(Vp + (int64_t)k0 * ld, ld, S - k0, st + C::BLK * 16, wu, l);
   };
 #pragma unroll
   for (int t = 0; t < NS - 1; ++t)
@@ -860,7 +864,7 @@ hipError_t fwd_launch(const void* qkv, void* o, float* lse2, int mu, int S, int 
   if constexpr (sizeof(T) == 2) {
     using C = FwdRing<DH>;
     dim3 grid(mu * H, (S + C::BQ - 1) / C::BQ);   // x fastest: every head's heaviest query block first
-    hipLaunchKernelGGL((attn_fwd_ring_kernel<DH>), grid, dim3(NT), 0, st, reinterpret_cast<const bf16*>(qkv),
+    hipLaunchKernelGGL((attn_fwd_ring_kernel<DH>), grid, dim3(C::NTF), 0, st, reinterpret_cast<const bf16*>(qkv),
                        reinterpret_cast<bf16*>(o), lse2, S, H, d, scale_log2);
     return hipGetLastError();
   }
@@ -890,11 +894,11 @@ hipError_t bwd_launch(const void* qkv, const void* o, const void* dO, const floa
                        reinterpret_cast<const bf16*>(o), g, lse2, Dbuf, S, S_pad, H, d, rows);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((attn_dkdv_ring_kernel<DH>), dim3(mu * H, (S + C::BR - 1) / C::BR), dim3(NT), 0, st, q, g,
+    hipLaunchKernelGGL((attn_dkdv_ring_kernel<DH>), dim3(mu * H, (S + C::BR - 1) / C::BR), dim3(C::NTB), 0, st, q, g,
                        Dbuf, dq, S, S_pad, H, d, scale_log2, scale);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((attn_dq_ring_kernel<DH>), dim3(mu * H, (S + C::BR - 1) / C::BR), dim3(NT), 0, st, q, g, Dbuf,
+    hipLaunchKernelGGL((attn_dq_ring_kernel<DH>), dim3(mu * H, (S + C::BR - 1) / C::BR), dim3(C::NTB), 0, st, q, g, Dbuf,
                        dq, S, S_pad, H, d, scale_log2, scale);
     return hipGetLastError();
   }
