@@ -61,10 +61,11 @@ hipError_t attn_bwd(DType dt, const void* qkv, const void* o, const void* dO, co
 hipError_t layernorm_fwd(DType dt, const void* x, void* n, float* mean, float* rstd, const float* gamma,
                          const float* beta, void* xcopy, int rows, int d, float eps, hipStream_t st);
 // dx = res + rstd * (g - mean(g) - xhat * mean(g * xhat)), g = dn * gamma (res optional);
-// Ggamma += sum_rows dn * xhat, Gbeta += sum_rows dn (fp32 atomics).
+// Ggamma += sum_rows dn * xhat, Gbeta += sum_rows dn and, if Gdx is not null,
+// Gdx += sum_rows dx (fp32 atomics; the column sums are one pass after dx).
 hipError_t layernorm_bwd(DType dt, const void* dn, const void* x, const float* mean, const float* rstd,
-                         const float* gamma, const void* res, void* dx, float* Ggamma, float* Gbeta, int rows, int d,
-                         hipStream_t st);
+                         const float* gamma, const void* res, void* dx, float* Ggamma, float* Gbeta, float* Gdx,
+                         int rows, int d, hipStream_t st);
 
 // ---- column sums accumulated into fp32 (bias gradients) ---------------------------------
 // G[c] += sum_r Y[r*ld + c], c < ncols (fp32 atomics).

@@ -139,7 +139,9 @@ __global__ void __launch_bounds__(NT) ln_bwd_kernel(const T* __restrict__ dn, co
 // together, the 8 row groups are combined in LDS, and one thread per column
 // adds the workgroup's sum into G. That is T / 64 atomic adds per column.
 // With AFFINE, the sums are of dy * xhat and dy, where
-// xhat = (x - mean) * rstd (the LayerNorm affine gradients).
+// xhat = (x - mean) * rstd (the LayerNorm affine gradients), and, when G3 is
+// given, of the rows of D as well (the LayerNorm's dx: the output-bias
+// gradient of the linear layer before it).
 constexpr int CS_THREADS = 256;
 constexpr int CS_COLV = 32;             // column vectors per workgroup
 constexpr int CS_RG = CS_THREADS / CS_COLV;
@@ -150,23 +152,25 @@ __global__ void __launch_bounds__(CS_THREADS) colsum_atomic_kernel(const T* __re
                                                                     int ncols, const T* __restrict__ x,
                                                                     const float* __restrict__ mean,
                                                                     const float* __restrict__ rstd, float* G,
-                                                                    float* G2) {
+                                                                    float* G2, const T* __restrict__ D, float* G3) {
   constexpr int V = Vec<T>::V;
-  __shared__ float red[AFFINE ? 2 : 1][CS_RG][CS_COLV * V];
+  __shared__ float red[AFFINE ? 3 : 1][CS_RG][CS_COLV * V];
   const int cv = threadIdx.x % CS_COLV, rg = threadIdx.x / CS_COLV;
   const int c0 = (blockIdx.x * CS_COLV + cv) * V;
   const bool colok = c0 < ncols;
   const int r0 = blockIdx.y * CS_ROWS + rg;
-  float a[V], b[V];
+  const bool with_d = AFFINE && G3 != nullptr;   // uniform
+  float a[V], b[V], e[V];
 #pragma unroll
-  for (int j = 0; j < V; ++j) a[j] = b[j] = 0.f;
-  u32x4 yv[CS_RPT], xv[CS_RPT];
+  for (int j = 0; j < V; ++j) a[j] = b[j] = e[j] = 0.f;
+  u32x4 yv[CS_RPT], xv[CS_RPT], dv[CS_RPT];
 #pragma unroll
   for (int i = 0; i < CS_RPT; ++i) {
     const int r = r0 + i * CS_RG;
     const bool ok = colok && r < rows;
     yv[i] = ok ? ld16(Y + (int64_t)r * ld + c0) : u32x4{0, 0, 0, 0};
     if (AFFINE) xv[i] = ok ? ld16(x + (int64_t)r * ld + c0) : u32x4{0, 0, 0, 0};
+    if (AFFINE) dv[i] = (ok && with_d) ? ld16(D + (int64_t)r * ld + c0) : u32x4{0, 0, 0, 0};
   }
 #pragma unroll
   for (int i = 0; i < CS_RPT; ++i) {
@@ -179,6 +183,7 @@ __global__ void __launch_bounds__(CS_THREADS) colsum_atomic_kernel(const T* __re
         const float g = vget<T>(yv[i], j);
         a[j] += g * (vget<T>(xv[i], j) - mu) * rs;
         b[j] += g;
+        e[j] += vget<T>(dv[i], j);
       }
     } else {
 #pragma unroll
@@ -188,20 +193,27 @@ __global__ void __launch_bounds__(CS_THREADS) colsum_atomic_kernel(const T* __re
 #pragma unroll
   for (int j = 0; j < V; ++j) {
     red[0][rg][cv * V + j] = a[j];
-    if (AFFINE) red[AFFINE ? 1 : 0][rg][cv * V + j] = b[j];
+    if (AFFINE) {
+      red[AFFINE ? 1 : 0][rg][cv * V + j] = b[j];
+      red[AFFINE ? 2 : 0][rg][cv * V + j] = e[j];
+    }
   }
   __syncthreads();
   for (int c = threadIdx.x; c < CS_COLV * V; c += CS_THREADS) {
     const int col = blockIdx.x * CS_COLV * V + c;
     if (col >= ncols) continue;
-    float sa = 0.f, sb = 0.f;
+    float sa = 0.f, sb = 0.f, se = 0.f;
 #pragma unroll
     for (int g = 0; g < CS_RG; ++g) {
       sa += red[0][g][c];
-      if (AFFINE) sb += red[AFFINE ? 1 : 0][g][c];
+      if (AFFINE) {
+        sb += red[AFFINE ? 1 : 0][g][c];
+        se += red[AFFINE ? 2 : 0][g][c];
+      }
     }
     atomicAdd(G + col, sa);
     if (AFFINE) atomicAdd(G2 + col, sb);
+    if (with_d) atomicAdd(G3 + col, se);
   }
 }
 
@@ -215,7 +227,7 @@ hipError_t ln_fwd_launch(const void* x, void* n, float* mean, float* rstd, const
 
 template <typename T, int MAXV>
 hipError_t ln_bwd_launch(const void* dn, const void* x, const float* mean, const float* rstd, const float* gamma,
-                         const void* res, void* dx, float* Gg, float* Gb, int rows, int d, hipStream_t st) {
+                         const void* res, void* dx, float* Gg, float* Gb, float* Gd, int rows, int d, hipStream_t st) {
   hipLaunchKernelGGL((ln_bwd_kernel<T, MAXV>), dim3((rows + 3) / 4), dim3(NT), 0, st, reinterpret_cast<const T*>(dn),
                      reinterpret_cast<const T*>(x), mean, rstd, gamma, reinterpret_cast<const T*>(res),
                      reinterpret_cast<T*>(dx), rows, d);
@@ -224,7 +236,8 @@ hipError_t ln_bwd_launch(const void* dn, const void* x, const float* mean, const
   constexpr int V = Vec<T>::V;
   const dim3 grid((d / V + CS_COLV - 1) / CS_COLV, (rows + CS_ROWS - 1) / CS_ROWS);
   hipLaunchKernelGGL((colsum_atomic_kernel<T, true>), grid, dim3(CS_THREADS), 0, st, reinterpret_cast<const T*>(dn),
-                     (int64_t)d, rows, d, reinterpret_cast<const T*>(x), mean, rstd, Gg, Gb);
+                     (int64_t)d, rows, d, reinterpret_cast<const T*>(x), mean, rstd, Gg, Gb,
+                     reinterpret_cast<const T*>(dx), Gd);
   return hipGetLastError();
 }
 
@@ -247,12 +260,12 @@ hipError_t ln_fwd_t(const void* x, void* n, float* mean, float* rstd, const floa
 
 template <typename T>
 hipError_t ln_bwd_t(const void* dn, const void* x, const float* mean, const float* rstd, const float* gamma,
-                    const void* res, void* dx, float* Gg, float* Gb, int rows, int d, hipStream_t st) {
+                    const void* res, void* dx, float* Gg, float* Gb, float* Gd, int rows, int d, hipStream_t st) {
   const int mv = maxv_for<T>(d);
-  if (mv <= 1) return ln_bwd_launch<T, 1>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, rows, d, st);
-  if (mv <= 2) return ln_bwd_launch<T, 2>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, rows, d, st);
-  if (mv <= 4) return ln_bwd_launch<T, 4>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, rows, d, st);
-  if (mv <= 8) return ln_bwd_launch<T, 8>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, rows, d, st);
+  if (mv <= 1) return ln_bwd_launch<T, 1>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, Gd, rows, d, st);
+  if (mv <= 2) return ln_bwd_launch<T, 2>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, Gd, rows, d, st);
+  if (mv <= 4) return ln_bwd_launch<T, 4>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, Gd, rows, d, st);
+  if (mv <= 8) return ln_bwd_launch<T, 8>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, Gd, rows, d, st);
   return hipErrorInvalidValue;
 }
 
@@ -266,11 +279,11 @@ hipError_t layernorm_fwd(DType dt, const void* x, void* n, float* mean, float* r
 }
 
 hipError_t layernorm_bwd(DType dt, const void* dn, const void* x, const float* mean, const float* rstd,
-                         const float* gamma, const void* res, void* dx, float* Gg, float* Gb, int rows, int d,
-                         hipStream_t st) {
+                         const float* gamma, const void* res, void* dx, float* Gg, float* Gb, float* Gd, int rows,
+                         int d, hipStream_t st) {
   if (rows <= 0 || d <= 0 || d % 8) return hipErrorInvalidValue;
-  if (dt == DT_BF16) return ln_bwd_t<bf16>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, rows, d, st);
-  return ln_bwd_t<float>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, rows, d, st);
+  if (dt == DT_BF16) return ln_bwd_t<bf16>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, Gd, rows, d, st);
+  return ln_bwd_t<float>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, Gd, rows, d, st);
 }
 
 hipError_t colsum_acc(DType dt, const void* Y, int64_t ld, int rows, int ncols, float* G, hipStream_t st) {
@@ -279,10 +292,12 @@ hipError_t colsum_acc(DType dt, const void* Y, int64_t ld, int rows, int ncols, 
   const dim3 grid((ncols / V + CS_COLV - 1) / CS_COLV, (rows + CS_ROWS - 1) / CS_ROWS);
   if (dt == DT_BF16)
     hipLaunchKernelGGL((colsum_atomic_kernel<bf16, false>), grid, dim3(CS_THREADS), 0, st,
-                       reinterpret_cast<const bf16*>(Y), ld, rows, ncols, nullptr, nullptr, nullptr, G, nullptr);
+                       reinterpret_cast<const bf16*>(Y), ld, rows, ncols, nullptr, nullptr, nullptr, G, nullptr,
+                       nullptr, nullptr);
   else
     hipLaunchKernelGGL((colsum_atomic_kernel<float, false>), grid, dim3(CS_THREADS), 0, st,
-                       reinterpret_cast<const float*>(Y), ld, rows, ncols, nullptr, nullptr, nullptr, G, nullptr);
+                       reinterpret_cast<const float*>(Y), ld, rows, ncols, nullptr, nullptr, nullptr, G, nullptr,
+                       nullptr, nullptr);
   return hipGetLastError();
 }
 

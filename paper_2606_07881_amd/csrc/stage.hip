@@ -476,12 +476,15 @@ int ln_fwd(paci_stage* h, const void* x, void* n, float* mean, float* rstd, int6
   });
 }
 
+// gd_off >= 0: also accumulate sum_rows dx into that gradient (the output-bias
+// gradient of the linear layer that produced x, or of the block before)
 int ln_bwd(paci_stage* h, const void* dn, const void* x, const float* mean, const float* rstd, int64_t g_off,
-           int64_t b_off, const void* res, void* dx) {
+           int64_t b_off, const void* res, void* dx, int64_t gd_off = -1) {
   const int T = (int)h->L.T, d = h->s.d_model;
-  return run(h, F_LN_BWD, (double)T * d * (res ? 4 : 3) * h->esz + 8.0 * T, [&] {  // dx pass; the affine pass rereads dn, x
-    return paci::layernorm_bwd(h->dt, dn, x, mean, rstd, h->th(g_off), res, dx, h->g(g_off), h->g(b_off), T, d,
-                               h->st);
+  // dx pass (dn, x, res in, dx out) and column pass (dn, x and, for gd_off, dx again)
+  return run(h, F_LN_BWD, (double)T * d * ((res ? 4 : 3) + 2 + (gd_off >= 0 ? 1 : 0)) * h->esz + 8.0 * T, [&] {
+    return paci::layernorm_bwd(h->dt, dn, x, mean, rstd, h->th(g_off), res, dx, h->g(g_off), h->g(b_off),
+                               gd_off >= 0 ? h->g(gd_off) : nullptr, T, d, h->st);
   });
 }
 
@@ -517,7 +520,9 @@ int blocks_fwd(paci_stage* h, char* sl, const void* in, bool copy_in, void* out)
 }
 
 // ---- backward of one block: dy -> dx ------------------------------------------------------------
-int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx) {
+// dy_bias_done: G_b2 of this block already holds sum dy (accumulated by the
+// LayerNorm backward that produced dy)
+int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx, bool dy_bias_done) {
   const paci_shapes& s = h->s;
   const int T = (int)h->L.T, d = s.d_model, f = s.d_ff;
   const BlockRefs& b = h->p.blocks[l];
@@ -530,18 +535,17 @@ int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx) {
   char* dqkv = h->ws(L.w_dqkv);
   // y = x1 + a W2^T + b2
   TRY(linear_wgrad(h, dy, d, sl + o.a, f, d, f, T, b.w_2));
-  TRY(bias_grad(h, dy, d, T, d, b.b_2));
+  if (!dy_bias_done) TRY(bias_grad(h, dy, d, T, d, b.b_2));
   TRY(linear_dgrad(h, dy, d, b.w_2, T, f, d, paci::EPI_GELU_GRAD, du, sl + o.u));
   // u = n2 W1^T + b1
   TRY(linear_wgrad(h, du, f, sl + o.n2, d, f, d, T, b.w_1));
   TRY(bias_grad(h, du, f, T, f, b.b_1));
   TRY(linear_dgrad(h, du, f, b.w_1, T, d, f, paci::EPI_STORE, dn, nullptr));
-  // n2 = LN2(x1); dx1 = dy + LN2 backward
+  // n2 = LN2(x1); dx1 = dy + LN2 backward, and G_bo += sum dx1
   TRY(ln_bwd(h, dn, sl + o.x1, reinterpret_cast<const float*>(sl + o.mean2),
-             reinterpret_cast<const float*>(sl + o.rstd2), b.ln2_g, b.ln2_b, dy, dx1));
+             reinterpret_cast<const float*>(sl + o.rstd2), b.ln2_g, b.ln2_b, dy, dx1, b.b_o));
   // x1 = x + o Wo^T + bo
   TRY(linear_wgrad(h, dx1, d, sl + o.o, d, d, d, T, b.w_o));
-  TRY(bias_grad(h, dx1, d, T, d, b.b_o));
   TRY(linear_dgrad(h, dx1, d, b.w_o, T, d, d, paci::EPI_STORE, dO, nullptr));
   // attention
   TRY(run(h, F_ATTN_BWD, 8.0 * attn_pairs(s) * s.head_dim, [&] {
@@ -553,9 +557,11 @@ int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx) {
   TRY(linear_wgrad(h, dqkv, 3 * d, sl + o.n1, d, 3 * d, d, T, b.w_qkv));
   TRY(bias_grad(h, dqkv, 3 * d, T, 3 * d, b.b_qkv));
   TRY(linear_dgrad(h, dqkv, 3 * d, b.w_qkv, T, d, 3 * d, paci::EPI_STORE, dn, nullptr));
-  // n1 = LN1(x); dx = dx1 + LN1 backward
+  // n1 = LN1(x); dx = dx1 + LN1 backward; dx is the output gradient of block l - 1,
+  // so G_b2 of that block += sum dx
   TRY(ln_bwd(h, dn, sl + o.x, reinterpret_cast<const float*>(sl + o.mean1),
-             reinterpret_cast<const float*>(sl + o.rstd1), b.ln1_g, b.ln1_b, dx1, dx));
+             reinterpret_cast<const float*>(sl + o.rstd1), b.ln1_g, b.ln1_b, dx1, dx,
+             l > 0 ? h->p.blocks[l - 1].b_2 : -1));
   return PACI_OK;
 }
 
@@ -783,9 +789,10 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
     });
     if (!r) r = linear_wgrad(h, dz, L.ldz, sl + L.s_nf, d, s.vocab, d, T, h->p.w_lm);
     if (!r) r = linear_dgrad(h, dz, L.ldz, h->p.w_lm, T, d, s.vocab, paci::EPI_STORE, dnf, nullptr);
-    if (!r)
+    if (!r)   // the last block's output gradient; G_b2 of that block += its column sums
       r = ln_bwd(h, dnf, sl + L.s_y, reinterpret_cast<const float*>(sl + L.s_meanf),
-                 reinterpret_cast<const float*>(sl + L.s_rstdf), h->p.lnf_g, h->p.lnf_b, nullptr, bufA);
+                 reinterpret_cast<const float*>(sl + L.s_rstdf), h->p.lnf_g, h->p.lnf_b, nullptr, bufA,
+                 h->p.blocks[s.n_layers - 1].b_2);
     dy = bufA;
   }
   for (int l = s.n_layers - 1; l >= 0 && !r; --l) {
@@ -794,7 +801,8 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
       dx = dev_grad_in;
     else
       dx = (dy == bufA) ? bufB : bufA;
-    r = block_bwd(h, sl, l, dy, dx);
+    // every block's dy but the given stage output gradient came out of a LayerNorm backward
+    r = block_bwd(h, sl, l, dy, dx, l < s.n_layers - 1 || s.kind == PACI_LAST);
     dy = dx;
   }
   if (!r && s.kind == PACI_FIRST) {
