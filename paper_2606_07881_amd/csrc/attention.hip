@@ -590,13 +590,41 @@ __global__ void __launch_bounds__(NT) attn_pairs_kernel(const bf16* o, const bf1
   }
 }
 
+// Column sums of the gradient tiles a workgroup holds, for the bias gradient of
+// the qkv projection: lane l holds columns 4 (l >> 4) + r of 16-column tile t,
+// for token l & 15; the 16 lanes of equal l >> 4 (one DPP row) are summed with
+// row moves, the waves through LDS (red: WAVES * NCOL floats, free for this
+// use), and each column goes out as one atomic add to gbias[col(c)].
+template <int WAVES, int NCOL, class Col>
+__device__ __forceinline__ void colsum_tiles(float (&v)[NCOL / 16][4], float* red, float* gbias, Col col) {
+  const int w = threadIdx.x >> 6, l = lane_id(), g = l >> 4;
+#pragma unroll
+  for (int t = 0; t < NCOL / 16; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[t][r] = row_sum16(v[t][r]);
+  if ((l & 15) == 0) {
+#pragma unroll
+    for (int t = 0; t < NCOL / 16; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) red[w * NCOL + t * 16 + 4 * g + r] = v[t][r];
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < NCOL; c += WAVES * 64) {
+    float sum = 0.f;
+#pragma unroll
+    for (int u = 0; u < WAVES; ++u) sum += red[u * NCOL + c];
+    atomicAdd(gbias + col(c), sum);
+  }
+}
+
 template <int DH>
 __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn_dkdv_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
                                                                 bf16* dqkv, int S, int S_pad, int H, int d,
-                                                                float scale_log2, float scale) {
+                                                                float scale_log2, float scale, float* gbias) {
   using C = BwdRing<DH>;
   constexpr int SUB = C::SUB, KST = C::KST, NS = C::NS, CPR = C::CPR;
   __shared__ u32x4 ring[NS * C::STAGE];
+  static_assert(NS * C::STAGE * 4 >= C::WAVES * 2 * DH, "LDS for the column sums");
   const int kb = blockIdx.y;                     // smallest keys first: they see the most queries
   const int bh = blockIdx.x, b = bh / H, h = bh % H;
   const int w = threadIdx.x >> 6, l = lane_id(), g = l >> 4;
@@ -727,15 +755,35 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
       }
     }
   }
+  if (gbias != nullptr) {   // uniform: G_bqkv += column sums of dK and dV over this workgroup's keys
+    float v[2 * DH / 16][4];
+#pragma unroll
+    for (int t = 0; t < DH / 16; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float sk = 0.f, sv = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < SUB; ++ks) {
+          sk += adk[ks][t][r];
+          sv += adv[ks][t][r];
+        }
+        v[t][r] = sk * scale;
+        v[DH / 16 + t][r] = sv;
+      }
+    __syncthreads();   // every wave is done with the ring
+    colsum_tiles<C::WAVES, 2 * DH>(v, reinterpret_cast<float*>(ring), gbias,
+                                   [&](int c) { return (c < DH ? d : 2 * d - DH) + h * DH + c; });
+  }
 }
 
 template <int DH>
 __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn_dq_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
                                                               bf16* dqkv, int S, int S_pad, int H, int d,
-                                                              float scale_log2, float scale) {
+                                                              float scale_log2, float scale, float* gbias) {
   using C = BwdRing<DH>;
   constexpr int SUB = C::SUB, KST = C::KST, NS = C::NS, CPR = C::CPR;
   __shared__ u32x4 ring[NS * 2 * C::BLK];
+  static_assert(NS * 2 * C::BLK * 4 >= C::WAVES * DH, "LDS for the column sums");
   const int nqb = (S + C::BR - 1) / C::BR;
   const int qb = nqb - 1 - blockIdx.y;           // largest queries first: they see the most keys
   const int bh = blockIdx.x, b = bh / H, h = bh % H;
@@ -855,6 +903,20 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
                   pack_bf16x2(adq[qs][t][2] * scale, adq[qs][t][3] * scale)};
     }
   }
+  if (gbias != nullptr) {   // uniform: G_bqkv += column sums of dQ over this workgroup's queries
+    float v[DH / 16][4];
+#pragma unroll
+    for (int t = 0; t < DH / 16; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float sq = 0.f;
+#pragma unroll
+        for (int qs = 0; qs < SUB; ++qs) sq += adq[qs][t][r];
+        v[t][r] = sq * scale;
+      }
+    __syncthreads();   // every wave is done with the ring
+    colsum_tiles<C::WAVES, DH>(v, reinterpret_cast<float*>(ring), gbias, [&](int c) { return h * DH + c; });
+  }
 }
 
 template <typename T, int DH>
@@ -876,7 +938,7 @@ hipError_t fwd_launch(const void* qkv, void* o, float* lse2, int mu, int S, int 
 
 template <typename T, int DH>
 hipError_t bwd_launch(const void* qkv, const void* o, const void* dO, const float* lse2, float* Dbuf, void* dqkv,
-                      int mu, int S, int H, hipStream_t st) {
+                      float* gbias, int mu, int S, int H, hipStream_t st) {
   const int d = H * DH;
   const float scale = 1.f / sqrtf((float)DH);
   const float scale_log2 = LOG2E * scale;
@@ -895,11 +957,11 @@ hipError_t bwd_launch(const void* qkv, const void* o, const void* dO, const floa
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((attn_dkdv_ring_kernel<DH>), dim3(mu * H, (S + C::BR - 1) / C::BR), dim3(C::NTB), 0, st, q, g,
-                       Dbuf, dq, S, S_pad, H, d, scale_log2, scale);
+                       Dbuf, dq, S, S_pad, H, d, scale_log2, scale, gbias);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((attn_dq_ring_kernel<DH>), dim3(mu * H, (S + C::BR - 1) / C::BR), dim3(C::NTB), 0, st, q, g, Dbuf,
-                       dq, S, S_pad, H, d, scale_log2, scale);
+                       dq, S, S_pad, H, d, scale_log2, scale, gbias);
     return hipGetLastError();
   }
   constexpr int LPR = DH / Vec<T>::V;
@@ -917,7 +979,9 @@ hipError_t bwd_launch(const void* qkv, const void* o, const void* dO, const floa
   hipLaunchKernelGGL((attn_bwd_dq_kernel<T, DH>), dim3((S + 63) / 64, mu * H), dim3(NT), 0, st,
                      reinterpret_cast<const T*>(qkv), reinterpret_cast<const T*>(dO), lse2, Dbuf,
                      reinterpret_cast<T*>(dqkv), S, H, d, scale_log2, scale);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e != hipSuccess || gbias == nullptr) return e;
+  return colsum_acc(sizeof(T) == 2 ? DT_BF16 : DT_F32, dqkv, 3 * d, mu * S, 3 * d, gbias, st);
 }
 
 template <typename T>
@@ -935,12 +999,13 @@ hipError_t fwd_dh(const void* qkv, void* o, float* lse2, int mu, int S, int H, i
 
 template <typename T>
 hipError_t bwd_dh(const void* qkv, const void* o, const void* dO, const float* lse2, float* Dbuf, void* dqkv,
-                  int mu, int S, int H, int dh, hipStream_t st) {
+                  float* gbias, int mu, int S, int H, int dh, hipStream_t st) {
   switch (dh) {
-    case 32: return bwd_launch<T, 32>(qkv, o, dO, lse2, Dbuf, dqkv, mu, S, H, st);
-    case 64: return bwd_launch<T, 64>(qkv, o, dO, lse2, Dbuf, dqkv, mu, S, H, st);
+    case 32: return bwd_launch<T, 32>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, st);
+    case 64: return bwd_launch<T, 64>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, st);
     case 128:
-      if constexpr (sizeof(T) == 2) return bwd_launch<T, 128>(qkv, o, dO, lse2, Dbuf, dqkv, mu, S, H, st);
+      if constexpr (sizeof(T) == 2)
+        return bwd_launch<T, 128>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, st);
       break;
   }
   return hipErrorInvalidValue;
@@ -960,10 +1025,10 @@ int64_t attn_bwd_workspace_floats(DType dt, int mu, int S, int H) {
 }
 
 hipError_t attn_bwd(DType dt, const void* qkv, const void* o, const void* dO, const float* lse2, float* Dbuf,
-                    void* dqkv, int mu, int S, int H, int dh, hipStream_t st) {
+                    void* dqkv, float* gbias, int mu, int S, int H, int dh, hipStream_t st) {
   if (mu <= 0 || S <= 0 || H <= 0) return hipErrorInvalidValue;
-  if (dt == DT_BF16) return bwd_dh<bf16>(qkv, o, dO, lse2, Dbuf, dqkv, mu, S, H, dh, st);
-  return bwd_dh<float>(qkv, o, dO, lse2, Dbuf, dqkv, mu, S, H, dh, st);
+  if (dt == DT_BF16) return bwd_dh<bf16>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, dh, st);
+  return bwd_dh<float>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, dh, st);
 }
 
 }  // namespace paci

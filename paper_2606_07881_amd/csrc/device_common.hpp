@@ -247,6 +247,21 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // 2^x by the hardware instruction alone: results below 2^-126 flush to zero
 // (exp2f adds a rescaling sequence around it to return denormals).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Sum over the 16 lanes of a DPP row (lanes 16k .. 16k + 15), returned to every
+// lane of the row: data-parallel moves within the row (swap neighbours, swap
+// pairs, reverse each half row, reverse the row) with no LDS traffic.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float row_sum16(float v) {
+  v += dpp_f<0xB1>(v);    // quad_perm [1, 0, 3, 2]
+  v += dpp_f<0x4E>(v);    // quad_perm [2, 3, 0, 1]
+  v += dpp_f<0x141>(v);   // row_half_mirror
+  v += dpp_f<0x140>(v);   // row_mirror
+  return v;
+}
 template <> __device__ __forceinline__ u32x4 acc_to_frag<bf16>(const floatx4* tiles, int s) {
   const floatx4 a = tiles[2 * s], b = tiles[2 * s + 1];
   return u32x4{pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3])};

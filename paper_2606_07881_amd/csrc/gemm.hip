@@ -380,7 +380,8 @@ __device__ __forceinline__ void pipe_fill(const bf16* src, int64_t ld, int row0,
 // unit column for all its rows, so the bias is loaded once; the aux rows of
 // all passes are loaded before any store, so their latencies overlap.
 template <typename TO, int EPI, int BN, int PR, int NT>
-__device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, int mb, int n0, int tid) {
+__device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, int mb, int n0, int tid,
+                                           float (&csum)[16 / sizeof(TO)]) {
   constexpr int U = 16 / sizeof(TO), UPR = BN / U, RPI = NT / UPR, P = PR / RPI;
   static_assert(NT % UPR == 0 && PR % RPI == 0, "units must tile the panel");
   constexpr int LDC = BN + 4;
@@ -459,6 +460,11 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
         o[j] = x;
       }
     }
+    if (a.colsum != nullptr) {
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (j < nv) csum[j] += o[j];
+    }
     TO* C = reinterpret_cast<TO*>(a.C);
     if (vec) {
       if constexpr (sizeof(TO) == 2) {
@@ -503,7 +509,11 @@ template <typename TO, int EPI, class CF, int N_I, int N_J>
 __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, float* cl, int m0, int n0, int wm0, int wn0,
                                                 const floatx4 (&acc)[N_I][N_J]) {
   constexpr int BM = CF::BM, BN = CF::BN, NT = CF::NT, LDC = CF::LDC, PR = CF::PR;
+  constexpr int U = 16 / sizeof(TO), UPR = BN / U;
   const int tid = threadIdx.x, l = lane_id();
+  float csum[U];
+#pragma unroll
+  for (int j = 0; j < U; ++j) csum[j] = 0.f;
 #pragma unroll
   for (int p = 0; p < BM / PR; ++p) {
     __syncthreads();   // every wave is done with the ring (or with the previous panel)
@@ -525,7 +535,30 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, float* cl, in
         if (m < a.M && n < a.N) atomicAdd(C + (int64_t)m * a.ldc + n, cl[r * LDC + c]);
       }
     } else {
-      staged_out<TO, EPI, BN, PR, NT>(a, cl, mb, n0, tid);
+      staged_out<TO, EPI, BN, PR, NT>(a, cl, mb, n0, tid, csum);
+    }
+  }
+  if constexpr (EPI != EPI_ATOMIC && UPR <= 64 && 64 % UPR == 0) {
+    if (a.colsum != nullptr) {   // uniform: column sums of the tile's output into a.colsum
+      // threads with equal tid % UPR hold the same columns: lanes l, l ^ UPR, ... within a
+      // wavefront, then the wavefronts through LDS, then one atomic per column
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+#pragma unroll
+        for (int off = UPR; off < 64; off *= 2) csum[j] += __shfl_xor(csum[j], off, 64);
+      __syncthreads();   // every thread is done reading the staged tile
+      const int w = tid >> 6;
+      if (l < UPR) {
+#pragma unroll
+        for (int j = 0; j < U; ++j) cl[w * BN + l * U + j] = csum[j];
+      }
+      __syncthreads();
+      for (int c = tid; c < BN; c += NT) {
+        float sum = 0.f;
+#pragma unroll
+        for (int v = 0; v < NT / 64; ++v) sum += cl[v * BN + c];
+        if (n0 + c < a.N) atomicAdd(a.colsum + n0 + c, sum);
+      }
     }
   }
 }
@@ -704,7 +737,13 @@ hipError_t launch(const GemmArgs& a, int splits, hipStream_t st) {
       }
     }
   }
-  return launch_cf<T, TO, AK, BK, EPI, T128x128>(a, splits, st);
+  hipError_t e = launch_cf<T, TO, AK, BK, EPI, T128x128>(a, splits, st);
+  if constexpr (EPI != EPI_ATOMIC && EPI != EPI_ACC) {
+    // the register-staged epilogue has no column sums: one pass over the output
+    if (e == hipSuccess && a.colsum != nullptr)
+      e = colsum_acc(sizeof(TO) == 2 ? DT_BF16 : DT_F32, a.C, a.ldc, a.M, a.N, a.colsum, st);
+  }
+  return e;
 }
 
 template <typename T, typename TO, bool AK, bool BK>
@@ -782,6 +821,7 @@ int gemm_acc_splits(DType dt, int M, int N, int K) {
 hipError_t gemm(DType dt, bool out_f32, GemmLayout lay, GemmEpi epi, const GemmArgs& a, int splits,
                 hipStream_t st) {
   if (a.M <= 0 || a.N <= 0 || a.K <= 0 || splits < 1) return hipErrorInvalidValue;
+  if (a.colsum != nullptr && (epi == EPI_ACC || epi == EPI_ATOMIC)) return hipErrorInvalidValue;
   if (dt == DT_BF16) return by_layout<bf16>(out_f32, lay, epi, a, splits, st);
   return by_layout<float>(out_f32, lay, epi, a, splits, st);
 }

@@ -33,6 +33,7 @@ struct GemmArgs {
   const void* aux; int64_t ld_aux;
   void* C2;
   const void* zeros;  // >= 16 bytes of device zeros (bf16 path: source of out-of-range tile slots)
+  float* colsum = nullptr;  // optional: += column sums of the output C (non-accumulating epilogues, bf16 path)
 };
 // bf16 operands: K-major vectors that straddle K read the memory just past K,
 // which must hold zeros (true when K % 8 == 0, or for zero-padded rows).
@@ -51,10 +52,11 @@ void gemm_set_tile_override(int cfg);
 // Forward: o [T, d]; lse2 [mu*H*S] = log2-sum-exp2 of the scaled scores in log2 units.
 hipError_t attn_fwd(DType dt, const void* qkv, void* o, float* lse2, int mu, int S, int H, int dh, hipStream_t st);
 // Backward: D = rowsum(dO * O) per (b, h, query), then dK, dV and dQ into dqkv [T, 3d].
-// Dbuf is workspace of attn_bwd_workspace_floats() floats.
+// Dbuf is workspace of attn_bwd_workspace_floats() floats. gbias (optional, fp32 [3d]):
+// += the column sums of dqkv, i.e. the gradient of the qkv projection's bias.
 int64_t attn_bwd_workspace_floats(DType dt, int mu, int S, int H);
 hipError_t attn_bwd(DType dt, const void* qkv, const void* o, const void* dO, const float* lse2, float* Dbuf,
-                    void* dqkv, int mu, int S, int H, int dh, hipStream_t st);
+                    void* dqkv, float* gbias, int mu, int S, int H, int dh, hipStream_t st);
 
 // ---- LayerNorm -----------------------------------------------------------------------
 // n = (x - mean) * rstd * gamma + beta, per row of d; xcopy (optional) receives x.

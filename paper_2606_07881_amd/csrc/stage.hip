@@ -445,9 +445,11 @@ int linear_fwd(paci_stage* h, const void* X, int64_t w_off, int64_t b_off, int M
 }
 
 // dX [M, N] = dY [M, K] . W [K, N]   (W = nn.Linear weight [out = K, in = N])
+// colsum_off >= 0: also accumulate the column sums of dX into that gradient
 int linear_dgrad(paci_stage* h, const void* dY, int64_t ldy, int64_t w_off, int M, int N, int K, paci::GemmEpi epi,
-                 void* C, const void* aux) {
+                 void* C, const void* aux, int64_t colsum_off = -1) {
   paci::GemmArgs a{dY, ldy, h->W(w_off), N, M, N, K, C, N, nullptr, aux, N, nullptr, h->arena + h->L.zeros};
+  if (colsum_off >= 0) a.colsum = h->g(colsum_off);
   return run(h, F_GEMM_DGRAD, 2.0 * M * N * K,
              [&] { return paci::gemm(h->dt, false, paci::GEMM_NN, epi, a, 1, h->st); });
 }
@@ -536,10 +538,10 @@ int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx, bool dy_
   // y = x1 + a W2^T + b2
   TRY(linear_wgrad(h, dy, d, sl + o.a, f, d, f, T, b.w_2));
   if (!dy_bias_done) TRY(bias_grad(h, dy, d, T, d, b.b_2));
-  TRY(linear_dgrad(h, dy, d, b.w_2, T, f, d, paci::EPI_GELU_GRAD, du, sl + o.u));
+  // du = (dy W2) * gelu'(u), and G_b1 += sum du in the same epilogue
+  TRY(linear_dgrad(h, dy, d, b.w_2, T, f, d, paci::EPI_GELU_GRAD, du, sl + o.u, b.b_1));
   // u = n2 W1^T + b1
   TRY(linear_wgrad(h, du, f, sl + o.n2, d, f, d, T, b.w_1));
-  TRY(bias_grad(h, du, f, T, f, b.b_1));
   TRY(linear_dgrad(h, du, f, b.w_1, T, d, f, paci::EPI_STORE, dn, nullptr));
   // n2 = LN2(x1); dx1 = dy + LN2 backward, and G_bo += sum dx1
   TRY(ln_bwd(h, dn, sl + o.x1, reinterpret_cast<const float*>(sl + o.mean2),
@@ -547,15 +549,14 @@ int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx, bool dy_
   // x1 = x + o Wo^T + bo
   TRY(linear_wgrad(h, dx1, d, sl + o.o, d, d, d, T, b.w_o));
   TRY(linear_dgrad(h, dx1, d, b.w_o, T, d, d, paci::EPI_STORE, dO, nullptr));
-  // attention
+  // attention; G_bqkv += sum dqkv in the same kernels
   TRY(run(h, F_ATTN_BWD, 8.0 * attn_pairs(s) * s.head_dim, [&] {
     return paci::attn_bwd(h->dt, sl + o.qkv, sl + o.o, dO, reinterpret_cast<const float*>(sl + o.lse2),
-                          reinterpret_cast<float*>(h->ws(L.w_D)), dqkv, s.micro_batch, s.seq, s.n_heads, s.head_dim,
-                          h->st);
+                          reinterpret_cast<float*>(h->ws(L.w_D)), dqkv, h->g(b.b_qkv), s.micro_batch, s.seq,
+                          s.n_heads, s.head_dim, h->st);
   }));
   // qkv = n1 Wqkv^T + bqkv
   TRY(linear_wgrad(h, dqkv, 3 * d, sl + o.n1, d, 3 * d, d, T, b.w_qkv));
-  TRY(bias_grad(h, dqkv, 3 * d, T, 3 * d, b.b_qkv));
   TRY(linear_dgrad(h, dqkv, 3 * d, b.w_qkv, T, d, 3 * d, paci::EPI_STORE, dn, nullptr));
   // n1 = LN1(x); dx = dx1 + LN1 backward; dx is the output gradient of block l - 1,
   // so G_b2 of that block += sum dx
