@@ -133,13 +133,17 @@ __global__ void __launch_bounds__(NT) attn_fwd_kernel(const T* qkv, T* out, floa
 // bf16 kernels on an LDS ring. A block is 64 consecutive rows (keys or
 // queries) of one head, [64][dh] bf16, copied by direct-to-LDS loads into a
 // ring of NS stages so that the next blocks load while one is used. Row r's
-// 16-byte chunk c sits at chunk c ^ blk_swz(r): both fragment reads of 16
-// rows at one chunk (ds_read_b128) and transpose reads of 4 rows x 2 chunks
-// per 16 lanes (ds_read_b64_tr_b16) then hit distinct LDS banks.
+// 16-byte chunk c sits at chunk c ^ blk_swz(r). Fragment reads (ds_read_b128)
+// take 16 rows at one chunk per 16 lanes; transpose reads (ds_read_b64_tr_b16)
+// take 4 rows x 2 chunks per 16 lanes, two lane groups (8 rows) per cycle. At
+// 8 and 16 chunks per row the swizzle sends row bits 0, 2, 1 to chunk bits 0,
+// 1, 2 (and row bit 0 also to chunk bit 3 at 16): both kinds of read then hit
+// every LDS bank once per cycle, which bank-conflict counters confirm.
 template <int CPR> __device__ __forceinline__ int blk_swz(int r) {
   if constexpr (CPR == 4) return (r >> 2) & 3;
-  else if constexpr (CPR == 8) return (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
-  else return ((r & 7) << 1) | ((r >> 3) & 1);
+  const int f = (r & 1) | (((r >> 2) & 1) << 1) | (((r >> 1) & 1) << 2);
+  if constexpr (CPR == 8) return f;
+  else return f | ((r & 1) << 3);
 }
 template <int CPR> __device__ __forceinline__ int blk_slot(int r, int c) { return r * CPR + (c ^ blk_swz<CPR>(r)); }
 

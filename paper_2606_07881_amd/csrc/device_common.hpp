@@ -134,8 +134,17 @@ template <int ROWS> __device__ __forceinline__ u32x4 lds_frag(const u32x4* tile,
 // If lane c addresses line kb + c / 4, rows r0 + 4 (c % 4) .. + 3, lane j
 // receives rows r0 + j of lines kb .. kb + 3. Two such reads (kb and kb + 4)
 // give the 8 contracted values an MFMA step wants, with no register transpose.
+// MN-major operand tile in LDS: row k holds ROWS elements as 16-byte chunks,
+// chunk j stored at chunk j ^ trt_swz(k). A transpose read takes 4 rows x 2
+// chunks per 16 lanes, and the hardware serves two such lane groups (rows k
+// and k + 8) per cycle: bits 1-2 of the swizzle separate the 4 rows of a
+// group, bit 3 the two groups, so the 64 banks are hit once per cycle.
+template <int ROWS> __device__ __forceinline__ int trt_swz(int k) {
+  if constexpr (ROWS >= 128) return ((k & 3) << 1) ^ (((k >> 3) & 1) << 3);
+  else return (k & 3) << 1;
+}
 template <int ROWS> __device__ __forceinline__ int trt_elem(int k, int r) {
-  return k * ROWS + ((((r >> 3) ^ ((k & 3) << 1))) << 3) + (r & 7);
+  return k * ROWS + (((r >> 3) ^ trt_swz<ROWS>(k)) << 3) + (r & 7);
 }
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 template <int ROWS> __device__ __forceinline__ u32x4 lds_frag_tr(const u32x4* tile, int s, int row0) {

@@ -366,7 +366,7 @@ __device__ __forceinline__ void pipe_fill(const bf16* src, int64_t ld, int row0,
     } else {
       constexpr int CPL = ROWS / 8;
       const int line = slot / CPL;
-      const int c = (slot % CPL) ^ ((line & 3) << 1);
+      const int c = (slot % CPL) ^ trt_swz<ROWS>(line);
       const int k = k0 + line, rb = row0 + c * 8;
       ok = (k < k_end) && (rb < rows_total);
       g = src + (int64_t)k * ld + rb;
