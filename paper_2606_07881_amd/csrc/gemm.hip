@@ -344,15 +344,13 @@ template <int ROWS> __device__ __forceinline__ u32x4 pipe_frag_k(const u32x4* ti
 }
 
 
-// Issue this thread's loads of one operand tile (ROWS rows x 64 contracted).
-// `tile` is the LDS byte address of the operand's part of the stage, `w` the
-// wave index (wave-uniform).
+// Issue load p (of ROWS * 8 / NT) of this thread's loads of one operand tile
+// (ROWS rows x 64 contracted). `tile` is the LDS byte address of the operand's
+// part of the stage, `w` the wave index (wave-uniform).
 template <int ROWS, bool KMAJ, int NT>
-__device__ __forceinline__ void pipe_fill(const bf16* src, int64_t ld, int row0, int rows_total, int k0, int k_end,
-                                          uint32_t tile, const void* zeros, int w, int l) {
-  constexpr int L = ROWS * 8 / NT;
-#pragma unroll
-  for (int p = 0; p < L; ++p) {
+__device__ __forceinline__ void pipe_fill_one(int p, const bf16* src, int64_t ld, int row0, int rows_total, int k0,
+                                              int k_end, uint32_t tile, const void* zeros, int w, int l) {
+  {
     const int blk = p * (NT / 64) + w;        // wave-uniform block of 64 slots
     const int slot = blk * 64 + l;
     const void* g;
@@ -596,11 +594,31 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
 
   const uint32_t smem_lds = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) u32x4*)smem);
   const int wu = __builtin_amdgcn_readfirstlane(w);
-  auto fill = [&](int kt) {
+  // load p of the L loads of tile kt (the A operand's first, then B's)
+  auto fill_one = [&](int kt, int p) {
     const uint32_t st = smem_lds + (uint32_t)((kt % NS) * CF::STAGE_SLOTS * 16);
     const int k0 = k_begin + kt * BKE;
-    pipe_fill<BM, AK, NT>(A, a.lda, m0, a.M, k0, k_end, st, a.zeros, wu, l);
-    pipe_fill<BN, BK, NT>(B, a.ldb, n0, a.N, k0, k_end, st + CF::SLOTS_A * 16, a.zeros, wu, l);
+    if (p < CF::LA) {
+      pipe_fill_one<BM, AK, NT>(p, A, a.lda, m0, a.M, k0, k_end, st, a.zeros, wu, l);
+    } else if constexpr (!AK && !BK) {
+      // weight gradients: B may come in segments of seg_rows contracted rows
+      // (a tile never straddles two); past k_end the rows are masked as usual
+      const bf16* Bs = B;
+      int kb = k0, ke = k_end;
+      if (a.seg_rows > 0) {
+        const int sg = k0 / (int)a.seg_rows;
+        Bs = B + (int64_t)((a.seg_first + sg) % a.seg_count) * a.seg_stride;
+        kb = k0 - sg * (int)a.seg_rows;
+        ke = k_end - sg * (int)a.seg_rows;
+      }
+      pipe_fill_one<BN, BK, NT>(p - CF::LA, Bs, a.ldb, n0, a.N, kb, ke, st + CF::SLOTS_A * 16, a.zeros, wu, l);
+    } else {
+      pipe_fill_one<BN, BK, NT>(p - CF::LA, B, a.ldb, n0, a.N, k0, k_end, st + CF::SLOTS_A * 16, a.zeros, wu, l);
+    }
+  };
+  auto fill = [&](int kt) {
+#pragma unroll
+    for (int p = 0; p < L; ++p) fill_one(kt, p);
   };
 
   floatx4 acc[WM / 16][WN / 16];
@@ -632,12 +650,27 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
 #pragma unroll
       for (int j = 0; j < WN / 16; ++j) mma_step<bf16>(acc[i][j], xf[j], yf[i]);
   };
+  // fragment f of step s (A's fragments first, then B's), and MFMA q of a step
+  auto read_frag = [&](int kt, int s, int f, u32x4* yf, u32x4* xf) {
+    const u32x4* sa = smem + (kt % NS) * CF::STAGE_SLOTS;
+    const u32x4* sb = sa + CF::SLOTS_A;
+    if (f < WM / 16) yf[f] = AK ? pipe_frag_k<BM>(sa, s, wm0 + f * 16) : lds_frag_tr<BM>(sa, s, wm0 + f * 16);
+    else {
+      const int j = f - WM / 16;
+      xf[j] = BK ? pipe_frag_k<BN>(sb, s, wn0 + j * 16) : lds_frag_tr<BN>(sb, s, wn0 + j * 16);
+    }
+  };
+  auto mma_one = [&](int q, const u32x4* yf, const u32x4* xf) {
+    const int i = q / (WN / 16), j = q % (WN / 16);
+    mma_step<bf16>(acc[i][j], xf[j], yf[i]);
+  };
 
   // The loop body has no branches: fills past the last tile read the zero page
   // and the reads after the last tile are discarded. Within each MFMA step the
   // scheduler spreads the LDS reads of the next step between the MFMAs.
   constexpr int NRI = (AK ? 1 : 2) * (WM / 16) + (BK ? 1 : 2) * (WN / 16);   // LDS read instructions per step
   constexpr int NM = (WM / 16) * (WN / 16);                                 // MFMAs per step
+  constexpr int NF = WM / 16 + WN / 16;                                      // fragments per step
 #pragma unroll
   for (int t = 0; t < NS; ++t) fill(t);
   wait_vmcnt<L * (NS - 1)>();
@@ -651,10 +684,27 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
     wait_lds_reads();     // reads of yb/xb
     wait_vmcnt<L * (NS - 2)>();   // tile kt + 1 has landed; kt + 2 .. kt + NS - 1 may be in flight
     barrier_no_fence();
-    fill(kt + NS);                // into the stage of tile kt, which every wave has read
-    read_step(kt + 1, 0, ya, xa);
-    mma_all(yb, xb);
-    interleave_reads<NRI, NM>();
+    // Refill the stage of tile kt (every wave has read it) with tile kt + NS.
+    if constexpr (AK && BK) {
+      // One load at a time between the MFMAs of this step and the reads of
+      // the next: the loads of all waves of the CU reach the address unit
+      // spread over the step instead of in one burst that holds up the MFMAs
+      // (measured faster with both operands K-major, slower with MN-major ones).
+#pragma unroll
+      for (int p = 0; p < L; ++p) {
+        fill_one(kt + NS, p);
+#pragma unroll
+        for (int f = p * NF / L; f < (p + 1) * NF / L; ++f) read_frag(kt + 1, 0, f, ya, xa);
+#pragma unroll
+        for (int q = p * NM / L; q < (p + 1) * NM / L; ++q) mma_one(q, yb, xb);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+      fill(kt + NS);
+      read_step(kt + 1, 0, ya, xa);
+      mma_all(yb, xb);
+      interleave_reads<NRI, NM>();
+    }
   }
   wait_vmcnt<0>();   // the fills past the last tile, before the ring is reused
   staged_epilogue<TO, EPI, CF>(a, reinterpret_cast<float*>(smem), m0, n0, wm0, wn0, acc);
@@ -719,6 +769,14 @@ bool pipe_eligible(const GemmArgs& a) {
 
 template <typename T, typename TO, bool AK, bool BK, int EPI>
 hipError_t launch(const GemmArgs& a, int splits, hipStream_t st) {
+  if (a.seg_rows > 0) {
+    // segmented B: the pipelined 128 x 128 TN kernel only
+    if constexpr (sizeof(T) == 2 && !AK && !BK) {
+      if (pipe_eligible<AK, BK>(a) && a.seg_rows % 64 == 0 && a.seg_count >= 1 && a.seg_first >= 0)
+        return launch_pipe<TO, AK, BK, EPI, P128x128o2>(a, splits, st);
+    }
+    return hipErrorInvalidValue;
+  }
   if constexpr (sizeof(T) == 2) {
     if (pipe_eligible<AK, BK>(a)) {
       switch (g_tile_override) {

@@ -34,6 +34,11 @@ struct GemmArgs {
   void* C2;
   const void* zeros;  // >= 16 bytes of device zeros (bf16 path: source of out-of-range tile slots)
   float* colsum = nullptr;  // optional: += column sums of the output C (non-accumulating epilogues, bf16 path)
+  // optional (TN layout, bf16 path): operand B's contracted rows come in segments of
+  // seg_rows rows (a multiple of 64); segment s starts at B + seg_stride elements
+  // times ((seg_first + s) % seg_count), each with row stride ldb
+  int64_t seg_rows = 0, seg_stride = 0;
+  int seg_first = 0, seg_count = 1;
 };
 // bf16 operands: K-major vectors that straddle K read the memory just past K,
 // which must hold zeros (true when K % 8 == 0, or for zero-padded rows).

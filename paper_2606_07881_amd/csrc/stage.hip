@@ -3,13 +3,23 @@
 // One stage of the asynchronous 1F1B pipeline (Alg. 1): a protocol object
 // holding the counters (version t, window count c, unresolved forwards q),
 // a single fp32 parameter copy, the fp32 gradient accumulator G, the AdamW
-// moments, and an activation store of delay + 1 micro-batch slots. All of it
-// is sub-allocated from one caller-owned device arena. Forward, backward and
+// moments, and an activation store of micro-batch slots. All of it is
+// sub-allocated from one caller-owned device arena. Forward, backward and
 // step enqueue the hand-written kernels on one in-order HIP stream. Stream
-// order alone guards the buffers. A slot is rewritten by F(mb + delay + 1)
-// only after B(mb) has consumed it. The update runs after the K-th
-// backward's gradient kernels. The next forward reads the refreshed bf16
-// weights after the update.
+// order alone guards the buffers. The update runs after the K-th backward's
+// gradient kernels. The next forward reads the refreshed bf16 weights after
+// the update.
+//
+// Weight gradients of the blocks (bf16 stages whose micro-batch token count is
+// a multiple of 64) are windowed: each backward keeps its output gradients
+// (dqkv, dx1, du, dy of every block) in a per-window buffer, and the K
+// micro-batches' G_W += dY^T X products run as one long contraction per weight
+// before the update (or before G is read, loaded or the counters reset). The
+// sum is the same; G is read-modified once per window instead of once per
+// micro-batch. The saved activations X then have to outlive the window: the
+// store keeps K + delay slots (delay + 1 otherwise); the slot of mb is reused
+// by F(mb + K + delay), which the protocol admits only after the update that
+// closes mb's window.
 //
 // Drift semantics (Eq. 1): a backward differentiates the activations saved by
 // its forward but reads the current parameters. dgrad uses the current bf16
@@ -242,7 +252,11 @@ struct Layout {
   size_t theta, G, m, v, theta16, chunks, zeros;
   int nchunks = 0;
   size_t stash, slot_bytes;
+  int n_slots = 1;             // activation slots: delay + 1, or K + delay with windowed weight gradients
+  bool window = false;         // weight gradients windowed (see the header)
   std::vector<BlockSlot> blk;  // per block, inside a slot
+  struct WinBlock { size_t dqkv, dx1, du, dy; };   // per block: [K * T, width] each
+  std::vector<WinBlock> win;
   size_t s_ids = 0, s_tgt = 0, s_y = 0, s_meanf = 0, s_rstdf = 0, s_nf = 0, s_z = 0, s_lse_ce = 0;
   // workspace
   size_t w_dyA, w_dyB, w_du, w_dn, w_dx1, w_do, w_dqkv, w_D, w_part, w_dz = 0, w_dnf = 0, w_loss = 0;
@@ -258,7 +272,6 @@ int count_chunks(const ParamTable& p) {
 }
 
 Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) {
-  (void)K;
   Layout L;
   const int64_t esz = s.dtype == PACI_BF16 ? 2 : 4;
   const int64_t d = s.d_model, f = s.d_ff, T = (int64_t)s.micro_batch * s.seq;
@@ -306,7 +319,19 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
     L.s_lse_ce = sl.take(4 * T);
   }
   L.slot_bytes = (sl.off + 255) & ~(size_t)255;
-  L.stash = a.take(L.slot_bytes * (size_t)(delay + 1));
+  L.window = s.dtype == PACI_BF16 && T % 64 == 0 && d % 8 == 0 && f % 8 == 0;
+  L.n_slots = L.window ? K + delay : delay + 1;
+  L.stash = a.take(L.slot_bytes * (size_t)L.n_slots);
+  if (L.window) {
+    for (int l = 0; l < s.n_layers; ++l) {
+      Layout::WinBlock w;
+      w.dqkv = a.take(esz * (size_t)K * T * 3 * d);
+      w.dx1 = a.take(esz * (size_t)K * T * d);
+      w.du = a.take(esz * (size_t)K * T * f);
+      w.dy = a.take(esz * (size_t)K * T * d);
+      L.win.push_back(w);
+    }
+  }
 
   // backward workspace (one micro-batch at a time)
   L.w_dyA = a.take(esz * T * d);
@@ -355,6 +380,7 @@ struct paci_stage {
   int esz;
   int last_hip = 0;
   bool broken = false;
+  int win_done = 0;   // micro-batches of the current window whose weight gradients are in G
 
   // timing
   bool timing = false;
@@ -375,7 +401,9 @@ struct paci_stage {
   }
   const float* th(int64_t off) const { return theta() + off; }
   float* g(int64_t off) const { return G() + off; }
-  char* slot(int mb) const { return arena + L.stash + (size_t)(mb % (fsm.delay + 1)) * L.slot_bytes; }
+  char* slot(int mb) const { return arena + L.stash + (size_t)(mb % L.n_slots) * L.slot_bytes; }
+  // window buffer of block l, tensor at offset off, micro-batch j of the window, width columns
+  char* win(size_t off, int j, int width) const { return arena + off + (size_t)j * L.T * width * esz; }
   char* ws(size_t off) const { return arena + off; }
 };
 
@@ -524,30 +552,33 @@ int blocks_fwd(paci_stage* h, char* sl, const void* in, bool copy_in, void* out)
 // ---- backward of one block: dy -> dx ------------------------------------------------------------
 // dy_bias_done: G_b2 of this block already holds sum dy (accumulated by the
 // LayerNorm backward that produced dy)
-int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx, bool dy_bias_done) {
+// j: the micro-batch's position in its window (windowed weight gradients: the
+// block's output gradients go to the window buffer and G_W waits for the flush)
+int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx, bool dy_bias_done, int j) {
   const paci_shapes& s = h->s;
   const int T = (int)h->L.T, d = s.d_model, f = s.d_ff;
   const BlockRefs& b = h->p.blocks[l];
   const BlockSlot& o = h->L.blk[l];
   const Layout& L = h->L;
-  char* du = h->ws(L.w_du);
+  const bool win = L.window;
+  char* du = win ? h->win(L.win[l].du, j, f) : h->ws(L.w_du);
   char* dn = h->ws(L.w_dn);
-  char* dx1 = h->ws(L.w_dx1);
+  char* dx1 = win ? h->win(L.win[l].dx1, j, d) : h->ws(L.w_dx1);
   char* dO = h->ws(L.w_do);
-  char* dqkv = h->ws(L.w_dqkv);
+  char* dqkv = win ? h->win(L.win[l].dqkv, j, 3 * d) : h->ws(L.w_dqkv);
   // y = x1 + a W2^T + b2
-  TRY(linear_wgrad(h, dy, d, sl + o.a, f, d, f, T, b.w_2));
+  if (!win) TRY(linear_wgrad(h, dy, d, sl + o.a, f, d, f, T, b.w_2));
   if (!dy_bias_done) TRY(bias_grad(h, dy, d, T, d, b.b_2));
   // du = (dy W2) * gelu'(u), and G_b1 += sum du in the same epilogue
   TRY(linear_dgrad(h, dy, d, b.w_2, T, f, d, paci::EPI_GELU_GRAD, du, sl + o.u, b.b_1));
   // u = n2 W1^T + b1
-  TRY(linear_wgrad(h, du, f, sl + o.n2, d, f, d, T, b.w_1));
+  if (!win) TRY(linear_wgrad(h, du, f, sl + o.n2, d, f, d, T, b.w_1));
   TRY(linear_dgrad(h, du, f, b.w_1, T, d, f, paci::EPI_STORE, dn, nullptr));
   // n2 = LN2(x1); dx1 = dy + LN2 backward, and G_bo += sum dx1
   TRY(ln_bwd(h, dn, sl + o.x1, reinterpret_cast<const float*>(sl + o.mean2),
              reinterpret_cast<const float*>(sl + o.rstd2), b.ln2_g, b.ln2_b, dy, dx1, b.b_o));
   // x1 = x + o Wo^T + bo
-  TRY(linear_wgrad(h, dx1, d, sl + o.o, d, d, d, T, b.w_o));
+  if (!win) TRY(linear_wgrad(h, dx1, d, sl + o.o, d, d, d, T, b.w_o));
   TRY(linear_dgrad(h, dx1, d, b.w_o, T, d, d, paci::EPI_STORE, dO, nullptr));
   // attention; G_bqkv += sum dqkv in the same kernels
   TRY(run(h, F_ATTN_BWD, 8.0 * attn_pairs(s) * s.head_dim, [&] {
@@ -556,7 +587,7 @@ int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx, bool dy_
                           s.n_heads, s.head_dim, h->st);
   }));
   // qkv = n1 Wqkv^T + bqkv
-  TRY(linear_wgrad(h, dqkv, 3 * d, sl + o.n1, d, 3 * d, d, T, b.w_qkv));
+  if (!win) TRY(linear_wgrad(h, dqkv, 3 * d, sl + o.n1, d, 3 * d, d, T, b.w_qkv));
   TRY(linear_dgrad(h, dqkv, 3 * d, b.w_qkv, T, d, 3 * d, paci::EPI_STORE, dn, nullptr));
   // n1 = LN1(x); dx = dx1 + LN1 backward; dx is the output gradient of block l - 1,
   // so G_b2 of that block += sum dx
@@ -567,6 +598,56 @@ int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx, bool dy_
 }
 
 size_t act_bytes(const paci_stage* h) { return (size_t)h->L.T * h->s.d_model * h->esz; }
+
+// G[out, in] += dY^T X over micro-batches j0 .. j0 + n - 1 of the window: dY from the
+// window buffer (contiguous), X from the activation slots of those micro-batches
+// (first micro-batch mb0), one contracted segment of T rows per slot.
+// Split-K count for these long contractions (128 x 128 output tiles): about 1536
+// workgroups, each split at least 8192 contracted rows, at most 16 splits
+// (measured best on MI355X for 64K-row weight gradients at d = 1024).
+int window_splits(int out, int in, int64_t Kt) {
+  const int64_t tiles = (int64_t)((out + 127) / 128) * ((in + 127) / 128);
+  const int by_rows = (int)std::min<int64_t>(16, Kt / 8192);
+  return std::max(1, std::min(by_rows, (int)std::lround(1536.0 / (double)tiles)));
+}
+
+int window_wgrad(paci_stage* h, size_t dy_off, size_t x_off, int out, int in, int j0, int n, int mb0,
+                 int64_t g_off) {
+  const Layout& L = h->L;
+  const int64_t Kt = (int64_t)n * L.T;
+  const int splits = window_splits(out, in, Kt);
+  paci::GemmArgs a{h->win(dy_off, j0, out), out, h->arena + L.stash + x_off, in, out, in, (int)Kt, h->g(g_off), in,
+                   nullptr, nullptr, 0, nullptr, h->arena + L.zeros};
+  a.seg_rows = L.T;
+  a.seg_stride = (int64_t)(L.slot_bytes / (size_t)h->esz);
+  a.seg_first = mb0 % L.n_slots;
+  a.seg_count = L.n_slots;
+  const paci::GemmEpi epi = splits > 1 ? paci::EPI_ATOMIC : paci::EPI_ACC;
+  return run(h, F_GEMM_WGRAD, 2.0 * out * in * (double)Kt,
+             [&] { return paci::gemm(h->dt, true, paci::GEMM_TN, epi, a, splits, h->st); });
+}
+
+// Adds the weight gradients of the window's micro-batches not yet in G (Alg. 1
+// accumulates them per backward; the sum is the same).
+int flush_window(paci_stage* h) {
+  const Layout& L = h->L;
+  if (!L.window) return PACI_OK;
+  const int c = h->fsm.c, j0 = h->win_done;
+  if (c <= j0) return PACI_OK;
+  const int n = c - j0, mb0 = h->fsm.next_b - c + j0;
+  const int d = h->s.d_model, f = h->s.d_ff;
+  for (int l = 0; l < h->s.n_layers; ++l) {
+    const BlockRefs& b = h->p.blocks[l];
+    const BlockSlot& o = L.blk[l];
+    const Layout::WinBlock& w = L.win[l];
+    TRY(window_wgrad(h, w.dy, o.a, d, f, j0, n, mb0, b.w_2));
+    TRY(window_wgrad(h, w.du, o.n2, f, d, j0, n, mb0, b.w_1));
+    TRY(window_wgrad(h, w.dx1, o.o, d, d, j0, n, mb0, b.w_o));
+    TRY(window_wgrad(h, w.dqkv, o.n1, 3 * d, d, j0, n, mb0, b.w_qkv));
+  }
+  h->win_done = c;
+  return PACI_OK;
+}
 
 }  // namespace
 
@@ -682,6 +763,7 @@ extern "C" int paci_stage_load(paci_stage* h, int what, const float* src, int64_
   if (h->broken) return PACI_E_HIP;
   float* dst = state_ptr(h, what);
   if (!dst) return PACI_E_INVAL;
+  if (what == PACI_GRADS) TRY(flush_window(h));   // pending products belong to the G being replaced
   hipError_t e = hipMemcpyAsync(dst, src, (size_t)n * 4, on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice,
                                 h->st);
   if (e == hipSuccess && what == PACI_PARAMS && h->dt == paci::DT_BF16)
@@ -699,6 +781,7 @@ extern "C" int paci_stage_read(paci_stage* h, int what, float* dst, int64_t n, i
   if (h->broken) return PACI_E_HIP;
   const float* src = state_ptr(h, what);
   if (!src) return PACI_E_INVAL;
+  if (what == PACI_GRADS) TRY(flush_window(h));
   hipError_t e = hipMemcpyAsync(dst, src, (size_t)n * 4, on_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost,
                                 h->st);
   if (e == hipSuccess && !on_device) e = hipStreamSynchronize(h->st);
@@ -777,6 +860,10 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
   char* bufA = h->ws(L.w_dyA);
   char* bufB = h->ws(L.w_dyB);
   const void* dy = dev_grad_out;
+  const int j = h->fsm.c;   // position in the window
+  const bool win = L.window;
+  // windowed: every block's output gradient lives in the window buffer
+  char* dy_last = win ? h->win(L.win[s.n_layers - 1].dy, j, d) : bufA;
   int r = PACI_OK;
   if (s.kind == PACI_LAST) {
     const float* z = reinterpret_cast<const float*>(sl + L.s_z);
@@ -792,18 +879,25 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
     if (!r) r = linear_dgrad(h, dz, L.ldz, h->p.w_lm, T, d, s.vocab, paci::EPI_STORE, dnf, nullptr);
     if (!r)   // the last block's output gradient; G_b2 of that block += its column sums
       r = ln_bwd(h, dnf, sl + L.s_y, reinterpret_cast<const float*>(sl + L.s_meanf),
-                 reinterpret_cast<const float*>(sl + L.s_rstdf), h->p.lnf_g, h->p.lnf_b, nullptr, bufA,
+                 reinterpret_cast<const float*>(sl + L.s_rstdf), h->p.lnf_g, h->p.lnf_b, nullptr, dy_last,
                  h->p.blocks[s.n_layers - 1].b_2);
-    dy = bufA;
+    dy = dy_last;
+  } else if (win) {
+    r = run(h, F_COPY, 2.0 * act_bytes(h), [&] {
+      return hipMemcpyAsync(dy_last, dev_grad_out, act_bytes(h), hipMemcpyDeviceToDevice, h->st);
+    });
+    dy = dy_last;
   }
   for (int l = s.n_layers - 1; l >= 0 && !r; --l) {
     void* dx;
     if (l == 0 && s.kind != PACI_FIRST && dev_grad_in)
       dx = dev_grad_in;
+    else if (l > 0 && win)
+      dx = h->win(L.win[l - 1].dy, j, d);
     else
       dx = (dy == bufA) ? bufB : bufA;
     // every block's dy but the given stage output gradient came out of a LayerNorm backward
-    r = block_bwd(h, sl, l, dy, dx, l < s.n_layers - 1 || s.kind == PACI_LAST);
+    r = block_bwd(h, sl, l, dy, dx, l < s.n_layers - 1 || s.kind == PACI_LAST, j);
     dy = dx;
   }
   if (!r && s.kind == PACI_FIRST) {
@@ -832,6 +926,7 @@ extern "C" int paci_stage_step(paci_stage* h, int* new_version) {
   a.weight_decay = s.weight_decay;
   a.bc1 = (float)(1.0 - std::pow((double)s.beta1, t_adam));
   a.bc2 = (float)(1.0 - std::pow((double)s.beta2, t_adam));
+  TRY(flush_window(h));
   const int r = run(h, F_ADAMW, 30.0 * (double)h->p.total, [&] {
     return paci::adamw(h->theta(), h->G(), h->m(), h->v(),
                        h->dt == paci::DT_BF16 ? (void*)(h->arena + h->L.theta16) : nullptr,
@@ -839,6 +934,7 @@ extern "C" int paci_stage_step(paci_stage* h, int* new_version) {
   });
   if (r) return r;
   fsm_commit_step(h->fsm);
+  h->win_done = 0;
   if (new_version) *new_version = h->fsm.t;
   return PACI_OK;
 }
@@ -897,6 +993,8 @@ extern "C" int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, cons
 
 extern "C" int paci_stage_reset_counters(paci_stage* h) {
   if (!h) return PACI_E_INVAL;
+  if (!h->broken) TRY(flush_window(h));   // G keeps what the backwards so far accumulated
+  h->win_done = 0;
   h->fsm.t = h->fsm.c = h->fsm.q = h->fsm.next_f = h->fsm.next_b = 0;
   return PACI_OK;
 }

@@ -81,6 +81,9 @@ def small_cfg(name, **kw):
                             micro_batch=2, K=4, delay=3, M=12, dtype="bf16"),
         "ragged_fp32": dict(kind="middle", n_layers=2, d_model=96, n_heads=3, head_dim=32, d_ff=320, seq=100,
                             micro_batch=2, K=3, delay=2, M=9, dtype="fp32"),
+        # T = 128 (a multiple of 64): bf16 weight gradients windowed over K = 3 micro-batches
+        "win_bf16": dict(kind="middle", n_layers=2, d_model=128, n_heads=2, head_dim=64, d_ff=384, seq=64,
+                         micro_batch=2, K=3, delay=2, M=9, dtype="bf16"),
         "dh128_bf16": dict(kind="middle", n_layers=1, d_model=256, n_heads=2, head_dim=128, d_ff=512, seq=160,
                            micro_batch=2, K=2, delay=1, M=6, dtype="bf16"),
         "dh32_bf16": dict(kind="middle", n_layers=1, d_model=128, n_heads=4, head_dim=32, d_ff=256, seq=96,
@@ -158,7 +161,8 @@ def unflatten(c, flat, table=None):
 
 
 # ---- GPU replay, driven event by event through the C ABI --------------------------------------
-def gpu_replay(c, inp, events=None, K=None, delay=None):
+def gpu_replay(c, inp, events=None, K=None, delay=None, read_mid=False):
+    """read_mid: also read G (and drop it) after the first backward of every window."""
     import torch
     from paper_2606_07881_amd import binding
     K = c["K"] if K is None else K
@@ -192,6 +196,8 @@ def gpu_replay(c, inp, events=None, K=None, delay=None):
                 gins[i] = torch.zeros(T, d, dtype=act, device="cuda")
                 gi = gins[i]
             rec["tB"][i], _ = st.backward(i, go, gi)
+            if read_mid and i % K == 0:
+                st.read(binding.GRADS)
         else:
             rec["G"].append(unflatten(c, st.read(binding.GRADS)))
             st.step()
