@@ -132,9 +132,13 @@ int paci_param_info_at(const paci_shapes* s, int index, paci_param_info* out); /
 
 /* ---- stage lifetime --------------------------------------------------------- */
 /* Bytes of device memory the stage needs: fp32 parameters, G, AdamW moments,
- * the bf16 working copy (bf16 stages), an activation store of delay + 1
- * micro-batch slots and the backward workspace. E_INVAL / E_UNSUPPORTED as for
- * paci_stage_init. */
+ * the bf16 working copy (bf16 stages), the activation store and the backward
+ * workspace. The store has delay + 1 micro-batch slots, or K + delay when the
+ * block weight gradients are windowed (bf16 stages with micro_batch * seq a
+ * multiple of 64 and d, d_ff multiples of 8): such a stage also keeps every
+ * block's output gradients of the K micro-batches of a window, and computes the
+ * window's weight gradients as one contraction per weight (see stage_backward).
+ * E_INVAL / E_UNSUPPORTED as for paci_stage_init. */
 int paci_stage_arena_bytes(const paci_shapes* s, int K, int delay, size_t* bytes);
 
 /* stage_init(shapes, K, delay). `dev_arena` is caller-owned device memory of
@@ -156,7 +160,9 @@ enum paci_what { PACI_PARAMS = 0, PACI_GRADS = 1, PACI_EXP_AVG = 2, PACI_EXP_AVG
  * equal the stage's element count (paci_param_count). `src`/`dst` are device
  * pointers if `on_device` is non-zero, else host pointers (the call then
  * synchronizes the stream). Loading PARAMS also rewrites the bf16 working copy.
- * E_INVAL on a wrong count or null pointer. */
+ * Reading or loading GRADS first adds any windowed weight gradients still
+ * pending, so G always holds every backward so far. E_INVAL on a wrong count
+ * or null pointer. */
 int paci_stage_load(paci_stage* h, int what, const float* src, int64_t n, int on_device);
 int paci_stage_read(paci_stage* h, int what, float* dst, int64_t n, int on_device);
 
@@ -167,8 +173,8 @@ int paci_stage_read(paci_stage* h, int what, float* dst, int64_t n, int on_devic
  * Middle/first stage: `dev_out` receives [T, d] (stage dtype). Last stage:
  * `dev_targets` are int32 [micro_batch, seq] in [0, vocab) and `dev_out`
  * receives one fp32, the mean cross-entropy over the T tokens.
- * The input is copied into the activation store (slot mb % (delay + 1)), so the
- * caller may reuse `dev_in` once the stream has passed this call. *version
+ * The input is copied into the activation store (slot mb modulo the slot
+ * count), so the caller may reuse `dev_in` once the stream has passed this call. *version
  * receives t^F; q is incremented.
  * Errors (state unchanged): E_ORDER (mb != next_f), E_BACKPRESSURE (q > delay),
  * E_STEP_PENDING (an update is due), E_INVAL (null pointer). */
@@ -178,7 +184,10 @@ int paci_stage_forward(paci_stage* h, int mb, const void* dev_in, const int32_t*
 /* stage_backward(mb, grad_out): B_i of micro-batch mb. It differentiates the
  * activations stored by F_mb at the parameters current now (Eq. 1: a stale
  * backward reads the newest version, with no weight stash), adds the local
- * gradient to the fp32 accumulator G, and writes the input gradient.
+ * gradient to the fp32 accumulator G, and writes the input gradient. On a
+ * windowed stage the block weight gradients are added later, all K of the
+ * window in one contraction per weight, before the update (or an earlier
+ * read of G): the same sum up to fp32 rounding order.
  * Middle/first stage: `dev_grad_out` is dL/d(out) [T, d] (stage dtype). Last
  * stage: `dev_grad_out` must be NULL; the backward is seeded with
  * (softmax(z) - onehot(target)) / (T * K). `dev_grad_in` receives dL/d(in)
@@ -211,7 +220,8 @@ int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, const int32_t* 
                    int32_t* host_stamps);
 
 /* Rewinds the counters to t = c = q = 0, next_f = next_b = 0, keeping
- * parameters and moments (used to replay again from the current state). */
+ * parameters, moments and G (pending windowed weight gradients are added to G
+ * first); used to replay again from the current state. */
 int paci_stage_reset_counters(paci_stage* h);
 
 /* ---- introspection ------------------------------------------------------------- */
