@@ -311,7 +311,7 @@ __global__ void __launch_bounds__(CF::NT, 1) gemm_kernel(GemmArgs a, int k_per_s
 //   K-major   [row][8 vectors of k], vector kv stored at kv ^ ((row >> 1) & 7);
 //             8 lanes fetch one 128-byte row segment, and a 16-row fragment
 //             read touches 16 distinct bank groups;
-//   MN-major  [k][rows] with 16-byte chunk c of line k at c ^ ((k & 3) << 1),
+//   MN-major  [k][rows] with 16-byte chunk c of line k at c ^ trt_swz(k),
 //             read by ds_read_b64_tr_b16 (see lds_frag_tr).
 // Slots outside the operand (rows past M or N, k past K) are filled from a
 // zero page, so the ring never holds stale data and the k tail sums exactly.

@@ -108,5 +108,7 @@ hipError_t adamw(float* theta, float* G, float* m, float* v, void* theta_bf16, c
                  const AdamwArgs& a, hipStream_t st);
 // dst (bf16) = round-to-nearest-even(src), n elements.
 hipError_t f32_to_bf16(const float* src, void* dst, int64_t n, hipStream_t st);
+// dst [cols, rows] = src [rows, cols]^T for 16-bit elements; rows, cols multiples of 8.
+hipError_t transpose16(const void* src, void* dst, int rows, int cols, hipStream_t st);
 
 }  // namespace paci

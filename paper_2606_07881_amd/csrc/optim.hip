@@ -51,7 +51,41 @@ __global__ void __launch_bounds__(NT) f32_to_bf16_kernel(const float* __restrict
   }
 }
 
+// dst [cols, rows] = src [rows, cols]^T, 16-bit elements, through a 64 x 64 LDS
+// tile; rows and cols multiples of 8 (whole 16-byte vectors on both sides).
+__global__ void __launch_bounds__(NT) transpose16_kernel(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
+                                                         int rows, int cols) {
+  __shared__ uint16_t t[64][64 + 8];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  for (int q = threadIdx.x; q < 512; q += NT) {
+    const int r = q >> 3, ch = q & 7;
+    const int gr = r0 + r, gc = c0 + ch * 8;
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (gr < rows && gc < cols) v = *reinterpret_cast<const u32x4*>(src + (int64_t)gr * cols + gc);
+    *reinterpret_cast<u32x4*>(&t[r][ch * 8]) = v;
+  }
+  __syncthreads();
+  for (int q = threadIdx.x; q < 512; q += NT) {
+    const int cc = q >> 3, ch = q & 7;
+    const int gr = c0 + cc, gc = r0 + ch * 8;
+    if (gr < cols && gc < rows) {
+      u32x4 o;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        o[j] = (uint32_t)t[ch * 8 + 2 * j][cc] | ((uint32_t)t[ch * 8 + 2 * j + 1][cc] << 16);
+      *reinterpret_cast<u32x4*>(dst + (int64_t)gr * rows + gc) = o;
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t transpose16(const void* src, void* dst, int rows, int cols, hipStream_t st) {
+  if (rows <= 0 || cols <= 0 || rows % 8 || cols % 8) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(transpose16_kernel, dim3((cols + 63) / 64, (rows + 63) / 64), dim3(NT), 0, st,
+                     reinterpret_cast<const uint16_t*>(src), reinterpret_cast<uint16_t*>(dst), rows, cols);
+  return hipGetLastError();
+}
 
 hipError_t adamw(float* theta, float* G, float* m, float* v, void* theta_bf16, const int4* chunks, int nchunks,
                  const AdamwArgs& a, hipStream_t st) {

@@ -249,7 +249,8 @@ struct Layout {
   int64_t P = 0;          // parameters
   int64_t T = 0;          // tokens per micro-batch
   int64_t ldz = 0;        // logits row stride (last stage)
-  size_t theta, G, m, v, theta16, chunks, zeros;
+  size_t theta, G, m, v, theta16, theta16T = 0, chunks, zeros;
+  bool wT = false;             // transposed bf16 block weights kept (theta16T)
   int nchunks = 0;
   size_t stash, slot_bytes;
   int n_slots = 1;             // activation slots: delay + 1, or K + delay with windowed weight gradients
@@ -285,6 +286,10 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
   L.m = a.take(4 * L.P);
   L.v = a.take(4 * L.P);
   L.theta16 = s.dtype == PACI_BF16 ? a.take(2 * L.P) : 0;
+  // bf16 stages: the block weight matrices also transposed ([in, out]), at the
+  // same offsets, for the input-gradient GEMMs
+  L.wT = s.dtype == PACI_BF16 && d % 8 == 0 && f % 8 == 0;
+  L.theta16T = L.wT ? a.take(2 * L.P) : 0;
   L.nchunks = count_chunks(p);
   L.chunks = a.take(16 * (size_t)L.nchunks);
   L.zeros = a.take(256);  // never written after init: source of out-of-range GEMM tile slots
@@ -399,6 +404,8 @@ struct paci_stage {
     return dt == paci::DT_BF16 ? (const void*)(reinterpret_cast<const uint16_t*>(arena + L.theta16) + off)
                                : (const void*)(theta() + off);
   }
+  // transposed bf16 copy of a block weight matrix [out, in] -> [in, out]
+  const void* WT(int64_t off) const { return reinterpret_cast<const uint16_t*>(arena + L.theta16T) + off; }
   const float* th(int64_t off) const { return theta() + off; }
   float* g(int64_t off) const { return G() + off; }
   char* slot(int mb) const { return arena + L.stash + (size_t)(mb % L.n_slots) * L.slot_bytes; }
@@ -473,13 +480,33 @@ int linear_fwd(paci_stage* h, const void* X, int64_t w_off, int64_t b_off, int M
 }
 
 // dX [M, N] = dY [M, K] . W [K, N]   (W = nn.Linear weight [out = K, in = N])
-// colsum_off >= 0: also accumulate the column sums of dX into that gradient
+// colsum_off >= 0: also accumulate the column sums of dX into that gradient.
+// block: W is a block weight, so with transposed copies kept the product reads
+// W^T [N, K] and both operands are contiguous along K.
 int linear_dgrad(paci_stage* h, const void* dY, int64_t ldy, int64_t w_off, int M, int N, int K, paci::GemmEpi epi,
-                 void* C, const void* aux, int64_t colsum_off = -1) {
-  paci::GemmArgs a{dY, ldy, h->W(w_off), N, M, N, K, C, N, nullptr, aux, N, nullptr, h->arena + h->L.zeros};
+                 void* C, const void* aux, int64_t colsum_off = -1, bool block = true) {
+  const bool tr = block && h->L.wT;
+  paci::GemmArgs a{dY, ldy, tr ? h->WT(w_off) : h->W(w_off), tr ? K : N, M, N, K, C, N, nullptr, aux, N, nullptr,
+                   h->arena + h->L.zeros};
   if (colsum_off >= 0) a.colsum = h->g(colsum_off);
   return run(h, F_GEMM_DGRAD, 2.0 * M * N * K,
-             [&] { return paci::gemm(h->dt, false, paci::GEMM_NN, epi, a, 1, h->st); });
+             [&] { return paci::gemm(h->dt, false, tr ? paci::GEMM_NT : paci::GEMM_NN, epi, a, 1, h->st); });
+}
+
+// Rewrites the transposed bf16 block weights from the bf16 working copy.
+int refresh_wT(paci_stage* h) {
+  if (!h->L.wT) return PACI_OK;
+  const int d = h->s.d_model, f = h->s.d_ff;
+  const uint16_t* w16 = reinterpret_cast<const uint16_t*>(h->arena + h->L.theta16);
+  uint16_t* wt = reinterpret_cast<uint16_t*>(h->arena + h->L.theta16T);
+  for (const BlockRefs& b : h->p.blocks) {
+    const int64_t offs[4] = {b.w_qkv, b.w_o, b.w_1, b.w_2};
+    const int rows[4] = {3 * d, d, f, d}, cols[4] = {d, d, d, f};
+    for (int i = 0; i < 4; ++i)
+      TRY(run(h, F_ADAMW, 4.0 * rows[i] * cols[i],
+              [&] { return paci::transpose16(w16 + offs[i], wt + offs[i], rows[i], cols[i], h->st); }));
+  }
+  return PACI_OK;
 }
 
 // G[out, in] += dY[T, out]^T X[T, in]
@@ -603,11 +630,11 @@ size_t act_bytes(const paci_stage* h) { return (size_t)h->L.T * h->s.d_model * h
 // window buffer (contiguous), X from the activation slots of those micro-batches
 // (first micro-batch mb0), one contracted segment of T rows per slot.
 // Split-K count for these long contractions (128 x 128 output tiles): about 1536
-// workgroups, each split at least 8192 contracted rows, at most 16 splits
-// (measured best on MI355X for 64K-row weight gradients at d = 1024).
+// workgroups, each split at least 1024 contracted rows, at most 16 splits
+// (measured on MI355X for 64K-row weight gradients at d = 1024).
 int window_splits(int out, int in, int64_t Kt) {
   const int64_t tiles = (int64_t)((out + 127) / 128) * ((in + 127) / 128);
-  const int by_rows = (int)std::min<int64_t>(16, Kt / 8192);
+  const int by_rows = (int)std::min<int64_t>(16, Kt / 1024);
   return std::max(1, std::min(by_rows, (int)std::lround(1536.0 / (double)tiles)));
 }
 
@@ -766,8 +793,10 @@ extern "C" int paci_stage_load(paci_stage* h, int what, const float* src, int64_
   if (what == PACI_GRADS) TRY(flush_window(h));   // pending products belong to the G being replaced
   hipError_t e = hipMemcpyAsync(dst, src, (size_t)n * 4, on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice,
                                 h->st);
-  if (e == hipSuccess && what == PACI_PARAMS && h->dt == paci::DT_BF16)
+  if (e == hipSuccess && what == PACI_PARAMS && h->dt == paci::DT_BF16) {
     e = paci::f32_to_bf16(h->theta(), h->arena + h->L.theta16, n, h->st);
+    if (e == hipSuccess && refresh_wT(h) != PACI_OK) e = (hipError_t)h->last_hip;
+  }
   if (e == hipSuccess && !on_device) e = hipStreamSynchronize(h->st);
   if (e != hipSuccess) {
     h->last_hip = (int)e;
@@ -876,7 +905,7 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
                           scale, h->st);
     });
     if (!r) r = linear_wgrad(h, dz, L.ldz, sl + L.s_nf, d, s.vocab, d, T, h->p.w_lm);
-    if (!r) r = linear_dgrad(h, dz, L.ldz, h->p.w_lm, T, d, s.vocab, paci::EPI_STORE, dnf, nullptr);
+    if (!r) r = linear_dgrad(h, dz, L.ldz, h->p.w_lm, T, d, s.vocab, paci::EPI_STORE, dnf, nullptr, -1, false);
     if (!r)   // the last block's output gradient; G_b2 of that block += its column sums
       r = ln_bwd(h, dnf, sl + L.s_y, reinterpret_cast<const float*>(sl + L.s_meanf),
                  reinterpret_cast<const float*>(sl + L.s_rstdf), h->p.lnf_g, h->p.lnf_b, nullptr, dy_last,
@@ -933,6 +962,7 @@ extern "C" int paci_stage_step(paci_stage* h, int* new_version) {
                        reinterpret_cast<const int4*>(h->arena + h->L.chunks), h->L.nchunks, a, h->st);
   });
   if (r) return r;
+  TRY(refresh_wT(h));
   fsm_commit_step(h->fsm);
   h->win_done = 0;
   if (new_version) *new_version = h->fsm.t;

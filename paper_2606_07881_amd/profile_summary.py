@@ -29,7 +29,8 @@ COPY_BYTES = 256 * 2 ** 20   # read and written by one copy16 dispatch of stage_
 FAMILIES = {
     "gemm_fwd": ["gemm_pipe_kernel<bool _Accum, bool, E, true, 1", "gemm_pipe_kernel<bool _Accum, bool, E, true, 2",
                  "gemm_pipe_kernel<bool _Accum, bool, E, true, 3"],
-    "gemm_dgrad": ["gemm_pipe_kernel<bool _Accum, bool, E, false, 0", "gemm_pipe_kernel<bool _Accum, bool, E, false, 4"],
+    "gemm_dgrad": ["gemm_pipe_kernel<bool _Accum, bool, E, true, 0", "gemm_pipe_kernel<bool _Accum, bool, E, true, 4",
+                   "gemm_pipe_kernel<bool _Accum, bool, E, false, 0", "gemm_pipe_kernel<bool _Accum, bool, E, false, 4"],
     "gemm_wgrad_acc": ["gemm_pipe_kernel<float, false, false, 5", "gemm_pipe_kernel<float, false, false, 6"],
     "attn_fwd": ["attn_fwd_ring_kernel"],
     "attn_bwd": ["attn_pairs_kernel", "attn_dkdv_ring_kernel", "attn_dq_ring_kernel"],

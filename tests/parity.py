@@ -84,6 +84,10 @@ def small_cfg(name, **kw):
         # T = 128 (a multiple of 64): bf16 weight gradients windowed over K = 3 micro-batches
         "win_bf16": dict(kind="middle", n_layers=2, d_model=128, n_heads=2, head_dim=64, d_ff=384, seq=64,
                          micro_batch=2, K=3, delay=2, M=9, dtype="bf16"),
+        # 8 micro-batches of T = 1024 per window: the window GEMMs split the 8192
+        # contracted rows 8 ways, one split per XCD
+        "win8_bf16": dict(kind="middle", n_layers=1, d_model=128, n_heads=2, head_dim=64, d_ff=256, seq=512,
+                          micro_batch=2, K=8, delay=2, M=16, dtype="bf16"),
         "dh128_bf16": dict(kind="middle", n_layers=1, d_model=256, n_heads=2, head_dim=128, d_ff=512, seq=160,
                            micro_batch=2, K=2, delay=1, M=6, dtype="bf16"),
         "dh32_bf16": dict(kind="middle", n_layers=1, d_model=128, n_heads=4, head_dim=32, d_ff=256, seq=96,

@@ -66,8 +66,8 @@ def test_first_forward_backward(binding, name):
         assert rel_err(G[n], o_G[n]) <= tol(c, "grad"), n
 
 
-@pytest.mark.parametrize("name", ["tiny_fp32", "ragged_bf16", "ragged_fp32", "win_bf16", "dh128_bf16", "dh32_bf16",
-                                  "first_bf16", "last_bf16", "first_fp32", "last_fp32"])
+@pytest.mark.parametrize("name", ["tiny_fp32", "ragged_bf16", "ragged_fp32", "win_bf16", "win8_bf16", "dh128_bf16",
+                                  "dh32_bf16", "first_bf16", "last_bf16", "first_fp32", "last_fp32"])
 def test_replay_parity(binding, name):
     """The whole asynchronous 1F1B replay: stamps bit-exact, every output, input
     gradient, accumulated G and the state after every AdamW update."""
@@ -85,13 +85,13 @@ def test_window_flush_on_read(binding):
     """Windowed weight gradients (bf16, T a multiple of 64): reading G after the
     first backward of every window adds the products so far; the rest follow at
     the update, and every G, theta, m and v still match the oracle."""
-    c = small_cfg("win_bf16")
+    c = small_cfg("win8_bf16")
     inp = Inputs(c, 4, c["M"])
     g = gpu_replay(c, inp, read_mid=True)
     o = oracle_replay(c, inp)
     sens = oracle_sensitivity(c, inp, o)
     rep = compare_replays(c, g, o, sens=sens, theta0=inp.params)
-    print("win_bf16 read_mid", {k: (f"{v:.2e}" if isinstance(v, float) else v) for k, v in rep.items()}, flush=True)
+    print("win8_bf16 read_mid", {k: (f"{v:.2e}" if isinstance(v, float) else v) for k, v in rep.items()}, flush=True)
     assert g["counters"]["version"] == c["M"] // c["K"]
 
 
