@@ -671,6 +671,10 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
   constexpr int NRI = (AK ? 1 : 2) * (WM / 16) + (BK ? 1 : 2) * (WN / 16);   // LDS read instructions per step
   constexpr int NM = (WM / 16) * (WN / 16);                                 // MFMAs per step
   constexpr int NF = WM / 16 + WN / 16;                                      // fragments per step
+  // weight gradients (both operands MN-major, two workgroups per CU): raise the
+  // wave's issue priority over its MFMA steps (measured 1.3% faster there,
+  // slightly slower for the K-major products)
+  constexpr bool PRIO = !AK && !BK;
 #pragma unroll
   for (int t = 0; t < NS; ++t) fill(t);
   wait_vmcnt<L * (NS - 1)>();
@@ -678,9 +682,11 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
   read_step(0, 0, ya, xa);
   for (int kt = 0; kt < nk; ++kt) {
     wait_lds_reads();     // reads of ya/xa, issued one MFMA step ago
+    if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
     read_step(kt, 1, yb, xb);
     mma_all(ya, xa);
     interleave_reads<NRI, NM>();
+    if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
     wait_lds_reads();     // reads of yb/xb
     wait_vmcnt<L * (NS - 2)>();   // tile kt + 1 has landed; kt + 2 .. kt + NS - 1 may be in flight
     barrier_no_fence();
@@ -701,9 +707,11 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
       }
     } else {
       fill(kt + NS);
+      if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
       read_step(kt + 1, 0, ya, xa);
       mma_all(yb, xb);
       interleave_reads<NRI, NM>();
+      if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
     }
   }
   wait_vmcnt<0>();   // the fills past the last tile, before the ring is reused
