@@ -13,6 +13,13 @@ a backward differentiates the activations saved by its own forward, while every
 parameter it reads is the version current when it runs. Activations that depend
 on parameters are therefore saved at forward time, never recomputed.
 
+With ``recompute=True`` the stage follows the activation-checkpointed variant
+(appendix "Activation checkpointing"): a forward keeps only its stage input
+(and the targets or token ids), and the backward first recomputes the stage's
+activations under the version current at that time, then differentiates them
+at that same version. The output gradient is still the one the pipeline
+delivered for the original forward.
+
 Parameter naming and order (nn.Linear weights are [out, in]):
   first stage prefix  wte [V, d], wpe [max_pos, d]
   block l             h{l}.ln1_g, h{l}.ln1_b, h{l}.w_qkv [3d, d], h{l}.b_qkv,
@@ -102,8 +109,8 @@ def stage_bwd(cfg, theta, saved, grad_out, K, ids=None):
 class Stage:
     """Alg. 1 for one stage over float64 state."""
 
-    def __init__(self, cfg, params, K, delay):
-        self.cfg, self.K, self.delay = cfg, K, delay
+    def __init__(self, cfg, params, K, delay, recompute=False):
+        self.cfg, self.K, self.delay, self.recompute = cfg, K, delay, recompute
         self.names = [n for n, _ in param_shapes(cfg)]
         self.theta = {n: np.array(params[n], dtype=np.float64) for n in self.names}
         self.G = {n: np.zeros_like(self.theta[n]) for n in self.names}
@@ -120,7 +127,9 @@ class Stage:
     def forward(self, mb, inp, targets=None):
         """F_mb: returns (output, t^F). Stores the activations until B_mb."""
         version = self.counters.forward(mb)
-        out, self.saved[mb] = stage_fwd(self.cfg, self.theta, inp, targets)
+        out, saved = stage_fwd(self.cfg, self.theta, inp, targets)
+        # checkpointed: keep the input only (the activations are dropped here)
+        self.saved[mb] = (inp, targets) if self.recompute else saved
         if self.cfg["kind"] == "first":
             self.ids[mb] = inp
         return out, version
@@ -128,8 +137,10 @@ class Stage:
     def backward(self, mb, grad_out=None):
         """B_mb at the current parameters: returns (grad_in, t^B, update_due)."""
         version = self.counters.backward(mb)
-        grad_in, g = stage_bwd(self.cfg, self.theta, self.saved.pop(mb), grad_out, self.K,
-                               ids=self.ids.pop(mb, None))
+        saved = self.saved.pop(mb)
+        if self.recompute:   # the activations again, under the current version
+            _, saved = stage_fwd(self.cfg, self.theta, saved[0], saved[1])
+        grad_in, g = stage_bwd(self.cfg, self.theta, saved, grad_out, self.K, ids=self.ids.pop(mb, None))
         for n, v in g.items():
             self.G[n] += v
         return grad_in, version, self.counters.step_due
@@ -151,7 +162,8 @@ def _copy(d):
     return {k: v.copy() for k, v in d.items()}
 
 
-def replay(cfg, params, K, delay, inputs, grad_outs=None, targets=None, events=None, grad_hook=None):
+def replay(cfg, params, K, delay, inputs, grad_outs=None, targets=None, events=None, grad_hook=None,
+           recompute=False):
     """Run ``events`` (default: the canonical asynchronous 1F1B order) on a Stage.
 
     inputs[i] is micro-batch i's stage input, grad_outs[i] its output gradient
@@ -161,12 +173,13 @@ def replay(cfg, params, K, delay, inputs, grad_outs=None, targets=None, events=N
     ``grad_hook(update_index, G)``, if given, may replace G just before each
     update (the recorded G is the one before the hook); tests use it to
     measure how strongly the trajectory after an update depends on small
-    changes of the accumulated gradient.
+    changes of the accumulated gradient. ``recompute`` selects the
+    activation-checkpointed stage (see the module docstring).
     """
     M = len(inputs)
     if events is None:
         events = canonical_events(M, K, delay)
-    st = Stage(cfg, params, K, delay)
+    st = Stage(cfg, params, K, delay, recompute=recompute)
     rec = dict(out=[None] * M, grad_in=[None] * M, tF=[None] * M, tB=[None] * M,
                G=[], theta=[], m=[], v=[], events=list(events))
     for kind, i in events:
