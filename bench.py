@@ -90,6 +90,9 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--recompute", action="store_true",
+                    help="the activation-checkpointed stage: keep only stage inputs, recompute the forward "
+                         "in each backward under the current parameters")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy a 256 MiB device buffer 3 times (a kernel of known traffic, for scaling "
                          "hardware byte counters)")
@@ -104,7 +107,9 @@ def main():
     from paper_2606_07881_amd import binding, configs, inputs
 
     name = args.config or configs.BENCH_CONFIG
-    c = configs.get(name)
+    c = configs.get(name, **({"recompute": 1} if args.recompute else {}))
+    if args.recompute:
+        name = c["name"]
     M, K, delay = c["M"], c["K"], c["delay"]
     T = c["micro_batch"] * c["seq"]
     log(f"bench: {name} M={M} K={K} delay={delay} T={T}")
@@ -225,7 +230,9 @@ def main():
         "config": {"workload": f"{name}: GPT-2-medium-shaped middle pipeline stage, {c['n_layers']} pre-LN blocks, "
                                f"d {c['d_model']}, {c['n_heads']}x{c['head_dim']} heads, FFN {c['d_ff']}, "
                                f"seq {c['seq']}, micro-batch {c['micro_batch']}; one step = async 1F1B replay of "
-                               f"{M} micro-batches, delay {delay}, AdamW every K={K}",
+                               f"{M} micro-batches, delay {delay}, AdamW every K={K}"
+                               + ("; activation-checkpointed (forward recomputed in each backward)"
+                                  if c.get("recompute") else ""),
                    "micro_batches_per_step": M, "tokens_per_step": tokens_per_step, "K": K, "delay": delay,
                    "parallelism": "single stage, 1 GPU"},
         "mfma_util": round(mfma_util, 4),

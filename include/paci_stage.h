@@ -70,6 +70,9 @@ typedef struct paci_shapes {
   int32_t dtype;        /* enum paci_dtype: arithmetic type of the activations */
   float lr, beta1, beta2, eps, weight_decay; /* AdamW hyper-parameters */
   float ln_eps;         /* LayerNorm epsilon */
+  int32_t recompute;    /* 1: activation-checkpointed stage (appendix "Activation checkpointing"):
+                           a forward keeps only the stage input, the backward recomputes the
+                           activations under the current parameters first; 0: stored activations */
 } paci_shapes;
 
 typedef struct paci_counters {
@@ -138,7 +141,9 @@ int paci_param_info_at(const paci_shapes* s, int index, paci_param_info* out); /
  * multiple of 64 and d, d_ff multiples of 8): such a stage also keeps every
  * block's output gradients of the K micro-batches of a window, and computes the
  * window's weight gradients as one contraction per weight (see stage_backward).
- * E_INVAL / E_UNSUPPORTED as for paci_stage_init. */
+ * A checkpointed stage (recompute = 1) has delay + 1 slots holding only the
+ * stage input (ids, targets) plus one work slot for the activations, and no
+ * window. E_INVAL / E_UNSUPPORTED as for paci_stage_init. */
 int paci_stage_arena_bytes(const paci_shapes* s, int K, int delay, size_t* bytes);
 
 /* stage_init(shapes, K, delay). `dev_arena` is caller-owned device memory of
@@ -187,7 +192,10 @@ int paci_stage_forward(paci_stage* h, int mb, const void* dev_in, const int32_t*
  * gradient to the fp32 accumulator G, and writes the input gradient. On a
  * windowed stage the block weight gradients are added later, all K of the
  * window in one contraction per weight, before the update (or an earlier
- * read of G): the same sum up to fp32 rounding order.
+ * read of G): the same sum up to fp32 rounding order. On a checkpointed stage
+ * (recompute = 1) the backward first recomputes the stage forward from the
+ * stored input under the current parameters and differentiates those
+ * activations (appendix "Activation checkpointing").
  * Middle/first stage: `dev_grad_out` is dL/d(out) [T, d] (stage dtype). Last
  * stage: `dev_grad_out` must be NULL; the backward is seeded with
  * (softmax(z) - onehot(target)) / (T * K). `dev_grad_in` receives dL/d(in)

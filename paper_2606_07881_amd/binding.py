@@ -33,7 +33,8 @@ DTYPES = {"fp32": FP32, "bf16": BF16}
 class PaciShapes(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("n_layers", "d_model", "n_heads", "head_dim", "d_ff", "seq",
                                               "micro_batch", "vocab", "max_pos", "kind", "dtype")] + \
-               [(n, ctypes.c_float) for n in ("lr", "beta1", "beta2", "eps", "weight_decay", "ln_eps")]
+               [(n, ctypes.c_float) for n in ("lr", "beta1", "beta2", "eps", "weight_decay", "ln_eps")] + \
+               [("recompute", ctypes.c_int32)]
 
 
 class PaciCounters(ctypes.Structure):
@@ -126,6 +127,7 @@ def shapes(cfg):
     s.dtype = DTYPES[cfg["dtype"]]
     for k in ("lr", "beta1", "beta2", "eps", "weight_decay", "ln_eps"):
         setattr(s, k, float(cfg[k]))
+    s.recompute = int(bool(cfg.get("recompute", False)))
     return s
 
 

@@ -186,6 +186,7 @@ int validate_shapes(const paci_shapes* s, int K, int delay) {
   if (s->d_model != s->n_heads * s->head_dim) return PACI_E_INVAL;
   if (s->kind != PACI_MIDDLE && s->kind != PACI_FIRST && s->kind != PACI_LAST) return PACI_E_UNSUPPORTED;
   if (s->dtype != PACI_FP32 && s->dtype != PACI_BF16) return PACI_E_UNSUPPORTED;
+  if (s->recompute != 0 && s->recompute != 1) return PACI_E_INVAL;
   if (s->kind != PACI_MIDDLE && s->vocab < 1) return PACI_E_INVAL;
   if (s->kind == PACI_FIRST && (s->max_pos < 1 || s->seq > s->max_pos)) return PACI_E_INVAL;
   const int dh = s->head_dim;
@@ -255,6 +256,10 @@ struct Layout {
   size_t stash, slot_bytes;
   int n_slots = 1;             // activation slots: delay + 1, or K + delay with windowed weight gradients
   bool window = false;         // weight gradients windowed (see the header)
+  // checkpointed stages: each slot holds the stage input only (c_* offsets,
+  // c_bytes per slot); one work slot of the full layout takes the activations
+  bool recompute = false;
+  size_t c_x = 0, c_ids = 0, c_tgt = 0, c_bytes = 0, work = 0;
   std::vector<BlockSlot> blk;  // per block, inside a slot
   struct WinBlock { size_t dqkv, dx1, du, dy; };   // per block: [K * T, width] each
   std::vector<WinBlock> win;
@@ -324,9 +329,20 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
     L.s_lse_ce = sl.take(4 * T);
   }
   L.slot_bytes = (sl.off + 255) & ~(size_t)255;
-  L.window = s.dtype == PACI_BF16 && T % 64 == 0 && d % 8 == 0 && f % 8 == 0;
+  L.recompute = s.recompute != 0;
+  L.window = !L.recompute && s.dtype == PACI_BF16 && T % 64 == 0 && d % 8 == 0 && f % 8 == 0;
   L.n_slots = L.window ? K + delay : delay + 1;
-  L.stash = a.take(L.slot_bytes * (size_t)L.n_slots);
+  if (L.recompute) {
+    Bump c;
+    if (s.kind == PACI_FIRST) L.c_ids = c.take(4 * T);
+    else L.c_x = c.take(esz * T * d);
+    if (s.kind == PACI_LAST) L.c_tgt = c.take(4 * T);
+    L.c_bytes = (c.off + 255) & ~(size_t)255;
+    L.stash = a.take(L.c_bytes * (size_t)L.n_slots);
+    L.work = a.take(L.slot_bytes);
+  } else {
+    L.stash = a.take(L.slot_bytes * (size_t)L.n_slots);
+  }
   if (L.window) {
     for (int l = 0; l < s.n_layers; ++l) {
       Layout::WinBlock w;
@@ -408,7 +424,12 @@ struct paci_stage {
   const void* WT(int64_t off) const { return reinterpret_cast<const uint16_t*>(arena + L.theta16T) + off; }
   const float* th(int64_t off) const { return theta() + off; }
   float* g(int64_t off) const { return G() + off; }
-  char* slot(int mb) const { return arena + L.stash + (size_t)(mb % L.n_slots) * L.slot_bytes; }
+  // the slot of mb: the stage input only on a checkpointed stage, else every activation
+  char* slot(int mb) const {
+    return arena + L.stash + (size_t)(mb % L.n_slots) * (L.recompute ? L.c_bytes : L.slot_bytes);
+  }
+  // where a micro-batch's activations are computed: the work slot, or its own slot
+  char* acts(int mb) const { return L.recompute ? arena + L.work : slot(mb); }
   // window buffer of block l, tensor at offset off, micro-batch j of the window, width columns
   char* win(size_t off, int j, int width) const { return arena + off + (size_t)j * L.T * width * esz; }
   char* ws(size_t off) const { return arena + off; }
@@ -550,8 +571,9 @@ double attn_pairs(const paci_shapes& s) {
 }
 
 // ---- forward of the block stack -----------------------------------------------------------------
-// in: block-0 input (stage input or embedding output); copy_in: also store it in the slot.
-int blocks_fwd(paci_stage* h, char* sl, const void* in, bool copy_in, void* out) {
+// in: block-0 input (stage input or embedding output); x0_copy: where to store a
+// copy of it (nullptr: `in` stays valid), which block 0's residual then reads.
+int blocks_fwd(paci_stage* h, char* sl, const void* in, void* x0_copy, void* out) {
   const paci_shapes& s = h->s;
   const int T = (int)h->L.T, d = s.d_model, f = s.d_ff;
   for (int l = 0; l < s.n_layers; ++l) {
@@ -560,13 +582,14 @@ int blocks_fwd(paci_stage* h, char* sl, const void* in, bool copy_in, void* out)
     const void* x = (l == 0) ? in : (const void*)(sl + o.x);
     float* mean1 = reinterpret_cast<float*>(sl + o.mean1);
     float* rstd1 = reinterpret_cast<float*>(sl + o.rstd1);
-    TRY(ln_fwd(h, x, sl + o.n1, mean1, rstd1, b.ln1_g, b.ln1_b, (l == 0 && copy_in) ? sl + o.x : nullptr));
+    TRY(ln_fwd(h, x, sl + o.n1, mean1, rstd1, b.ln1_g, b.ln1_b, l == 0 ? x0_copy : nullptr));
     TRY(linear_fwd(h, sl + o.n1, b.w_qkv, b.b_qkv, T, 3 * d, d, paci::EPI_BIAS, sl + o.qkv, nullptr, nullptr));
     TRY(run(h, F_ATTN_FWD, 4.0 * attn_pairs(s) * s.head_dim, [&] {
       return paci::attn_fwd(h->dt, sl + o.qkv, sl + o.o, reinterpret_cast<float*>(sl + o.lse2), s.micro_batch, s.seq,
                             s.n_heads, s.head_dim, h->st);
     }));
-    TRY(linear_fwd(h, sl + o.o, b.w_o, b.b_o, T, d, d, paci::EPI_BIAS_RES, sl + o.x1, sl + o.x, nullptr));
+    const void* res = l > 0 ? (const void*)(sl + o.x) : (x0_copy ? (const void*)x0_copy : in);
+    TRY(linear_fwd(h, sl + o.o, b.w_o, b.b_o, T, d, d, paci::EPI_BIAS_RES, sl + o.x1, res, nullptr));
     TRY(ln_fwd(h, sl + o.x1, sl + o.n2, reinterpret_cast<float*>(sl + o.mean2), reinterpret_cast<float*>(sl + o.rstd2),
                b.ln2_g, b.ln2_b, nullptr));
     TRY(linear_fwd(h, sl + o.n2, b.w_1, b.b_1, T, f, d, paci::EPI_BIAS_GELU, sl + o.u, nullptr, sl + o.a));
@@ -674,6 +697,39 @@ int flush_window(paci_stage* h) {
   }
   h->win_done = c;
   return PACI_OK;
+}
+
+// The stage forward of one micro-batch into the activation area A (its slot, or
+// the work slot of a checkpointed stage). in: the stage input (middle, last);
+// x0_copy: where block 0 keeps it; ids / tgt: the micro-batch's token ids (first
+// stage) and targets (last stage) as stored; out: the stage output (last stage:
+// the loss).
+int stage_forward_into(paci_stage* h, char* A, const void* in, void* x0_copy, const int32_t* ids,
+                       const int32_t* tgt, void* out) {
+  const paci_shapes& s = h->s;
+  const Layout& L = h->L;
+  const int T = (int)L.T, d = s.d_model;
+  if (s.kind == PACI_FIRST) {
+    TRY(run(h, F_EMBED, (double)T * d * (8 + h->esz), [&] {
+      return paci::embed_fwd(h->dt, ids, h->th(h->p.wte), h->th(h->p.wpe), A + L.blk[0].x, s.micro_batch, s.seq, d,
+                             s.vocab, h->st);
+    }));
+    return blocks_fwd(h, A, A + L.blk[0].x, nullptr, out);
+  }
+  if (s.kind == PACI_MIDDLE) return blocks_fwd(h, A, in, x0_copy, out);
+  TRY(blocks_fwd(h, A, in, x0_copy, A + L.s_y));
+  float* meanf = reinterpret_cast<float*>(A + L.s_meanf);
+  float* rstdf = reinterpret_cast<float*>(A + L.s_rstdf);
+  float* z = reinterpret_cast<float*>(A + L.s_z);
+  TRY(ln_fwd(h, A + L.s_y, A + L.s_nf, meanf, rstdf, h->p.lnf_g, h->p.lnf_b, nullptr));
+  paci::GemmArgs a{A + L.s_nf, d, h->W(h->p.w_lm), d, T, s.vocab, d, z, L.ldz, nullptr, nullptr, 0, nullptr,
+                   h->arena + L.zeros};
+  TRY(run(h, F_GEMM_FWD, 2.0 * T * s.vocab * d,
+          [&] { return paci::gemm(h->dt, true, paci::GEMM_NT, paci::EPI_STORE, a, 1, h->st); }));
+  return run(h, F_CE, 4.0 * T * s.vocab, [&] {
+    return paci::ce_fwd(z, L.ldz, tgt, reinterpret_cast<float*>(A + L.s_lse_ce), reinterpret_cast<float*>(out),
+                        reinterpret_cast<float*>(h->ws(L.w_part)), T, s.vocab, h->st);
+  });
 }
 
 }  // namespace
@@ -830,43 +886,26 @@ extern "C" int paci_stage_forward(paci_stage* h, int mb, const void* dev_in, con
   if (chk) return chk;
   const paci_shapes& s = h->s;
   const Layout& L = h->L;
-  const int T = (int)L.T, d = s.d_model;
+  const int T = (int)L.T;
   char* sl = h->slot(mb);
+  char* A = h->acts(mb);
+  // what a checkpointed stage keeps: the input (and ids / targets) in the slot
+  void* x0 = L.recompute ? (void*)(sl + L.c_x) : (void*)(A + L.blk[0].x);
   int r = PACI_OK;
   if (s.kind == PACI_FIRST) {
-    int32_t* ids = reinterpret_cast<int32_t*>(sl + L.s_ids);
+    int32_t* ids = reinterpret_cast<int32_t*>(sl + (L.recompute ? L.c_ids : L.s_ids));
     r = run(h, F_COPY, 8.0 * T, [&] {
       return hipMemcpyAsync(ids, dev_in, 4 * (size_t)T, hipMemcpyDeviceToDevice, h->st);
     });
-    if (!r)
-      r = run(h, F_EMBED, (double)T * d * (8 + h->esz), [&] {
-        return paci::embed_fwd(h->dt, ids, h->th(h->p.wte), h->th(h->p.wpe), sl + L.blk[0].x, s.micro_batch, s.seq,
-                               d, s.vocab, h->st);
-      });
-    if (!r) r = blocks_fwd(h, sl, sl + L.blk[0].x, false, dev_out);
+    if (!r) r = stage_forward_into(h, A, nullptr, nullptr, ids, nullptr, dev_out);
   } else if (s.kind == PACI_MIDDLE) {
-    r = blocks_fwd(h, sl, dev_in, true, dev_out);
+    r = stage_forward_into(h, A, dev_in, x0, nullptr, nullptr, dev_out);
   } else {
-    int32_t* tgt = reinterpret_cast<int32_t*>(sl + L.s_tgt);
+    int32_t* tgt = reinterpret_cast<int32_t*>(sl + (L.recompute ? L.c_tgt : L.s_tgt));
     r = run(h, F_COPY, 8.0 * T, [&] {
       return hipMemcpyAsync(tgt, dev_targets, 4 * (size_t)T, hipMemcpyDeviceToDevice, h->st);
     });
-    if (!r) r = blocks_fwd(h, sl, dev_in, true, sl + L.s_y);
-    float* meanf = reinterpret_cast<float*>(sl + L.s_meanf);
-    float* rstdf = reinterpret_cast<float*>(sl + L.s_rstdf);
-    float* z = reinterpret_cast<float*>(sl + L.s_z);
-    if (!r) r = ln_fwd(h, sl + L.s_y, sl + L.s_nf, meanf, rstdf, h->p.lnf_g, h->p.lnf_b, nullptr);
-    if (!r) {
-      paci::GemmArgs a{sl + L.s_nf, d, h->W(h->p.w_lm), d, T, s.vocab, d, z, L.ldz, nullptr, nullptr, 0, nullptr,
-                       h->arena + h->L.zeros};
-      r = run(h, F_GEMM_FWD, 2.0 * T * s.vocab * d,
-              [&] { return paci::gemm(h->dt, true, paci::GEMM_NT, paci::EPI_STORE, a, 1, h->st); });
-    }
-    if (!r)
-      r = run(h, F_CE, 4.0 * T * s.vocab, [&] {
-        return paci::ce_fwd(z, L.ldz, tgt, reinterpret_cast<float*>(sl + L.s_lse_ce), reinterpret_cast<float*>(dev_out),
-                            reinterpret_cast<float*>(h->ws(L.w_part)), T, s.vocab, h->st);
-      });
+    if (!r) r = stage_forward_into(h, A, dev_in, x0, nullptr, tgt, dev_out);
   }
   if (r) return r;
   const int t = fsm_commit_forward(h->fsm);
@@ -886,6 +925,9 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
   const Layout& L = h->L;
   const int T = (int)L.T, d = s.d_model;
   char* sl = h->slot(mb);
+  char* A = h->acts(mb);   // the activations the backward differentiates
+  const int32_t* ids = reinterpret_cast<const int32_t*>(sl + (L.recompute ? L.c_ids : L.s_ids));
+  const int32_t* tgt = reinterpret_cast<const int32_t*>(sl + (L.recompute ? L.c_tgt : L.s_tgt));
   char* bufA = h->ws(L.w_dyA);
   char* bufB = h->ws(L.w_dyB);
   const void* dy = dev_grad_out;
@@ -894,24 +936,30 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
   // windowed: every block's output gradient lives in the window buffer
   char* dy_last = win ? h->win(L.win[s.n_layers - 1].dy, j, d) : bufA;
   int r = PACI_OK;
-  if (s.kind == PACI_LAST) {
-    const float* z = reinterpret_cast<const float*>(sl + L.s_z);
-    const int32_t* tgt = reinterpret_cast<const int32_t*>(sl + L.s_tgt);
+  if (L.recompute) {
+    // checkpointed: the activations again, from the stored input, under the
+    // parameters current now (the output, or loss, is discarded)
+    void* out = s.kind == PACI_LAST ? (void*)h->ws(L.w_loss) : (void*)bufB;
+    r = s.kind == PACI_FIRST ? stage_forward_into(h, A, nullptr, nullptr, ids, nullptr, out)
+                             : stage_forward_into(h, A, sl + L.c_x, A + L.blk[0].x, nullptr, tgt, out);
+  }
+  if (!r && s.kind == PACI_LAST) {
+    const float* z = reinterpret_cast<const float*>(A + L.s_z);
     char* dz = h->ws(L.w_dz);
     char* dnf = h->ws(L.w_dnf);
     const float scale = 1.0f / ((float)T * (float)h->fsm.K);
     r = run(h, F_CE, (double)T * L.ldz * (4 + h->esz), [&] {
-      return paci::ce_bwd(h->dt, z, L.ldz, tgt, reinterpret_cast<const float*>(sl + L.s_lse_ce), dz, T, s.vocab,
+      return paci::ce_bwd(h->dt, z, L.ldz, tgt, reinterpret_cast<const float*>(A + L.s_lse_ce), dz, T, s.vocab,
                           scale, h->st);
     });
-    if (!r) r = linear_wgrad(h, dz, L.ldz, sl + L.s_nf, d, s.vocab, d, T, h->p.w_lm);
+    if (!r) r = linear_wgrad(h, dz, L.ldz, A + L.s_nf, d, s.vocab, d, T, h->p.w_lm);
     if (!r) r = linear_dgrad(h, dz, L.ldz, h->p.w_lm, T, d, s.vocab, paci::EPI_STORE, dnf, nullptr, -1, false);
     if (!r)   // the last block's output gradient; G_b2 of that block += its column sums
-      r = ln_bwd(h, dnf, sl + L.s_y, reinterpret_cast<const float*>(sl + L.s_meanf),
-                 reinterpret_cast<const float*>(sl + L.s_rstdf), h->p.lnf_g, h->p.lnf_b, nullptr, dy_last,
+      r = ln_bwd(h, dnf, A + L.s_y, reinterpret_cast<const float*>(A + L.s_meanf),
+                 reinterpret_cast<const float*>(A + L.s_rstdf), h->p.lnf_g, h->p.lnf_b, nullptr, dy_last,
                  h->p.blocks[s.n_layers - 1].b_2);
     dy = dy_last;
-  } else if (win) {
+  } else if (!r && win) {
     r = run(h, F_COPY, 2.0 * act_bytes(h), [&] {
       return hipMemcpyAsync(dy_last, dev_grad_out, act_bytes(h), hipMemcpyDeviceToDevice, h->st);
     });
@@ -926,12 +974,12 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
     else
       dx = (dy == bufA) ? bufB : bufA;
     // every block's dy but the given stage output gradient came out of a LayerNorm backward
-    r = block_bwd(h, sl, l, dy, dx, l < s.n_layers - 1 || s.kind == PACI_LAST, j);
+    r = block_bwd(h, A, l, dy, dx, l < s.n_layers - 1 || s.kind == PACI_LAST, j);
     dy = dx;
   }
   if (!r && s.kind == PACI_FIRST) {
     r = run(h, F_EMBED, (double)T * d * (h->esz + 8), [&] {
-      return paci::embed_bwd(h->dt, reinterpret_cast<const int32_t*>(sl + L.s_ids), dy, h->g(h->p.wte),
+      return paci::embed_bwd(h->dt, ids, dy, h->g(h->p.wte),
                              h->g(h->p.wpe), s.micro_batch, s.seq, d, s.vocab, h->st);
     });
   }

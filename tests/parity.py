@@ -74,7 +74,13 @@ def rel_err(x, r):
 
 def small_cfg(name, **kw):
     """Parity workloads small enough for the oracle (seconds), spanning several
-    tiles with ragged tails."""
+    tiles with ragged tails. ``ckpt_<name>``: workload <name> on an
+    activation-checkpointed stage."""
+    if name.startswith("ckpt_"):
+        base = name[len("ckpt_"):]
+        c = configs.get(base) if base == "tiny_fp32" else small_cfg(base)
+        c.update(recompute=1, **kw)
+        return c
     base = {
         # ragged in tokens (T = 400), model width (192 = 1.5 GEMM tiles) and keys (S = 200)
         "ragged_bf16": dict(kind="middle", n_layers=2, d_model=192, n_heads=3, head_dim=64, d_ff=768, seq=200,
@@ -225,7 +231,8 @@ def oracle_replay(c, inp, events=None, K=None, delay=None, grad_hook=None):
     delay = c["delay"] if delay is None else delay
     return ostage.replay(c, inp.oracle_params(), K, delay, inp.x,
                          grad_outs=None if c["kind"] == "last" else inp.dy,
-                         targets=inp.tgt if c["kind"] == "last" else None, events=events, grad_hook=grad_hook)
+                         targets=inp.tgt if c["kind"] == "last" else None, events=events, grad_hook=grad_hook,
+                         recompute=bool(c.get("recompute", 0)))
 
 
 def oracle_sensitivity(c, inp, ref, seed=12345):

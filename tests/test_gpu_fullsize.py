@@ -17,7 +17,8 @@ sequence depends on that prefix only):
 * B_K: the input gradient of sequence 0 with activations saved at version
   t^F(K) and the parameters of version 1 (the GPU's theta_1): for delay > 0
   this is the stale backward of the method (activations of version 0,
-  weights of version 1);
+  weights of version 1); on a checkpointed stage the activations are
+  recomputed at version 1 as well;
 * F_(K+delay): outputs of sequence 0 (prefix) at version 1;
 * every version stamp, exactly; every output finite.
 """
@@ -31,7 +32,8 @@ from paper_2606_07881_amd import configs, inputs
 
 pytestmark = pytest.mark.gpu
 
-FULL = ["gpt2s_mid_bf16", "gpt2m_mid_bf16", "gpt2m_first_bf16", "gpt2m_last_bf16", "gpt1p3b_pos0_bf16"]
+FULL = ["gpt2s_mid_bf16", "gpt2m_mid_bf16", "gpt2m_first_bf16", "gpt2m_last_bf16", "gpt1p3b_pos0_bf16",
+        "gpt2m_mid_bf16+ckpt"]   # +ckpt: the same workload on an activation-checkpointed stage
 PREFIX = 256   # tokens of a sequence whose forward is checked where the whole one is not needed
 
 
@@ -79,7 +81,7 @@ def oracle_grad_in(c, theta_f, theta_b, x_seq, dy_seq, tgt_seq):
 @pytest.mark.parametrize("name", FULL)
 def test_fullsize_sampled(binding, name):
     import torch
-    c = configs.get(name)
+    c = configs.get(name.split("+")[0], **({"recompute": 1} if name.endswith("+ckpt") else {}))
     K, delay, seed = c["K"], c["delay"], 0
     T, d, mu = c["micro_batch"] * c["seq"], c["d_model"], c["micro_batch"]
     kind = c["kind"]
@@ -197,7 +199,8 @@ def test_fullsize_sampled(binding, name):
             continue    # no input gradient
         gin = to_host(gins[i])
         assert np.all(np.isfinite(gin))
-        ref = oracle_grad_in(c, versions[tF[i]], versions[tB[i]], seq_input(c, x_host[i], 0),
+        t_act = tB[i] if c.get("recompute") else tF[i]   # the version the activations are from
+        ref = oracle_grad_in(c, versions[t_act], versions[tB[i]], seq_input(c, x_host[i], 0),
                              None if kind == "last" else seq_rows(c, dy_host[i], 0).astype(np.float64),
                              tg_host[i][0:1] if kind == "last" else None)
         e = rel_err(seq_rows(c, gin, 0), ref)
