@@ -30,6 +30,29 @@ def adamw_update(theta, grad, m, v, step, lr, beta1, beta2, eps, weight_decay):
     return theta - lr * mhat / (np.sqrt(vhat) + eps), m, v
 
 
+def lr_at(cfg, step):
+    """Learning rate of update ``step`` (1 for the first update).
+
+    The paper's recipe (appendix "Detailed experimental setup") warms the rate
+    up linearly over the first 1% of the updates and then decays it along a
+    cosine to 10% of the peak. Read here as: with W = lr_warmup and
+    N = lr_total updates (N = 0: the constant rate cfg["lr"]),
+      step <= W:  lr * step / W
+      step >  W:  lr * (r + (1 - r) * (1 + cos(pi * p)) / 2),
+                  p = min(1, (step - W) / (N - W)), r = lr_min_ratio.
+    """
+    peak = cfg["lr"]
+    total = int(cfg.get("lr_total", 0))
+    if total <= 0:
+        return peak
+    warm = int(cfg.get("lr_warmup", 0))
+    r = float(cfg.get("lr_min_ratio", 0.1))
+    if step <= warm:
+        return peak * step / warm
+    p = min(1.0, (step - warm) / max(1, total - warm))
+    return peak * (r + (1.0 - r) * 0.5 * (1.0 + math.cos(math.pi * p)))
+
+
 def direction_bound(step, beta1, beta2):
     """Largest |m_hat / sqrt(v_hat)| any gradient sequence can produce at ``step``.
 

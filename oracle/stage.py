@@ -149,11 +149,12 @@ class Stage:
         """AdamW with the accumulated G, then G <- 0; returns the new version."""
         c = self.cfg
         t_adam = self.counters.t + 1
+        lr = adamw.lr_at(c, t_adam)
         for n in self.names:
             wd = c["weight_decay"] if decayed(n) else 0.0
             self.theta[n], self.m[n], self.v[n] = adamw.adamw_update(
                 self.theta[n], self.G[n], self.m[n], self.v[n], t_adam,
-                c["lr"], c["beta1"], c["beta2"], c["eps"], wd)
+                lr, c["beta1"], c["beta2"], c["eps"], wd)
             self.G[n] = np.zeros_like(self.G[n])
         return self.counters.step()
 
@@ -243,7 +244,7 @@ def replay_with_version_store(cfg, params, K, delay, inputs, grad_outs=None, tar
                 wd = cfg["weight_decay"] if decayed(n) else 0.0
                 new[n], m[n], v[n] = adamw.adamw_update(
                     versions[t][n], G[n], m[n], v[n], t + 1,
-                    cfg["lr"], cfg["beta1"], cfg["beta2"], cfg["eps"], wd)
+                    adamw.lr_at(cfg, t + 1), cfg["beta1"], cfg["beta2"], cfg["eps"], wd)
                 G[n] = np.zeros_like(G[n])
             versions.append(new)
             thetas.append(new)

@@ -260,7 +260,7 @@ def oracle_sensitivity(c, inp, ref, seed=12345):
 def adamw_np(theta, G, m, v, step, c, decay):
     """The AdamW update (decoupled decay first, bias-corrected moments, eps outside
     the root) in float64, used to check a GPU update against the GPU's own state."""
-    lr, b1, b2, eps, wd = c["lr"], c["beta1"], c["beta2"], c["eps"], c["weight_decay"]
+    lr, b1, b2, eps, wd = oadamw.lr_at(c, step), c["beta1"], c["beta2"], c["eps"], c["weight_decay"]
     th = theta * (1.0 - lr * wd) if decay else theta.copy()
     m = b1 * m + (1 - b1) * G
     v = b2 * v + (1 - b2) * G * G
@@ -303,13 +303,13 @@ def compare_replays(c, g, o, sens=None, theta0=None):
             L = lim(t_grad, sens["grad_in"][i] if sens else 0.0, after_b)
             assert e <= L, f"input gradient of micro-batch {i}: {e:.3e} (limit {L:.3e})"
     names = [n for n, _, _ in inputs.param_specs(c)]
-    lr, b1, b2 = c["lr"], c["beta1"], c["beta2"]
+    b1, b2 = c["beta1"], c["beta2"]
     masked = {n: None for n in names}
     gerr = {n: None for n in names}
     n_masked = n_total = 0
     budget = 0.0
     for s in range(len(o["G"])):
-        budget += 2.0 * lr * oadamw.direction_bound(s + 1, b1, b2)
+        budget += 2.0 * oadamw.lr_at(c, s + 1) * oadamw.direction_bound(s + 1, b1, b2)
         for n in names:
             sv = (lambda key: sens[key][s][n]) if sens else (lambda key: 0.0)
             gg, og = g["G"][s][n], o["G"][s][n]

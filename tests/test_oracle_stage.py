@@ -196,3 +196,43 @@ def test_adamw_direction_bound():
                 m, v = 0.9 * m + 0.1 * g, 0.95 * v + 0.05 * g * g
             u = (m / (1 - 0.9 ** t)) / np.sqrt(v / (1 - 0.95 ** t))
             assert abs(u) <= bound * (1 + 1e-12)
+
+
+def test_lr_schedule_closed_forms():
+    """Linear warmup to the peak, cosine decay to lr_min_ratio * peak, then flat;
+    no schedule (lr_total = 0) keeps the constant rate."""
+    c = dict(lr=1e-3, lr_warmup=2, lr_total=10, lr_min_ratio=0.1)
+    assert adamw.lr_at(c, 1) == pytest.approx(0.5e-3, rel=1e-15)
+    assert adamw.lr_at(c, 2) == pytest.approx(1e-3, rel=1e-15)
+    assert adamw.lr_at(c, 6) == pytest.approx(1e-3 * (0.1 + 0.9 * 0.5), rel=1e-14)   # halfway down the cosine
+    assert adamw.lr_at(c, 10) == pytest.approx(1e-4, rel=1e-14)
+    assert adamw.lr_at(c, 25) == pytest.approx(1e-4, rel=1e-14)
+    assert adamw.lr_at(dict(lr=3e-4), 7) == 3e-4
+
+
+def test_lr_schedule_matches_torch_schedulers():
+    """Each phase against PyTorch's own scheduler: update t <= W runs at LinearLR's
+    rate after t - 1 steps (from peak / W to the peak over W - 1 steps); update
+    t > W at CosineAnnealingLR's rate after t - W steps (T_max = N - W, down to
+    lr_min_ratio * peak)."""
+    W, N, r, peak = 3, 17, 0.1, 2e-3
+    c = dict(lr=peak, lr_warmup=W, lr_total=N, lr_min_ratio=r)
+
+    def rates(make, n):
+        p = torch.nn.Parameter(torch.zeros(1))
+        opt = torch.optim.SGD([p], lr=peak)
+        sched = make(opt)
+        out = []
+        for _ in range(n):
+            out.append(opt.param_groups[0]["lr"])
+            opt.step()
+            sched.step()
+        return out
+
+    warm = rates(lambda o: torch.optim.lr_scheduler.LinearLR(o, start_factor=1.0 / W, end_factor=1.0,
+                                                             total_iters=W - 1), W)
+    cos = rates(lambda o: torch.optim.lr_scheduler.CosineAnnealingLR(o, T_max=N - W, eta_min=r * peak), N - W + 1)
+    for t in range(1, W + 1):
+        assert adamw.lr_at(c, t) == pytest.approx(warm[t - 1], rel=1e-12), t
+    for t in range(W + 1, N + 1):
+        assert adamw.lr_at(c, t) == pytest.approx(cos[t - W], rel=1e-9), t
