@@ -73,6 +73,11 @@ typedef struct paci_shapes {
   int32_t recompute;    /* 1: activation-checkpointed stage (appendix "Activation checkpointing"):
                            a forward keeps only the stage input, the backward recomputes the
                            activations under the current parameters first; 0: stored activations */
+  int32_t lr_warmup;    /* learning-rate schedule (appendix "Detailed experimental setup"): update t
+                           (1-based) uses lr * t / lr_warmup while t <= lr_warmup, then a cosine
+                           from lr down to lr * lr_min_ratio at update lr_total, flat after it */
+  int32_t lr_total;     /* 0: no schedule, every update uses lr */
+  float lr_min_ratio;
 } paci_shapes;
 
 typedef struct paci_counters {

@@ -34,7 +34,8 @@ class PaciShapes(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("n_layers", "d_model", "n_heads", "head_dim", "d_ff", "seq",
                                               "micro_batch", "vocab", "max_pos", "kind", "dtype")] + \
                [(n, ctypes.c_float) for n in ("lr", "beta1", "beta2", "eps", "weight_decay", "ln_eps")] + \
-               [("recompute", ctypes.c_int32)]
+               [("recompute", ctypes.c_int32), ("lr_warmup", ctypes.c_int32), ("lr_total", ctypes.c_int32),
+                ("lr_min_ratio", ctypes.c_float)]
 
 
 class PaciCounters(ctypes.Structure):
@@ -128,6 +129,9 @@ def shapes(cfg):
     for k in ("lr", "beta1", "beta2", "eps", "weight_decay", "ln_eps"):
         setattr(s, k, float(cfg[k]))
     s.recompute = int(bool(cfg.get("recompute", False)))
+    s.lr_warmup = int(cfg.get("lr_warmup", 0))
+    s.lr_total = int(cfg.get("lr_total", 0))
+    s.lr_min_ratio = float(cfg.get("lr_min_ratio", 0.1))
     return s
 
 

@@ -187,6 +187,9 @@ int validate_shapes(const paci_shapes* s, int K, int delay) {
   if (s->kind != PACI_MIDDLE && s->kind != PACI_FIRST && s->kind != PACI_LAST) return PACI_E_UNSUPPORTED;
   if (s->dtype != PACI_FP32 && s->dtype != PACI_BF16) return PACI_E_UNSUPPORTED;
   if (s->recompute != 0 && s->recompute != 1) return PACI_E_INVAL;
+  if (s->lr_warmup < 0 || s->lr_total < 0 || (s->lr_total > 0 && s->lr_warmup > s->lr_total) ||
+      !(s->lr_min_ratio >= 0.f && s->lr_min_ratio <= 1.f))
+    return PACI_E_INVAL;
   if (s->kind != PACI_MIDDLE && s->vocab < 1) return PACI_E_INVAL;
   if (s->kind == PACI_FIRST && (s->max_pos < 1 || s->seq > s->max_pos)) return PACI_E_INVAL;
   const int dh = s->head_dim;
@@ -699,6 +702,17 @@ int flush_window(paci_stage* h) {
   return PACI_OK;
 }
 
+// Learning rate of update t (1-based): linear warmup to the peak, then a cosine
+// down to lr_min_ratio of it at update lr_total (appendix "Detailed
+// experimental setup"); lr_total = 0: the constant rate.
+double lr_at(const paci_shapes& s, int t) {
+  if (s.lr_total <= 0) return s.lr;
+  if (t <= s.lr_warmup) return (double)s.lr * t / s.lr_warmup;
+  const double p = std::min(1.0, (double)(t - s.lr_warmup) / std::max(1, s.lr_total - s.lr_warmup));
+  const double r = s.lr_min_ratio;
+  return s.lr * (r + (1.0 - r) * 0.5 * (1.0 + std::cos(3.14159265358979323846 * p)));
+}
+
 // The stage forward of one micro-batch into the activation area A (its slot, or
 // the work slot of a checkpointed stage). in: the stage input (middle, last);
 // x0_copy: where block 0 keeps it; ids / tgt: the micro-batch's token ids (first
@@ -996,7 +1010,7 @@ extern "C" int paci_stage_step(paci_stage* h, int* new_version) {
   const paci_shapes& s = h->s;
   const int t_adam = h->fsm.t + 1;
   paci::AdamwArgs a;
-  a.lr = s.lr;
+  a.lr = (float)lr_at(s, t_adam);
   a.beta1 = s.beta1;
   a.beta2 = s.beta2;
   a.eps = s.eps;

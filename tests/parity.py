@@ -87,6 +87,10 @@ def small_cfg(name, **kw):
                             micro_batch=2, K=4, delay=3, M=12, dtype="bf16"),
         "ragged_fp32": dict(kind="middle", n_layers=2, d_model=96, n_heads=3, head_dim=32, d_ff=320, seq=100,
                             micro_batch=2, K=3, delay=2, M=9, dtype="fp32"),
+        # the learning-rate schedule: warmup over the first update, cosine to 10% by the third
+        "sched_bf16": dict(kind="middle", n_layers=1, d_model=128, n_heads=2, head_dim=64, d_ff=256, seq=64,
+                           micro_batch=2, K=2, delay=1, M=8, dtype="bf16", lr=3e-3, lr_warmup=1, lr_total=3,
+                           lr_min_ratio=0.1),
         # T = 128 (a multiple of 64): bf16 weight gradients windowed over K = 3 micro-batches
         "win_bf16": dict(kind="middle", n_layers=2, d_model=128, n_heads=2, head_dim=64, d_ff=384, seq=64,
                          micro_batch=2, K=3, delay=2, M=9, dtype="bf16"),

@@ -69,7 +69,7 @@ def test_first_forward_backward(binding, name):
 @pytest.mark.parametrize("name", ["tiny_fp32", "ragged_bf16", "ragged_fp32", "win_bf16", "win8_bf16", "dh128_bf16",
                                   "dh32_bf16", "first_bf16", "last_bf16", "first_fp32", "last_fp32",
                                   "ckpt_tiny_fp32", "ckpt_ragged_bf16", "ckpt_win_bf16", "ckpt_first_bf16",
-                                  "ckpt_last_bf16"])
+                                  "ckpt_last_bf16", "sched_bf16"])
 def test_replay_parity(binding, name):
     """The whole asynchronous 1F1B replay: stamps bit-exact, every output, input
     gradient, accumulated G and the state after every AdamW update."""
