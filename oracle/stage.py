@@ -119,6 +119,7 @@ class Stage:
         self.counters = StageCounters(K, delay)
         self.saved = {}
         self.ids = {}
+        self.applied = self.skipped = 0   # updates applied / skipped by the non-finite guard
 
     @property
     def version(self):
@@ -146,9 +147,21 @@ class Stage:
         return grad_in, version, self.counters.step_due
 
     def step(self):
-        """AdamW with the accumulated G, then G <- 0; returns the new version."""
+        """AdamW with the accumulated G, then G <- 0; returns the new version.
+
+        Non-finite guard (the paper implements no handling of invalid gradients,
+        Sec. "Limitations"): if any element of G is not finite, no parameter
+        or moment changes; G is still cleared and the version still advances,
+        so the stamps remain a function of the event order alone. AdamW's
+        bias correction and the rate schedule count applied updates only."""
         c = self.cfg
-        t_adam = self.counters.t + 1
+        if not all(np.all(np.isfinite(g)) for g in self.G.values()):
+            self.skipped += 1
+            for n in self.names:
+                self.G[n] = np.zeros_like(self.G[n])
+            return self.counters.step()
+        self.applied += 1
+        t_adam = self.applied
         lr = adamw.lr_at(c, t_adam)
         for n in self.names:
             wd = c["weight_decay"] if decayed(n) else 0.0

@@ -236,3 +236,30 @@ def test_lr_schedule_matches_torch_schedulers():
         assert adamw.lr_at(c, t) == pytest.approx(warm[t - 1], rel=1e-12), t
     for t in range(W + 1, N + 1):
         assert adamw.lr_at(c, t) == pytest.approx(cos[t - W], rel=1e-9), t
+
+
+def test_nonfinite_gradient_skips_the_update():
+    """A window whose G holds a NaN changes no parameter or moment, clears G and
+    still advances the version; the next update is AdamW's first (bias
+    correction step 1, the closed form of test_adamw_first_step_closed_form)."""
+    cfg = _cfg(kind="middle", weight_decay=0.1)
+    params, xs, dys, tg = _data(cfg, 6, seed=9)
+
+    def hook(s, G):
+        if s == 0:
+            G = {n: g.copy() for n, g in G.items()}
+            G["h0.w_qkv"].flat[3] = np.nan
+        return G
+
+    rec = stage.replay(cfg, params, 2, 1, xs, grad_outs=dys, grad_hook=hook)
+    st = rec["stage"]
+    assert st.skipped == 1 and st.applied == 2 and rec["final_version"] == 3
+    for n in params:
+        assert np.array_equal(rec["theta"][0][n], np.asarray(params[n], np.float64)), n
+        assert not np.any(rec["m"][0][n]) and not np.any(rec["v"][0][n]), n
+    lr, wd = cfg["lr"], cfg["weight_decay"]
+    for n in params:
+        g = rec["G"][1][n]
+        th0 = np.asarray(params[n], np.float64)
+        first = (th0 * (1 - lr * wd) if stage.decayed(n) else th0) - lr * g / (np.abs(g) + cfg["eps"])
+        np.testing.assert_allclose(rec["theta"][1][n], first, rtol=1e-12, atol=1e-15)
