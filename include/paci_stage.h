@@ -214,9 +214,16 @@ int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_out, void* d
                         int* version);
 
 /* stage_step(): one AdamW update with G (the plain sum of the window's K local
- * gradients, Alg. 1), local step count t + 1 for bias correction, decoupled
- * weight decay on the w_* matrices; then G <- 0, c <- 0, t <- t + 1 and the bf16
- * working copy is rewritten. *new_version receives t. E_NOT_DUE if c != K. */
+ * gradients, Alg. 1), decoupled weight decay on the w_* matrices; then G <- 0,
+ * c <- 0, t <- t + 1 and the bf16 working copy is rewritten. *new_version
+ * receives t. E_NOT_DUE if c != K.
+ * Non-finite guard (the paper has none; its limitations section leaves invalid
+ * gradients unhandled): if any element of G is NaN or infinite, parameters and
+ * moments are left unchanged, G is still cleared and t still advances, so the
+ * version stamps stay a function of the event order alone. The decision is
+ * taken on the device (no host synchronization). AdamW's bias correction and
+ * the learning-rate schedule use a = (updates applied so far) + 1, which equals
+ * t + 1 while no update was skipped. */
 int paci_stage_step(paci_stage* h, int* new_version);
 
 /* ---- schedule driver --------------------------------------------------------- */
@@ -232,10 +239,16 @@ int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, const int32_t* 
                    const void* dev_grad_out_all, void* dev_out_all, void* dev_grad_in_all,
                    int32_t* host_stamps);
 
-/* Rewinds the counters to t = c = q = 0, next_f = next_b = 0, keeping
- * parameters, moments and G (pending windowed weight gradients are added to G
- * first); used to replay again from the current state. */
+/* Rewinds the counters to t = c = q = 0, next_f = next_b = 0 and the applied /
+ * skipped update counts to 0, keeping parameters, moments and G (pending
+ * windowed weight gradients are added to G first); used to replay again from
+ * the current state. */
 int paci_stage_reset_counters(paci_stage* h);
+
+/* Number of updates paci_stage_step applied and skipped (non-finite G) since
+ * creation or the last paci_stage_reset_counters, which clears both.
+ * Synchronizes the stream. Errors: E_INVAL (null pointer), E_HIP. */
+int paci_stage_updates(paci_stage* h, int32_t* applied, int32_t* skipped);
 
 /* ---- introspection ------------------------------------------------------------- */
 int paci_stage_counters(const paci_stage* h, paci_counters* out);

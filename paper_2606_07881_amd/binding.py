@@ -81,6 +81,7 @@ def _load():
         "paci_stage_step": (I, [P, ctypes.POINTER(I)]),
         "paci_stage_run": (I, [P, I, P, P, P, P, P, I32P]),
         "paci_stage_reset_counters": (I, [P]),
+        "paci_stage_updates": (I, [P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
         "paci_stage_counters": (I, [P, ctypes.POINTER(PaciCounters)]),
         "paci_stage_sync": (I, [P]),
         "paci_last_hip_error": (I, [P]),
@@ -304,6 +305,12 @@ class Stage:
 
     def reset_counters(self):
         _check(lib.paci_stage_reset_counters(self.h), "paci_stage_reset_counters")
+
+    def updates(self):
+        """(applied, skipped): updates the step applied and skipped (non-finite G)."""
+        a, k = ctypes.c_int32(), ctypes.c_int32()
+        _check(lib.paci_stage_updates(self.h, ctypes.byref(a), ctypes.byref(k)), "paci_stage_updates")
+        return a.value, k.value
 
     def counters(self):
         c = PaciCounters()

@@ -99,13 +99,21 @@ hipError_t ce_bwd(DType dt, const float* z, int64_t ldz, const int32_t* tgt, con
                   float scale, hipStream_t st);
 
 // ---- AdamW over the flat parameter arena --------------------------------------------------
-// One launch over every parameter: chunks[i] = {begin, end, decay, 0} (elements;
-// begin/end multiples of 4). theta <- theta * (1 - lr * wd * decay), then the
-// bias-corrected Adam direction; m, v updated; G cleared; theta_bf16 (nullable)
-// rewritten with the new theta.
-struct AdamwArgs { float lr, beta1, beta2, eps, weight_decay, bc1, bc2; };
+// ctl: 4 device ints {G not finite, updates applied, updates skipped, unused}.
+// adamw_guard: ctl[0] = 1 if any of the n values of G is not finite (else ctl[0]
+// is left as is: clear it first with adamw_ctl(..., 0)).
+// adamw: one launch over every parameter: chunks[i] = {begin, end, decay, 0}
+// (elements; begin/end multiples of 4). Unless ctl[0] is set: with t = ctl[1] + 1,
+// theta <- theta * (1 - lr_t * wd * decay), then the Adam direction with bias
+// correction of step t; m, v updated; theta_bf16 (nullable) rewritten. G is
+// cleared either way. lr_t follows the schedule (lr_total = 0: lr).
+// adamw_ctl: mode 0 clears ctl[0]; 1 counts the update (ctl[1] or ctl[2]);
+// 2 clears all of ctl.
+struct AdamwArgs { float lr, beta1, beta2, eps, weight_decay, lr_min_ratio; int lr_warmup, lr_total; };
+hipError_t adamw_guard(const float* G, int64_t n, int* ctl, hipStream_t st);
 hipError_t adamw(float* theta, float* G, float* m, float* v, void* theta_bf16, const int4* chunks, int nchunks,
-                 const AdamwArgs& a, hipStream_t st);
+                 const AdamwArgs& a, const int* ctl, hipStream_t st);
+hipError_t adamw_ctl(int* ctl, int mode, hipStream_t st);
 // dst (bf16) = round-to-nearest-even(src), n elements.
 hipError_t f32_to_bf16(const float* src, void* dst, int64_t n, hipStream_t st);
 // dst [cols, rows] = src [rows, cols]^T for 16-bit elements; rows, cols multiples of 8.

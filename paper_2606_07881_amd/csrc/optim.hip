@@ -6,6 +6,8 @@
 // and writes theta, m, v, the bf16 working copy and G = 0. That is 16 B read
 // and 14 B (bf16) or 12 B (fp32 stage) written per parameter, plus the 4 B
 // G clear, with no reuse.
+#include <algorithm>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -14,13 +16,33 @@ namespace {
 
 constexpr int NT = 256;
 
+// Learning rate of update t (1-based): linear warmup, then a cosine down to
+// lr_min_ratio of the peak at update lr_total; lr_total = 0: the constant rate.
+__device__ double lr_at(const AdamwArgs& a, int t) {
+  if (a.lr_total <= 0) return a.lr;
+  if (t <= a.lr_warmup) return (double)a.lr * t / a.lr_warmup;
+  const double p = fmin(1.0, (double)(t - a.lr_warmup) / (double)max(1, a.lr_total - a.lr_warmup));
+  const double r = a.lr_min_ratio;
+  return a.lr * (r + (1.0 - r) * 0.5 * (1.0 + cos(3.14159265358979323846 * p)));
+}
+
 __global__ void __launch_bounds__(NT) adamw_kernel(float* __restrict__ theta, float* __restrict__ G,
                                                     float* __restrict__ m, float* __restrict__ v, bf16* theta16,
-                                                    const int4* __restrict__ chunks, AdamwArgs a) {
+                                                    const int4* __restrict__ chunks, AdamwArgs a,
+                                                    const int* __restrict__ ctl) {
   const int4 ch = chunks[blockIdx.x];
-  const float decay = ch.z ? (1.f - a.lr * a.weight_decay) : 1.f;
-  const float step = a.lr / a.bc1;
-  const float rbc2 = 1.f / sqrtf(a.bc2);
+  if (ctl[0] != 0) {   // non-finite G: no update, G cleared
+    for (int64_t i = (int64_t)ch.x + 4 * (int64_t)threadIdx.x; i < ch.y; i += 4 * NT)
+      *reinterpret_cast<floatx4*>(G + i) = floatx4{0.f, 0.f, 0.f, 0.f};
+    return;
+  }
+  const int t = ctl[1] + 1;   // applied updates so far + 1: bias correction and schedule step
+  const float lr = (float)lr_at(a, t);
+  const float bc1 = (float)(1.0 - pow((double)a.beta1, (double)t));
+  const float bc2 = (float)(1.0 - pow((double)a.beta2, (double)t));
+  const float decay = ch.z ? (1.f - lr * a.weight_decay) : 1.f;
+  const float step = lr / bc1;
+  const float rbc2 = 1.f / sqrtf(bc2);
   for (int64_t i = (int64_t)ch.x + 4 * (int64_t)threadIdx.x; i < ch.y; i += 4 * NT) {
     const floatx4 g = *reinterpret_cast<const floatx4*>(G + i);
     floatx4 th = *reinterpret_cast<const floatx4*>(theta + i);
@@ -48,6 +70,32 @@ __global__ void __launch_bounds__(NT) f32_to_bf16_kernel(const float* __restrict
     *reinterpret_cast<u32x2*>(dst + i) = u32x2{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
   } else {
     for (int64_t j = i; j < n; ++j) dst[j] = (bf16)src[j];
+  }
+}
+
+// ctl[0] = 1 if any element is NaN or infinite (ordinary vector stores; every
+// writer stores the same value).
+__global__ void __launch_bounds__(NT) guard_kernel(const floatx4* __restrict__ G, int64_t vecs, int* ctl) {
+  bool bad = false;
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < vecs; i += (int64_t)gridDim.x * NT) {
+    const floatx4 g = G[i];
+    bad |= !__builtin_isfinite(g[0]) | !__builtin_isfinite(g[1]) | !__builtin_isfinite(g[2]) |
+           !__builtin_isfinite(g[3]);
+  }
+  if (bad) ctl[0] = 1;
+}
+
+// mode 0: clear the non-finite flag; 1: count the update as applied or skipped;
+// 2: clear every counter.
+__global__ void ctl_kernel(int* ctl, int mode) {
+  if (threadIdx.x != 0) return;
+  if (mode == 0) {
+    ctl[0] = 0;
+  } else if (mode == 1) {
+    if (ctl[0]) ctl[2] = ctl[2] + 1;
+    else ctl[1] = ctl[1] + 1;
+  } else {
+    ctl[0] = ctl[1] = ctl[2] = ctl[3] = 0;
   }
 }
 
@@ -88,10 +136,24 @@ hipError_t transpose16(const void* src, void* dst, int rows, int cols, hipStream
 }
 
 hipError_t adamw(float* theta, float* G, float* m, float* v, void* theta_bf16, const int4* chunks, int nchunks,
-                 const AdamwArgs& a, hipStream_t st) {
-  if (nchunks <= 0) return hipErrorInvalidValue;
+                 const AdamwArgs& a, const int* ctl, hipStream_t st) {
+  if (nchunks <= 0 || ctl == nullptr) return hipErrorInvalidValue;
   hipLaunchKernelGGL(adamw_kernel, dim3(nchunks), dim3(NT), 0, st, theta, G, m, v, reinterpret_cast<bf16*>(theta_bf16),
-                     chunks, a);
+                     chunks, a, ctl);
+  return hipGetLastError();
+}
+
+hipError_t adamw_guard(const float* G, int64_t n, int* ctl, hipStream_t st) {
+  if (n <= 0 || n % 4) return hipErrorInvalidValue;
+  const int64_t vecs = n / 4;
+  const int blocks = (int)std::min<int64_t>(4096, (vecs + NT - 1) / NT);
+  hipLaunchKernelGGL(guard_kernel, dim3(blocks), dim3(NT), 0, st, reinterpret_cast<const floatx4*>(G), vecs, ctl);
+  return hipGetLastError();
+}
+
+hipError_t adamw_ctl(int* ctl, int mode, hipStream_t st) {
+  if (mode < 0 || mode > 2) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ctl_kernel, dim3(1), dim3(64), 0, st, ctl, mode);
   return hipGetLastError();
 }
 

@@ -253,7 +253,7 @@ struct Layout {
   int64_t P = 0;          // parameters
   int64_t T = 0;          // tokens per micro-batch
   int64_t ldz = 0;        // logits row stride (last stage)
-  size_t theta, G, m, v, theta16, theta16T = 0, chunks, zeros;
+  size_t theta, G, m, v, theta16, theta16T = 0, chunks, zeros, ctl = 0;
   bool wT = false;             // transposed bf16 block weights kept (theta16T)
   int nchunks = 0;
   size_t stash, slot_bytes;
@@ -301,6 +301,7 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
   L.nchunks = count_chunks(p);
   L.chunks = a.take(16 * (size_t)L.nchunks);
   L.zeros = a.take(256);  // never written after init: source of out-of-range GEMM tile slots
+  L.ctl = a.take(256);    // update control: {G not finite, updates applied, updates skipped, 0}
 
   // one activation slot
   Bump sl;
@@ -702,17 +703,6 @@ int flush_window(paci_stage* h) {
   return PACI_OK;
 }
 
-// Learning rate of update t (1-based): linear warmup to the peak, then a cosine
-// down to lr_min_ratio of it at update lr_total (appendix "Detailed
-// experimental setup"); lr_total = 0: the constant rate.
-double lr_at(const paci_shapes& s, int t) {
-  if (s.lr_total <= 0) return s.lr;
-  if (t <= s.lr_warmup) return (double)s.lr * t / s.lr_warmup;
-  const double p = std::min(1.0, (double)(t - s.lr_warmup) / std::max(1, s.lr_total - s.lr_warmup));
-  const double r = s.lr_min_ratio;
-  return s.lr * (r + (1.0 - r) * 0.5 * (1.0 + std::cos(3.14159265358979323846 * p)));
-}
-
 // The stage forward of one micro-batch into the activation area A (its slot, or
 // the work slot of a checkpointed stage). in: the stage input (middle, last);
 // x0_copy: where block 0 keeps it; ids / tgt: the micro-batch's token ids (first
@@ -1008,22 +998,27 @@ extern "C" int paci_stage_step(paci_stage* h, int* new_version) {
   if (h->fsm.c != h->fsm.K) return PACI_E_NOT_DUE;
   if (h->broken) return PACI_E_HIP;
   const paci_shapes& s = h->s;
-  const int t_adam = h->fsm.t + 1;
   paci::AdamwArgs a;
-  a.lr = (float)lr_at(s, t_adam);
+  a.lr = s.lr;
   a.beta1 = s.beta1;
   a.beta2 = s.beta2;
   a.eps = s.eps;
   a.weight_decay = s.weight_decay;
-  a.bc1 = (float)(1.0 - std::pow((double)s.beta1, t_adam));
-  a.bc2 = (float)(1.0 - std::pow((double)s.beta2, t_adam));
+  a.lr_min_ratio = s.lr_min_ratio;
+  a.lr_warmup = s.lr_warmup;
+  a.lr_total = s.lr_total;
+  int* ctl = reinterpret_cast<int*>(h->arena + h->L.ctl);
   TRY(flush_window(h));
+  // the non-finite guard decides on the device: no host synchronization
+  TRY(run(h, F_ADAMW, 0.0, [&] { return paci::adamw_ctl(ctl, 0, h->st); }));
+  TRY(run(h, F_ADAMW, 4.0 * (double)h->p.total, [&] { return paci::adamw_guard(h->G(), h->p.total, ctl, h->st); }));
   const int r = run(h, F_ADAMW, 30.0 * (double)h->p.total, [&] {
     return paci::adamw(h->theta(), h->G(), h->m(), h->v(),
                        h->dt == paci::DT_BF16 ? (void*)(h->arena + h->L.theta16) : nullptr,
-                       reinterpret_cast<const int4*>(h->arena + h->L.chunks), h->L.nchunks, a, h->st);
+                       reinterpret_cast<const int4*>(h->arena + h->L.chunks), h->L.nchunks, a, ctl, h->st);
   });
   if (r) return r;
+  TRY(run(h, F_ADAMW, 0.0, [&] { return paci::adamw_ctl(ctl, 1, h->st); }));
   TRY(refresh_wT(h));
   fsm_commit_step(h->fsm);
   h->win_done = 0;
@@ -1083,10 +1078,27 @@ extern "C" int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, cons
   return PACI_OK;
 }
 
+extern "C" int paci_stage_updates(paci_stage* h, int32_t* applied, int32_t* skipped) {
+  if (!h || !applied || !skipped) return PACI_E_INVAL;
+  if (h->broken) return PACI_E_HIP;
+  int ctl[4] = {0, 0, 0, 0};
+  hipError_t e = hipMemcpyAsync(ctl, h->arena + h->L.ctl, sizeof(ctl), hipMemcpyDeviceToHost, h->st);
+  if (e == hipSuccess) e = hipStreamSynchronize(h->st);
+  if (e != hipSuccess) {
+    h->last_hip = (int)e;
+    return PACI_E_HIP;
+  }
+  *applied = ctl[1];
+  *skipped = ctl[2];
+  return PACI_OK;
+}
+
 extern "C" int paci_stage_reset_counters(paci_stage* h) {
   if (!h) return PACI_E_INVAL;
   if (!h->broken) TRY(flush_window(h));   // G keeps what the backwards so far accumulated
   h->win_done = 0;
+  if (!h->broken)   // update counts restart with the version (bias correction from step 1)
+    TRY(run(h, F_ADAMW, 0.0, [&] { return paci::adamw_ctl(reinterpret_cast<int*>(h->arena + h->L.ctl), 2, h->st); }));
   h->fsm.t = h->fsm.c = h->fsm.q = h->fsm.next_f = h->fsm.next_b = 0;
   return PACI_OK;
 }

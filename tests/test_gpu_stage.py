@@ -2,8 +2,8 @@
 import numpy as np
 import pytest
 
-from parity import (Inputs, compare_replays, gpu_replay, oracle_replay, oracle_sensitivity, rel_err, small_cfg,
-                    to_host, to_torch, tol, unflatten)
+from parity import (Inputs, adamw_np, compare_replays, gpu_replay, oracle_replay, oracle_sensitivity, rel_err,
+                    small_cfg, to_host, to_torch, tol, unflatten)
 from oracle import schedule as osched
 from oracle import stage as ostage
 from paper_2606_07881_amd import configs, inputs
@@ -163,4 +163,56 @@ def test_protocol_errors_leave_state_unchanged(binding):
     # null pointers are refused
     assert st.try_forward(3, None, outs[3]) == binding.E_INVAL
     assert st.try_backward(2, None) == binding.E_INVAL
+    st.close()
+
+
+def test_nonfinite_gradient_skips_the_update(binding):
+    """A window whose G holds a NaN or an infinity: the step leaves theta, m and v
+    bit-for-bit unchanged, clears G and still advances the version; the next
+    window's update is AdamW's first (bias correction and rate schedule at
+    update 1) on the GPU's own G, as the oracle's guard defines it."""
+    import torch
+    c = small_cfg("sched_bf16")
+    inp = Inputs(c, 5, 4)
+    T, d = c["micro_batch"] * c["seq"], c["d_model"]
+    st = binding.Stage(c, K=2, delay=1)
+    st.load_params(inp.params)
+    xs = [to_torch(a) for a in inp.x_dev]
+    dys = [to_torch(a) for a in inp.dy_dev]
+    out = torch.zeros(T, d, dtype=st.act_dtype, device="cuda")
+
+    def window(i0):
+        for i in (i0, i0 + 1):
+            st.forward(i, xs[i], out)
+            v, due = st.backward(i, dys[i])
+        assert due
+
+    window(0)
+    th0, m0, v0 = st.read(binding.PARAMS), st.read(binding.EXP_AVG), st.read(binding.EXP_AVG_SQ)
+    G = st.read(binding.GRADS)
+    assert np.isfinite(G).all()
+    G[7] = np.nan
+    G[-3] = np.inf
+    st.load(binding.GRADS, G)
+    assert st.step() == 1
+    assert st.updates() == (0, 1)
+    assert np.array_equal(st.read(binding.PARAMS).view(np.uint32), th0.view(np.uint32))
+    assert np.array_equal(st.read(binding.EXP_AVG).view(np.uint32), m0.view(np.uint32))
+    assert np.array_equal(st.read(binding.EXP_AVG_SQ).view(np.uint32), v0.view(np.uint32))
+    assert not st.read(binding.GRADS).any()
+
+    window(2)
+    G2 = unflatten(c, st.read(binding.GRADS))
+    assert st.step() == 2
+    assert st.updates() == (1, 1)
+    th0d = unflatten(c, th0)
+    th, m, v = (unflatten(c, st.read(w)) for w in (binding.PARAMS, binding.EXP_AVG, binding.EXP_AVG_SQ))
+    for n in th:
+        g = np.asarray(G2[n], np.float64)
+        th_x, m_x, v_x = adamw_np(np.asarray(th0d[n], np.float64), g, np.zeros_like(g), np.zeros_like(g), 1, c,
+                                  ostage.decayed(n))
+        e = max(rel_err(th[n], th_x), rel_err(m[n], m_x), rel_err(v[n], v_x))
+        assert e <= 1e-5, f"{n}: update after a skipped one differs from AdamW's first: {e:.3e}"
+    st.reset_counters()
+    assert st.updates() == (0, 0)
     st.close()
