@@ -89,6 +89,29 @@ def canonical_events(M, K, delay):
     return ev
 
 
+def flush_events(M, K, delay):
+    """Synchronous 1F1B with a flush (Sec. 2, Eq. (3)) seen at one stage.
+
+    Each window of K micro-batches runs on its own: the stage's first forwards
+    (up to delay + 1 of them, the warm-up of the 1F1B order), then one backward
+    and, while the window has one left, one forward; the update follows the
+    window's last backward, and the next window starts only after it. Every
+    forward and backward of a window then sees the same version (Delta = 0).
+    A trailing partial window gets no update.
+    """
+    ev = []
+    for a in range(0, M, K):
+        b = min(M, a + K)
+        ev += [("F", i) for i in range(a, min(a + delay + 1, b))]
+        for j in range(a, b):
+            ev.append(("B", j))
+            if j + delay + 1 < b:
+                ev.append(("F", j + delay + 1))
+        if b - a == K:
+            ev.append(("S", None))
+    return ev
+
+
 def run_events(events, K, delay):
     """Drive StageCounters through ``events``; return (tF, tB, delta, n_updates)."""
     sc = StageCounters(K, delay)

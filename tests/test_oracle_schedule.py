@@ -123,3 +123,33 @@ def test_table1_projection():
     for c in cols:
         proj = pipeline.paci_throughput_proxy(c["flush"], c["m"], c["gpus"])
         assert abs(proj - c["paci"]) <= 0.005 + 1e-9, c
+
+
+def test_flush_order_by_hand():
+    # Synchronous 1F1B with a flush at K = 4: at delay 3 each window fills the
+    # stage, drains it and updates; at delay 1 it alternates after one warm-up.
+    assert schedule.events_to_string(schedule.flush_events(8, 4, 3)) == \
+        "F0 F1 F2 F3 B0 B1 B2 B3 S F4 F5 F6 F7 B4 B5 B6 B7 S"
+    assert schedule.events_to_string(schedule.flush_events(8, 4, 1)) == \
+        "F0 F1 B0 F2 B1 F3 B2 B3 S F4 F5 B4 F6 B5 F7 B6 B7 S"
+    # a trailing partial window has no update
+    assert schedule.events_to_string(schedule.flush_events(5, 2, 0)) == "F0 B0 F1 B1 S F2 B2 F3 B3 S F4 B4"
+
+
+@pytest.mark.parametrize("M,K,delay", [(16, 4, 3), (64, 8, 3), (128, 16, 7), (10, 3, 5), (7, 2, 9), (0, 2, 1)])
+def test_flush_order_has_no_crossings(M, K, delay):
+    """Alg. 1's counters accept the flush order (it never exceeds the admission
+    window) and stamp every micro-batch with Delta = 0, against sum Delta =
+    delay * (M/K - 1) for the asynchronous order when delay <= K divides M."""
+    ev = schedule.flush_events(M, K, delay)
+    assert len(ev) == 2 * M + M // K
+    tF, tB, delta, n_upd = schedule.run_events(ev, K, delay)
+    assert delta == [0] * M and n_upd == M // K
+    assert tF == [i // K for i in range(M)] == tB
+
+
+@pytest.mark.parametrize("M,K,delay", [(6, 2, 1), (6, 3, 2), (8, 4, 3), (6, 1, 2)])
+def test_flush_order_is_one_of_the_admissible_interleavings(M, K, delay):
+    # the synchronous order is a special case of Alg. 1: a stage that waits
+    flush = schedule.flush_events(M, K, delay)
+    assert any(list(o) == flush for o in schedule.all_admissible_orders(M, K, delay))

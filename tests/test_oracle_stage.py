@@ -263,3 +263,27 @@ def test_nonfinite_gradient_skips_the_update():
         th0 = np.asarray(params[n], np.float64)
         first = (th0 * (1 - lr * wd) if stage.decayed(n) else th0) - lr * g / (np.abs(g) + cfg["eps"])
         np.testing.assert_allclose(rec["theta"][1][n], first, rtol=1e-12, atol=1e-15)
+
+
+@pytest.mark.parametrize("kind", ["middle", "last"])
+def test_flush_order_equals_synchronous_training(kind):
+    """The synchronous 1F1B-with-flush order, at any delay, is plain synchronous
+    gradient accumulation: the replay equals the fwd; bwd; AdamW loop, while the
+    asynchronous order at the same delay differs after the first update."""
+    cfg = _cfg(kind=kind)
+    K, delay, M = 2, 3, 6
+    params, xs, dys, tg = _data(cfg, M, seed=4)
+    go = None if kind == "last" else dys
+    tgs = tg if kind == "last" else None
+    rec = stage.replay(cfg, params, K, delay, xs, go, tgs, events=schedule.flush_events(M, K, delay))
+    outs, gins, Gs, thetas = _sync_loop(cfg, params, xs, dys, tg, K)
+    assert rec["delta"] == [0] * M
+    for i in range(M):
+        np.testing.assert_allclose(rec["out"][i], outs[i], rtol=1e-13, atol=1e-13)
+        np.testing.assert_allclose(rec["grad_in"][i], gins[i], rtol=1e-13, atol=1e-13)
+    for s in range(M // K):
+        for n in thetas[s]:
+            np.testing.assert_allclose(rec["theta"][s][n], thetas[s][n], rtol=1e-13, atol=1e-15)
+    paci = stage.replay(cfg, params, K, delay, xs, go, tgs)
+    assert sum(paci["delta"]) > 0
+    assert max(np.abs(paci["theta"][-1][n] - thetas[-1][n]).max() for n in thetas[-1]) > 1e-6
