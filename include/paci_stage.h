@@ -127,6 +127,15 @@ int paci_fsm_destroy(paci_fsm* f);
  * (then *n still receives the required count). */
 int paci_schedule(int M, int K, int delay, int32_t* kinds, int32_t* idx, int cap, int* n);
 
+/* Synchronous 1F1B with a flush, the comparison schedule of Sec. 2 and Eq. (3),
+ * at one stage: window by window (micro-batches wK .. wK+K-1), the forwards
+ * F_wK .. F_wK+min(delay, K-1), then B_j followed by F_j+delay+1 while it lies
+ * in the window, and the update after the window's last backward. No forward of
+ * a window runs before the previous window's update, so every stamp has
+ * Delta = 0. Same arrays, count and errors as paci_schedule; a trailing partial
+ * window (M % K != 0) has no update. */
+int paci_schedule_flush(int M, int K, int delay, int32_t* kinds, int32_t* idx, int cap, int* n);
+
 /* ---- parameter layout (host only) ------------------------------------------
  * The canonical order: first stage prefix wte [V, d], wpe [max_pos, d]; per
  * block l: h{l}.ln1_g, ln1_b, w_qkv [3d, d], b_qkv, w_o [d, d], b_o, ln2_g,
@@ -238,6 +247,18 @@ int paci_stage_step(paci_stage* h, int* new_version);
 int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, const int32_t* dev_targets_all,
                    const void* dev_grad_out_all, void* dev_out_all, void* dev_grad_in_all,
                    int32_t* host_stamps);
+
+/* Replays the event list (kinds[e], idx[e]) for e < n, in the encoding of
+ * paci_schedule (e.g. paci_schedule_flush's order), with the buffers and
+ * stamps of paci_stage_run (host_stamps needs 3 entries per micro-batch index
+ * used). Host arrays. The list is checked first (kinds in {0, 1, 2}, idx >= 0
+ * for forwards and backwards: else E_INVAL and nothing runs); each event then
+ * goes through the protocol, and the first error is returned with the events
+ * before it done. The handle must be fresh, as for paci_stage_run. */
+int paci_stage_run_events(paci_stage* h, int n, const int32_t* kinds, const int32_t* idx,
+                          const void* dev_in_all, const int32_t* dev_targets_all,
+                          const void* dev_grad_out_all, void* dev_out_all, void* dev_grad_in_all,
+                          int32_t* host_stamps);
 
 /* Rewinds the counters to t = c = q = 0, next_f = next_b = 0 and the applied /
  * skipped update counts to 0, keeping parameters, moments and G (pending

@@ -69,6 +69,7 @@ def _load():
         "paci_fsm_counters": (I, [P, ctypes.POINTER(PaciCounters)]),
         "paci_fsm_destroy": (I, [P]),
         "paci_schedule": (I, [I, I, I, I32P, I32P, I, ctypes.POINTER(I)]),
+        "paci_schedule_flush": (I, [I, I, I, I32P, I32P, I, ctypes.POINTER(I)]),
         "paci_param_count": (I, [ctypes.POINTER(PaciShapes), ctypes.POINTER(I), ctypes.POINTER(I64)]),
         "paci_param_info_at": (I, [ctypes.POINTER(PaciShapes), I, ctypes.POINTER(PaciParamInfo)]),
         "paci_stage_arena_bytes": (I, [ctypes.POINTER(PaciShapes), I, I, ctypes.POINTER(SZ)]),
@@ -80,6 +81,7 @@ def _load():
         "paci_stage_backward": (I, [P, I, P, P, ctypes.POINTER(I)]),
         "paci_stage_step": (I, [P, ctypes.POINTER(I)]),
         "paci_stage_run": (I, [P, I, P, P, P, P, P, I32P]),
+        "paci_stage_run_events": (I, [P, I, I32P, I32P, P, P, P, P, P, I32P]),
         "paci_stage_reset_counters": (I, [P]),
         "paci_stage_updates": (I, [P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
         "paci_stage_counters": (I, [P, ctypes.POINTER(PaciCounters)]),
@@ -137,15 +139,17 @@ def shapes(cfg):
 
 
 # ---- host-only calls ----------------------------------------------------------------------
-def schedule(M, K, delay):
-    """paci_schedule: returns (kinds, idx) int32 arrays (0 = F, 1 = B, 2 = step)."""
+def schedule(M, K, delay, flush=False):
+    """paci_schedule (asynchronous 1F1B) or, with ``flush``, paci_schedule_flush
+    (synchronous 1F1B with a flush per window): returns (kinds, idx) int32
+    arrays (0 = F, 1 = B, 2 = step)."""
     n = ctypes.c_int(0)
     cap = 2 * M + M // max(K, 1) + 1
     kinds = np.zeros(cap, np.int32)
     idx = np.zeros(cap, np.int32)
-    _check(lib.paci_schedule(M, K, delay, kinds.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
-                             idx.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), cap, ctypes.byref(n)),
-           "paci_schedule")
+    name = "paci_schedule_flush" if flush else "paci_schedule"
+    _check(getattr(lib, name)(M, K, delay, kinds.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                              idx.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), cap, ctypes.byref(n)), name)
     return kinds[:n.value].copy(), idx[:n.value].copy()
 
 
@@ -302,6 +306,20 @@ class Stage:
                                   stamps.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))),
                "paci_stage_run")
         return stamps
+
+    def run_events(self, kinds, idx, in_all, grad_out_all=None, out_all=None, grad_in_all=None, targets_all=None):
+        """paci_stage_run_events: replays the (kinds, idx) list; returns stamps [M, 3]
+        for micro-batch indices 0 .. max(idx)."""
+        kinds = np.ascontiguousarray(kinds, np.int32)
+        idx = np.ascontiguousarray(idx, np.int32)
+        M = int(idx.max()) + 1 if idx.size else 0
+        stamps = np.zeros((max(M, 1), 3), np.int32)
+        i32 = ctypes.POINTER(ctypes.c_int32)
+        _check(lib.paci_stage_run_events(self.h, kinds.size, kinds.ctypes.data_as(i32), idx.ctypes.data_as(i32),
+                                         _ptr(in_all), ctypes.cast(_ptr(targets_all), i32), _ptr(grad_out_all),
+                                         _ptr(out_all), _ptr(grad_in_all), stamps.ctypes.data_as(i32)),
+               "paci_stage_run_events")
+        return stamps[:M]
 
     def reset_counters(self):
         _check(lib.paci_stage_reset_counters(self.h), "paci_stage_reset_counters")

@@ -141,6 +141,26 @@ extern "C" int paci_schedule(int M, int K, int delay, int32_t* kinds, int32_t* i
   return PACI_OK;
 }
 
+extern "C" int paci_schedule_flush(int M, int K, int delay, int32_t* kinds, int32_t* idx, int cap, int* n) {
+  if (M < 0 || K < 1 || delay < 0 || !n) return PACI_E_INVAL;
+  const int total = 2 * M + M / K;
+  *n = total;
+  if (cap < total || (total > 0 && (!kinds || !idx))) return PACI_E_INVAL;
+  int e = 0;
+  auto emit = [&](int k, int i) { kinds[e] = k; idx[e] = i; ++e; };
+  // window by window; a window's forwards wait for the previous window's update
+  for (int a = 0; a < M; a += K) {
+    const int b = std::min(M, a + K);
+    for (int i = a; i < std::min(a + delay + 1, b); ++i) emit(0, i);
+    for (int j = a; j < b; ++j) {
+      emit(1, j);
+      if (j + delay + 1 < b) emit(0, j + delay + 1);
+    }
+    if (b - a == K) emit(2, -1);
+  }
+  return PACI_OK;
+}
+
 // ============================================================================================
 // Parameter layout
 // ============================================================================================
@@ -1026,16 +1046,17 @@ extern "C" int paci_stage_step(paci_stage* h, int* new_version) {
   return PACI_OK;
 }
 
-extern "C" int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, const int32_t* dev_targets_all,
-                              const void* dev_grad_out_all, void* dev_out_all, void* dev_grad_in_all,
-                              int32_t* host_stamps) {
-  if (!h || M < 0 || !dev_in_all) return PACI_E_INVAL;
+extern "C" int paci_stage_run_events(paci_stage* h, int n, const int32_t* kinds, const int32_t* idx,
+                                     const void* dev_in_all, const int32_t* dev_targets_all,
+                                     const void* dev_grad_out_all, void* dev_out_all, void* dev_grad_in_all,
+                                     int32_t* host_stamps) {
+  if (!h || n < 0 || !dev_in_all || (n > 0 && (!kinds || !idx))) return PACI_E_INVAL;
+  for (int e = 0; e < n; ++e)   // the whole list is checked before any event runs
+    if (kinds[e] < 0 || kinds[e] > 2 || (kinds[e] < 2 && idx[e] < 0)) return PACI_E_INVAL;
   const paci_shapes& s = h->s;
   if (s.kind == PACI_LAST && !dev_targets_all) return PACI_E_INVAL;
   if (s.kind != PACI_LAST && !dev_grad_out_all) return PACI_E_INVAL;
   if (h->fsm.next_f != 0 || h->fsm.next_b != 0 || h->fsm.c != 0) return PACI_E_ORDER;
-  const paci_fsm& f = h->fsm;
-  const int K = f.K, delay = f.delay;
   const int64_t T = h->L.T;
   const size_t act = act_bytes(h);
   const size_t in_stride = s.kind == PACI_FIRST ? 4 * (size_t)T : act;
@@ -1043,10 +1064,7 @@ extern "C" int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, cons
   // scratch outputs when the caller discards them
   char* out_scratch = h->ws(h->L.w_dyB);
   float* loss_scratch = reinterpret_cast<float*>(h->ws(h->L.w_loss));
-  std::vector<int32_t> kinds(2 * (size_t)M + M / K + 1), idx(kinds.size());
-  int n = 0;
-  int r = paci_schedule(M, K, delay, kinds.data(), idx.data(), (int)kinds.size(), &n);
-  if (r) return r;
+  int r = PACI_OK;
   for (int e = 0; e < n; ++e) {
     const int i = idx[e];
     int ver = 0;
@@ -1076,6 +1094,18 @@ extern "C" int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, cons
     }
   }
   return PACI_OK;
+}
+
+extern "C" int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, const int32_t* dev_targets_all,
+                              const void* dev_grad_out_all, void* dev_out_all, void* dev_grad_in_all,
+                              int32_t* host_stamps) {
+  if (!h || M < 0) return PACI_E_INVAL;
+  std::vector<int32_t> kinds(2 * (size_t)M + M / h->fsm.K + 1), idx(kinds.size());
+  int n = 0;
+  const int r = paci_schedule(M, h->fsm.K, h->fsm.delay, kinds.data(), idx.data(), (int)kinds.size(), &n);
+  if (r) return r;
+  return paci_stage_run_events(h, n, kinds.data(), idx.data(), dev_in_all, dev_targets_all, dev_grad_out_all,
+                               dev_out_all, dev_grad_in_all, host_stamps);
 }
 
 extern "C" int paci_stage_updates(paci_stage* h, int32_t* applied, int32_t* skipped) {

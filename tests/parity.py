@@ -239,9 +239,10 @@ def oracle_replay(c, inp, events=None, K=None, delay=None, grad_hook=None):
                          recompute=bool(c.get("recompute", 0)))
 
 
-def oracle_sensitivity(c, inp, ref, seed=12345):
+def oracle_sensitivity(c, inp, ref, seed=12345, events=None):
     """Oracle-only change of every compared quantity when each accumulated G is
-    perturbed by Gaussian noise of SENS_RHO[dtype] * max|G| before each update.
+    perturbed by Gaussian noise of SENS_RHO[dtype] * max|G| before each update
+    (``events``: the event list ``ref`` was replayed with, default canonical).
     Returns dict(out=[...], grad_in=[...], G=[{name: e}], m=..., v=..., theta=...)."""
     rng = np.random.default_rng(seed)
     rho = SENS_RHO[c["dtype"]]
@@ -249,7 +250,7 @@ def oracle_sensitivity(c, inp, ref, seed=12345):
     def hook(s, G):
         return {n: g + rho * np.abs(g).max() * rng.standard_normal(g.shape) for n, g in G.items()}
 
-    pert = oracle_replay(c, inp, grad_hook=hook)
+    pert = oracle_replay(c, inp, events=events, grad_hook=hook)
     out = dict(out=[], grad_in=[], G=[], m=[], v=[], theta=[])
     for i in range(len(ref["out"])):
         out["out"].append(rel_err(np.atleast_1d(pert["out"][i]), np.atleast_1d(ref["out"][i])))

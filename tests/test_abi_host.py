@@ -176,3 +176,19 @@ def test_init_refuses_bad_arguments_without_device_work():
                                        ctypes.byref(h)) == binding.E_INVAL
     assert binding.lib.paci_stage_init(ctypes.byref(s), 4, 3, ctypes.c_void_p(0x100000), 16, None,
                                        ctypes.byref(h)) == binding.E_NOMEM
+
+
+@pytest.mark.parametrize("M,K,delay", [(16, 4, 3), (64, 8, 3), (64, 8, 0), (128, 16, 7), (5, 1, 0),
+                                       (7, 3, 9), (0, 1, 0), (1, 2, 0), (13, 5, 2)])
+def test_flush_schedule_matches_oracle(M, K, delay):
+    kinds, idx = binding.schedule(M, K, delay, flush=True)
+    ev = osched.flush_events(M, K, delay)
+    lib_ev = [("F", int(i)) if k == 0 else ("B", int(i)) if k == 1 else ("S", None) for k, i in zip(kinds, idx)]
+    assert lib_ev == ev
+    n = ctypes.c_int(0)
+    k = np.zeros(1, np.int32)
+    p = k.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    if len(ev) > 1:
+        assert binding.lib.paci_schedule_flush(M, K, delay, p, p, 1, ctypes.byref(n)) == binding.E_INVAL
+        assert n.value == len(ev)
+    assert binding.lib.paci_schedule_flush(M, 0, delay, p, p, 1, ctypes.byref(n)) == binding.E_INVAL

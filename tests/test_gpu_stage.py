@@ -216,3 +216,53 @@ def test_nonfinite_gradient_skips_the_update(binding):
     st.reset_counters()
     assert st.updates() == (0, 0)
     st.close()
+
+
+@pytest.mark.parametrize("name", ["dh32_bf16", "tiny_fp32"])
+def test_flush_schedule_parity(binding, name):
+    """Synchronous 1F1B with a flush per window (Delta = 0 everywhere): the
+    event calls against the oracle replaying the same order, then the native
+    driver paci_stage_run_events on that order against the event calls."""
+    import torch
+    c = small_cfg(name) if name != "tiny_fp32" else configs.get(name)
+    M, K, delay = c["M"], c["K"], c["delay"]
+    inp = Inputs(c, 6, M)
+    ev = osched.flush_events(M, K, delay)
+    g = gpu_replay(c, inp, events=ev)
+    o = oracle_replay(c, inp, events=ev)
+    sens = oracle_sensitivity(c, inp, o, events=ev)
+    rep = compare_replays(c, g, o, sens=sens, theta0=inp.params)
+    print(name, "flush", {k: (f"{v:.2e}" if isinstance(v, float) else v) for k, v in rep.items()}, flush=True)
+    assert g["delta"] == [0] * M
+
+    kinds, idx = binding.schedule(M, K, delay, flush=True)
+    T, d = c["micro_batch"] * c["seq"], c["d_model"]
+    st = binding.Stage(c, K, delay)
+    st.load_params(inp.params)
+    x_all = torch.stack([to_torch(a) for a in inp.x_dev])
+    dy_all = torch.stack([to_torch(a) for a in inp.dy_dev])
+    out_all = torch.zeros(M, T, d, dtype=st.act_dtype, device="cuda")
+    gin_all = torch.zeros(M, T, d, dtype=st.act_dtype, device="cuda")
+    stamps = st.run_events(kinds, idx, x_all, dy_all, out_all, gin_all)
+    st.sync()
+    assert stamps[:, 0].tolist() == [i // K for i in range(M)] == stamps[:, 1].tolist()
+    assert stamps[:, 2].tolist() == [0] * M
+    lim = 1e-2 if c["dtype"] == "bf16" else 1e-5
+    for i in range(M):
+        assert rel_err(to_host(out_all[i]), g["out"][i]) <= lim
+        assert rel_err(to_host(gin_all[i]), g["grad_in"][i]) <= lim
+    theta = unflatten(c, st.read(binding.PARAMS))
+    for n in theta:
+        # fp32 atomics make G differ in its last bits between runs, and AdamW's
+        # normalized step can turn that into up to 2 lr per update where G ~ 0
+        assert np.abs(theta[n] - g["theta"][-1][n]).max() <= 2 * c["lr"] * (M // K) + 1e-6
+    # a malformed list is refused before any event runs
+    st.reset_counters()
+    before = st.read(binding.PARAMS)
+    bad = np.array([0, 1, 7], np.int32)
+    with pytest.raises(binding.PaciError) as ei:
+        st.run_events(bad, np.array([0, 0, 0], np.int32), x_all, dy_all)
+    assert ei.value.code == binding.E_INVAL
+    assert st.counters()["next_f"] == 0
+    assert np.array_equal(st.read(binding.PARAMS), before)
+    st.close()
