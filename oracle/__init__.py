@@ -20,6 +20,8 @@ stage     one stage's state (single parameter copy, fp32-style accumulator G,
           parameters read in the backward are the current version.
 pipeline  bubble-efficiency formulas (Eqs. 3-5) used only to pin the paper's
           printed numbers.
+partition the memory-constrained stage partitioning problem and its
+          infeasibility fallback, solved by exhaustive search.
 
 Every function states the passage of the paper it follows. Precision is
 float64 throughout; inputs that the GPU sees in bf16 are handed to the oracle as
