@@ -288,6 +288,37 @@ const char* paci_kernel_family_name(int family);
 int paci_stage_set_timing(paci_stage* h, int enable);
 int paci_stage_kernel_times(paci_stage* h, int family, int64_t* launches, double* ms, double* work);
 
+/* ---- stage planning (host only) --------------------------------------------------
+ * Memory-constrained partition of a sequential stack of L layers over N
+ * pipeline stages (appendix "Memory-constrained pipeline partitioning").
+ * Layer l (0-based) has forward time t[l], static bytes s[l] (parameters,
+ * gradients, optimizer state) and activation bytes a[l] per micro-batch. The
+ * stages hold contiguous, non-empty layer ranges; stage j (1-based) keeps
+ * w_j = N - j + 1 micro-batches in flight, so its memory is
+ * sum s + w_j * sum a over its layers. The result minimises the largest stage
+ * time subject to every stage's memory <= budget. If no partition fits, it
+ * minimises the largest overshoot max(0, memory - budget) first and the
+ * largest stage time second.
+ * cuts (host int32 [N + 1]) receives 0 = c_0 < c_1 < ... < c_N = L (stage j
+ * holds layers c_{j-1} .. c_j - 1); *max_time and *max_overshoot (nullable)
+ * the optimum, with *max_overshoot == 0 exactly when a partition fits. Among
+ * equal optima any one may be returned. Sums run left to right over each
+ * stage's layers, so integer-valued inputs give exact results. O(L^2 N) time.
+ * Errors: E_INVAL (N < 1, L < N, a null array, a negative or non-finite
+ * t/s/a, or a budget that is negative or NaN; it may be +infinity). */
+int paci_partition(int L, int N, const double* t, const double* s, const double* a, double budget,
+                   int32_t* cuts, double* max_time, double* max_overshoot);
+
+/* Bubble efficiency of synchronous 1F1B with a flush, m / (m + N - 1) (Eq. 3),
+ * and of interleaved 1F1B with V model chunks per device, mV / (mV + N - 1)
+ * (Eq. 4), for m micro-batches (real m > 0 allowed, as in the paper's worked
+ * values) on N stages; NaN if m <= 0, N < 1 or V < 1. */
+double paci_eta_flush(double m, int N);
+double paci_eta_interleaved(double m, int N, int V);
+/* Projected bubble-free throughput from a measured 1F1B-flush throughput,
+ * t_flush / eta_flush(m, N) (Eq. 5). */
+double paci_throughput_proxy(double t_flush, double m, int N);
+
 #ifdef __cplusplus
 }
 #endif

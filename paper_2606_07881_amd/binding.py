@@ -61,6 +61,7 @@ def _load():
                            "(the stage has no fallback implementation)")
     lib = ctypes.CDLL(LIB_PATH)
     P, I, I32P, I64, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.POINTER(ctypes.c_int32), ctypes.c_int64, ctypes.c_size_t
+    DP = ctypes.POINTER(ctypes.c_double)
     sig = {
         "paci_fsm_create": (I, [I, I, ctypes.POINTER(P)]),
         "paci_fsm_forward": (I, [P, I, ctypes.POINTER(I)]),
@@ -70,6 +71,10 @@ def _load():
         "paci_fsm_destroy": (I, [P]),
         "paci_schedule": (I, [I, I, I, I32P, I32P, I, ctypes.POINTER(I)]),
         "paci_schedule_flush": (I, [I, I, I, I32P, I32P, I, ctypes.POINTER(I)]),
+        "paci_partition": (I, [I, I, DP, DP, DP, ctypes.c_double, I32P, DP, DP]),
+        "paci_eta_flush": (ctypes.c_double, [ctypes.c_double, I]),
+        "paci_eta_interleaved": (ctypes.c_double, [ctypes.c_double, I, I]),
+        "paci_throughput_proxy": (ctypes.c_double, [ctypes.c_double, ctypes.c_double, I]),
         "paci_param_count": (I, [ctypes.POINTER(PaciShapes), ctypes.POINTER(I), ctypes.POINTER(I64)]),
         "paci_param_info_at": (I, [ctypes.POINTER(PaciShapes), I, ctypes.POINTER(PaciParamInfo)]),
         "paci_stage_arena_bytes": (I, [ctypes.POINTER(PaciShapes), I, I, ctypes.POINTER(SZ)]),
@@ -139,6 +144,20 @@ def shapes(cfg):
 
 
 # ---- host-only calls ----------------------------------------------------------------------
+def partition(t, s, a, N, budget=float("inf")):
+    """paci_partition: returns (cuts, max_time, max_overshoot); max_overshoot == 0
+    exactly when every stage fits the budget."""
+    t, s, a = (np.ascontiguousarray(x, np.float64) for x in (t, s, a))
+    assert t.shape == s.shape == a.shape and t.ndim == 1
+    cuts = np.zeros(max(N, 0) + 1, np.int32)
+    mt, mo = ctypes.c_double(), ctypes.c_double()
+    dp = ctypes.POINTER(ctypes.c_double)
+    _check(lib.paci_partition(t.size, N, t.ctypes.data_as(dp), s.ctypes.data_as(dp), a.ctypes.data_as(dp),
+                              float(budget), cuts.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                              ctypes.byref(mt), ctypes.byref(mo)), "paci_partition")
+    return cuts, mt.value, mo.value
+
+
 def schedule(M, K, delay, flush=False):
     """paci_schedule (asynchronous 1F1B) or, with ``flush``, paci_schedule_flush
     (synchronous 1F1B with a flush per window): returns (kinds, idx) int32

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libpaci_stage.so")
 EXE = os.path.join(HERE, "stage_bench")
-SOURCES = ["gemm.hip", "attention.hip", "rowwise.hip", "optim.hip", "stage.hip"]
+SOURCES = ["gemm.hip", "attention.hip", "rowwise.hip", "optim.hip", "stage.hip", "planner.cpp"]
 TOOLS = ["stage_bench.hip"]
 
 ARCH = "gfx950"
