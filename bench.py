@@ -28,6 +28,9 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_gpt2m_mid_bf16.md")
+WORKLOAD_SHAPE = {"gpt2s_mid_bf16": "GPT-2-small-shaped", "gpt2m_mid_bf16": "GPT-2-medium-shaped",
+                  "gpt2m_first_bf16": "GPT-2-medium-shaped", "gpt2m_last_bf16": "GPT-2-medium-shaped",
+                  "gpt1p3b_pos0_bf16": "1.3B-class"}
 
 
 def log(msg):
@@ -35,17 +38,27 @@ def log(msg):
 
 
 def make_device_inputs(torch, c, M, seed):
-    """Seeded N(0,1) stage inputs and N(0, 0.01^2) output gradients, bf16, [M, T, d]."""
+    """Seeded stage inputs [M, T, d] (N(0,1); token ids uniform over the vocabulary
+    for a first stage), output gradients [M, T, d] (N(0, 0.01^2); none for a
+    last stage) and targets [M, T] (uniform; last stage only)."""
     T, d = c["micro_batch"] * c["seq"], c["d_model"]
     g = torch.Generator(device="cuda")
     g.manual_seed(seed)
     dt = torch.bfloat16 if c["dtype"] == "bf16" else torch.float32
-    x = torch.empty(M, T, d, dtype=dt, device="cuda")
-    dy = torch.empty(M, T, d, dtype=dt, device="cuda")
-    for i in range(M):
-        x[i].copy_(torch.randn(T, d, generator=g, device="cuda"))
-        dy[i].copy_(torch.randn(T, d, generator=g, device="cuda") * 1e-2)
-    return x, dy
+    if c["kind"] == "first":
+        x = torch.randint(0, c["vocab"], (M, T), generator=g, device="cuda", dtype=torch.int32)
+    else:
+        x = torch.empty(M, T, d, dtype=dt, device="cuda")
+        for i in range(M):
+            x[i].copy_(torch.randn(T, d, generator=g, device="cuda"))
+    dy = tgt = None
+    if c["kind"] == "last":
+        tgt = torch.randint(0, c["vocab"], (M, T), generator=g, device="cuda", dtype=torch.int32)
+    else:
+        dy = torch.empty(M, T, d, dtype=dt, device="cuda")
+        for i in range(M):
+            dy[i].copy_(torch.randn(T, d, generator=g, device="cuda") * 1e-2)
+    return x, dy, tgt
 
 
 def cpu_baseline(c, seed=0, budget_s=20.0):
@@ -63,13 +76,14 @@ def cpu_baseline(c, seed=0, budget_s=20.0):
     one = dict(c)
     one["micro_batch"] = 1
     params = {k: v.astype(np.float64) for k, v in inputs.make_params(c, seed).items()}
-    x, _ = inputs.make_x(one, seed, 0)
-    dy, _ = inputs.make_dy(one, seed, 0)
-    x, dy = x.astype(np.float64), dy.astype(np.float64)
+    kind = c["kind"]
+    x = inputs.make_ids(one, seed, 0) if kind == "first" else inputs.make_x(one, seed, 0)[0].astype(np.float64)
+    dy = None if kind == "last" else inputs.make_dy(one, seed, 0)[0].astype(np.float64)
+    tgt = inputs.make_targets(one, seed, 0) if kind == "last" else None
     n, t0 = 0, time.perf_counter()
     while True:
-        _, saved = ostage.stage_fwd(one, params, x)
-        ostage.stage_bwd(one, params, saved, dy, c["K"])
+        _, saved = ostage.stage_fwd(one, params, x, tgt)
+        ostage.stage_bwd(one, params, saved, dy, c["K"], ids=x if kind == "first" else None)
         n += 1
         el = time.perf_counter() - t0
         if el >= budget_s or n >= 8:
@@ -93,6 +107,8 @@ def main():
     ap.add_argument("--recompute", action="store_true",
                     help="the activation-checkpointed stage: keep only stage inputs, recompute the forward "
                          "in each backward under the current parameters")
+    ap.add_argument("--fused-head", action="store_true",
+                    help="last stage: the fused LM head (no [T, V] logits kept; the backward recomputes them)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy a 256 MiB device buffer 3 times (a kernel of known traffic, for scaling "
                          "hardware byte counters)")
@@ -107,16 +123,20 @@ def main():
     from paper_2606_07881_amd import binding, configs, inputs
 
     name = args.config or configs.BENCH_CONFIG
-    c = configs.get(name, **({"recompute": 1} if args.recompute else {}))
+    over = {}
     if args.recompute:
-        name = c["name"]
+        over["recompute"] = 1
+    if args.fused_head:
+        over["fused_head"] = 1
+    c = configs.get(name, **over)
+    name = c["name"]
     M, K, delay = c["M"], c["K"], c["delay"]
     T = c["micro_batch"] * c["seq"]
     log(f"bench: {name} M={M} K={K} delay={delay} T={T}")
     torch.cuda.set_device(0)
     st = binding.Stage(c)
     st.load_params(inputs.make_params(c, args.seed))
-    x_all, dy_all = make_device_inputs(torch, c, M, args.seed)
+    x_all, dy_all, tgt_all = make_device_inputs(torch, c, M, args.seed)
     torch.cuda.synchronize()
     log("bench: inputs resident")
     if args.copy_probe:
@@ -130,7 +150,7 @@ def main():
 
     def replay():
         st.reset_counters()
-        stamps = st.run(M, x_all, dy_all)
+        stamps = st.run(M, x_all, dy_all, targets_all=tgt_all)
         return stamps
 
     for w in range(args.warmup):
@@ -227,12 +247,16 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if c["dtype"] == "bf16" else "f32",
         "data": "synthetic (seeded N(0,1) stage inputs, N(0,0.01^2) output gradients, N(0,0.02^2) weights)",
-        "config": {"workload": f"{name}: GPT-2-medium-shaped middle pipeline stage, {c['n_layers']} pre-LN blocks, "
+        "config": {"workload": f"{name}: {WORKLOAD_SHAPE.get(name.split('+')[0], 'GPT-style')} {c['kind']} "
+                               f"pipeline stage, {c['n_layers']} pre-LN blocks, "
                                f"d {c['d_model']}, {c['n_heads']}x{c['head_dim']} heads, FFN {c['d_ff']}, "
                                f"seq {c['seq']}, micro-batch {c['micro_batch']}; one step = async 1F1B replay of "
                                f"{M} micro-batches, delay {delay}, AdamW every K={K}"
                                + ("; activation-checkpointed (forward recomputed in each backward)"
-                                  if c.get("recompute") else ""),
+                                  if c.get("recompute") else "")
+                               + (f"; LM head over V={c['vocab']} with softmax cross-entropy"
+                                  + (", fused (no logits kept)" if c.get("fused_head") else ", fp32 logits kept")
+                                  if c["kind"] == "last" else ""),
                    "micro_batches_per_step": M, "tokens_per_step": tokens_per_step, "K": K, "delay": delay,
                    "parallelism": "single stage, 1 GPU"},
         "mfma_util": round(mfma_util, 4),

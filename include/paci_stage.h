@@ -78,6 +78,11 @@ typedef struct paci_shapes {
                            from lr down to lr * lr_min_ratio at update lr_total, flat after it */
   int32_t lr_total;     /* 0: no schedule, every update uses lr */
   float lr_min_ratio;
+  int32_t fused_head;   /* PACI_LAST, bf16, d % 8 == 0, delay 0 only. 1: no [T, V] logits are stored;
+                           the LM-head forward product reduces each row to its log-sum-exp and target
+                           logit as it goes, and the backward recomputes the product (same parameters,
+                           since a delay-0 stage's backward follows its forward before any update) and
+                           turns it into dL/dz inside the same kernel. 0: fp32 logits per slot */
 } paci_shapes;
 
 typedef struct paci_counters {

@@ -35,7 +35,7 @@ class PaciShapes(ctypes.Structure):
                                               "micro_batch", "vocab", "max_pos", "kind", "dtype")] + \
                [(n, ctypes.c_float) for n in ("lr", "beta1", "beta2", "eps", "weight_decay", "ln_eps")] + \
                [("recompute", ctypes.c_int32), ("lr_warmup", ctypes.c_int32), ("lr_total", ctypes.c_int32),
-                ("lr_min_ratio", ctypes.c_float)]
+                ("lr_min_ratio", ctypes.c_float), ("fused_head", ctypes.c_int32)]
 
 
 class PaciCounters(ctypes.Structure):
@@ -140,6 +140,7 @@ def shapes(cfg):
     s.lr_warmup = int(cfg.get("lr_warmup", 0))
     s.lr_total = int(cfg.get("lr_total", 0))
     s.lr_min_ratio = float(cfg.get("lr_min_ratio", 0.1))
+    s.fused_head = int(bool(cfg.get("fused_head", False)))
     return s
 
 

@@ -449,6 +449,11 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
         for (int j = 0; j < U; ++j)
           if (j < nv) o[j] += C[off + j];
       }
+    } else if constexpr (EPI == EPI_CE_GRAD) {
+      const float l = a.row_lse[m];
+      const int y = a.row_tgt[m] - n;
+#pragma unroll
+      for (int j = 0; j < U; ++j) o[j] = a.alpha * (expf(o[j] - l) - (j == y ? 1.f : 0.f));
     } else {
 #pragma unroll
       for (int j = 0; j < U; ++j) {
@@ -497,6 +502,33 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
   }
 }
 
+// Cross-entropy row statistics of a staged panel (EPI_CE_STATS): per row and
+// 64-column group, the maximum and the sum of exp(x - max) over the valid
+// columns, and the target's logit when the group holds it. Consecutive lanes
+// take consecutive rows; a full group is read starting at column r mod 64, so
+// the 64 lanes of a wavefront hit 64 distinct banks (row stride BN + 4).
+template <int BN, int PR, int NT>
+__device__ __forceinline__ void ce_stats_panel(const GemmArgs& a, const float* cl, int mb, int n0, int tid) {
+  constexpr int LDC = BN + 4, G = BN / 64;
+  static_assert(BN % 64 == 0, "64-column groups must tile the block");
+  for (int idx = tid; idx < PR * G; idx += NT) {
+    const int r = idx % PR, g = idx / PR;
+    const int m = mb + r, nb = n0 + 64 * g;
+    if (m >= a.M || nb >= a.N) continue;
+    const int nv = min(64, a.N - nb);
+    const float* row = cl + r * LDC + 64 * g;
+    const int rot = nv == 64 ? r : 0;
+    float mx = -INFINITY;
+    for (int c = 0; c < nv; ++c) mx = fmaxf(mx, row[(c + rot) & 63]);
+    float sum = 0.f;
+    for (int c = 0; c < nv; ++c) sum += expf(row[(c + rot) & 63] - mx);
+    const int64_t q = (int64_t)m * a.ld_part + nb / 64;
+    *reinterpret_cast<float2*>(a.ce_part + 2 * q) = make_float2(mx, sum);
+    const int y = a.row_tgt[m] - nb;
+    if (y >= 0 && y < nv) a.ce_zt[m] = row[y];
+  }
+}
+
 // Epilogue through LDS. The accumulator tile goes to LDS as fp32 (row stride
 // BN + 4 floats, so the 16 rows a wave writes at once fall in distinct banks)
 // and is read back with consecutive lanes on consecutive columns: a wave then
@@ -525,7 +557,9 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, float* cl, in
     }
     __syncthreads();
     const int mb = m0 + p * PR;
-    if constexpr (EPI == EPI_ATOMIC) {
+    if constexpr (EPI == EPI_CE_STATS) {
+      ce_stats_panel<BN, PR, NT>(a, cl, mb, n0, tid);
+    } else if constexpr (EPI == EPI_ATOMIC) {
       float* C = reinterpret_cast<float*>(a.C);
       for (int idx = tid; idx < PR * BN; idx += NT) {
         const int r = idx / BN, c = idx % BN;
@@ -536,7 +570,7 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, float* cl, in
       staged_out<TO, EPI, BN, PR, NT>(a, cl, mb, n0, tid, csum);
     }
   }
-  if constexpr (EPI != EPI_ATOMIC && UPR <= 64 && 64 % UPR == 0) {
+  if constexpr (EPI != EPI_ATOMIC && EPI != EPI_CE_STATS && UPR <= 64 && 64 % UPR == 0) {
     if (a.colsum != nullptr) {   // uniform: column sums of the tile's output into a.colsum
       // threads with equal tid % UPR hold the same columns: lanes l, l ^ UPR, ... within a
       // wavefront, then the wavefronts through LDS, then one atomic per column
@@ -839,6 +873,20 @@ hipError_t by_layout(bool out_f32, GemmLayout lay, GemmEpi epi, const GemmArgs& 
     return hipErrorInvalidValue;
   }
   if (splits != 1) return hipErrorInvalidValue;
+  if (epi == EPI_CE_STATS || epi == EPI_CE_GRAD) {
+    // pipelined bf16 kernel only; the statistics need 64-column groups
+    if constexpr (sizeof(T) == 2) {
+      if (lay != GEMM_NT || !pipe_eligible<true, true>(a) || a.row_tgt == nullptr || a.colsum != nullptr)
+        return hipErrorInvalidValue;
+      if (epi == EPI_CE_STATS) {
+        if (a.ce_part == nullptr || a.ce_zt == nullptr || a.ld_part < (a.N + 63) / 64) return hipErrorInvalidValue;
+        return launch_pipe<float, true, true, EPI_CE_STATS, P256x128>(a, 1, st);
+      }
+      if (a.row_lse == nullptr || out_f32) return hipErrorInvalidValue;
+      return launch_pipe<T, true, true, EPI_CE_GRAD, P256x128>(a, 1, st);
+    }
+    return hipErrorInvalidValue;
+  }
   if (lay == GEMM_NT) {
     if (out_f32) {
       if (epi != EPI_STORE) return hipErrorInvalidValue;

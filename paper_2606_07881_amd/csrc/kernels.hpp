@@ -22,7 +22,13 @@ enum GemmLayout { GEMM_NT = 0, GEMM_NN = 1, GEMM_TN = 2 };
 //   EPI_GELU_GRAD  C = acc * gelu'(aux[m*ld_aux + n])            (FFN down-projection dgrad)
 //   EPI_ACC        Cf32 += acc  (plain read-modify-write; one split only)
 //   EPI_ATOMIC     Cf32 += acc  (atomic add; any number of splits)
-enum GemmEpi { EPI_STORE = 0, EPI_BIAS, EPI_BIAS_RES, EPI_BIAS_GELU, EPI_GELU_GRAD, EPI_ACC, EPI_ATOMIC };
+// Softmax cross-entropy over the output columns (bf16 GEMM_NT only, one split):
+//   EPI_CE_STATS   nothing stored in C; per row m and 64-column group g (columns
+//                  64g .. 64g+63 below N): ce_part[2 (m ld_part + g) + {0, 1}] =
+//                  {max, sum exp(acc - max)}; ce_zt[m] = acc at column row_tgt[m]
+//   EPI_CE_GRAD    C = alpha * (exp(acc - row_lse[m]) - [n == row_tgt[m]])  (bf16)
+enum GemmEpi { EPI_STORE = 0, EPI_BIAS, EPI_BIAS_RES, EPI_BIAS_GELU, EPI_GELU_GRAD, EPI_ACC, EPI_ATOMIC, EPI_CE_STATS,
+               EPI_CE_GRAD };
 
 struct GemmArgs {
   const void* A; int64_t lda;
@@ -39,6 +45,13 @@ struct GemmArgs {
   // times ((seg_first + s) % seg_count), each with row stride ldb
   int64_t seg_rows = 0, seg_stride = 0;
   int seg_first = 0, seg_count = 1;
+  // cross-entropy epilogues (see GemmEpi)
+  const int32_t* row_tgt = nullptr;
+  const float* row_lse = nullptr;
+  float* ce_part = nullptr;
+  int64_t ld_part = 0;
+  float* ce_zt = nullptr;
+  float alpha = 1.f;
 };
 // bf16 operands: K-major vectors that straddle K read the memory just past K,
 // which must hold zeros (true when K % 8 == 0, or for zero-padded rows).
@@ -93,6 +106,12 @@ hipError_t embed_bwd(DType dt, const int32_t* ids, const void* dx, float* Gwte, 
 hipError_t ce_fwd(const float* z, int64_t ldz, const int32_t* tgt, float* lse, float* loss_out, float* part, int T,
                   int V, hipStream_t st);
 int64_t ce_part_floats(int T);
+// From the EPI_CE_STATS partials of a [T, V] logit product (ngroups = ceil(V / 64)
+// groups of 64 columns per row, row stride ld_part float2): lse[t] and the mean
+// loss over t of lse[t] - zt[t] into loss_out (a target outside [0, V) gives NaN).
+// `part_loss` needs ce_part_floats(T) floats.
+hipError_t ce_combine(const float* ce_part, int64_t ld_part, int ngroups, const float* zt, const int32_t* tgt, int V,
+                      float* lse, float* loss_out, float* part_loss, int T, hipStream_t st);
 // dz[t, v] = scale * (exp(z[t, v] - lse[t]) - [v == tgt[t]]) in the stage dtype; columns
 // V .. ldz-1 are written as zero.
 hipError_t ce_bwd(DType dt, const float* z, int64_t ldz, const int32_t* tgt, const float* lse, void* dz, int T, int V,

@@ -392,6 +392,33 @@ __global__ void __launch_bounds__(NT) mean_kernel(const float* __restrict__ x, i
   if (threadIdx.x == 0) *out = s / n;
 }
 
+// One wavefront per token: lse from the (max, sum) partials of its 64-column
+// groups, and its loss lse - z[target].
+__global__ void __launch_bounds__(NT) ce_combine_kernel(const float2* __restrict__ part, int64_t ld_part,
+                                                         int ngroups, const float* __restrict__ zt,
+                                                         const int32_t* __restrict__ tgt, int V, float* lse,
+                                                         float* loss_row, int T) {
+  const int64_t t = (int64_t)blockIdx.x * (NT / 64) + (threadIdx.x >> 6);
+  const int l = threadIdx.x & 63;
+  if (t >= T) return;
+  const float2* pr = part + t * ld_part;
+  float mx = -INFINITY;
+  for (int g = l; g < ngroups; g += 64) mx = fmaxf(mx, pr[g].x);
+  mx = wave_max(mx);
+  float s = 0.f;
+  for (int g = l; g < ngroups; g += 64) {
+    const float2 p = pr[g];
+    s += p.y * expf(p.x - mx);
+  }
+  s = wave_sum(s);
+  if (l == 0) {
+    const float lt = mx + logf(s);
+    const int y = tgt[t];
+    lse[t] = lt;
+    loss_row[t] = (y >= 0 && y < V) ? lt - zt[t] : NAN;
+  }
+}
+
 template <typename T>
 __global__ void __launch_bounds__(NT) ce_bwd_kernel(const float* __restrict__ z, int64_t ldz,
                                                      const int32_t* __restrict__ tgt, const float* __restrict__ lse,
@@ -452,6 +479,18 @@ hipError_t ce_fwd(const float* z, int64_t ldz, const int32_t* tgt, float* lse, f
 }
 
 int64_t ce_part_floats(int T) { return T; }
+
+hipError_t ce_combine(const float* ce_part, int64_t ld_part, int ngroups, const float* zt, const int32_t* tgt, int V,
+                      float* lse, float* loss_out, float* part_loss, int T, hipStream_t st) {
+  if (T <= 0 || ngroups <= 0 || ld_part < ngroups || ngroups != (V + 63) / 64) return hipErrorInvalidValue;
+  constexpr int RPB = NT / 64;
+  hipLaunchKernelGGL(ce_combine_kernel, dim3((T + RPB - 1) / RPB), dim3(NT), 0, st,
+                     reinterpret_cast<const float2*>(ce_part), ld_part, ngroups, zt, tgt, V, lse, part_loss, T);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(NT), 0, st, part_loss, T, loss_out);
+  return hipGetLastError();
+}
 
 hipError_t ce_bwd(DType dt, const float* z, int64_t ldz, const int32_t* tgt, const float* lse, void* dz, int T, int V,
                   float scale, hipStream_t st) {

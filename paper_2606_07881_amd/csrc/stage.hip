@@ -207,6 +207,11 @@ int validate_shapes(const paci_shapes* s, int K, int delay) {
   if (s->kind != PACI_MIDDLE && s->kind != PACI_FIRST && s->kind != PACI_LAST) return PACI_E_UNSUPPORTED;
   if (s->dtype != PACI_FP32 && s->dtype != PACI_BF16) return PACI_E_UNSUPPORTED;
   if (s->recompute != 0 && s->recompute != 1) return PACI_E_INVAL;
+  if (s->fused_head != 0 && s->fused_head != 1) return PACI_E_INVAL;
+  if (s->fused_head) {
+    if (s->kind != PACI_LAST || s->dtype != PACI_BF16 || s->d_model % 8) return PACI_E_UNSUPPORTED;
+    if (delay != 0) return PACI_E_INVAL;   // the recomputed logits must see the forward's parameters
+  }
   if (s->lr_warmup < 0 || s->lr_total < 0 || (s->lr_total > 0 && s->lr_warmup > s->lr_total) ||
       !(s->lr_min_ratio >= 0.f && s->lr_min_ratio <= 1.f))
     return PACI_E_INVAL;
@@ -287,6 +292,10 @@ struct Layout {
   struct WinBlock { size_t dqkv, dx1, du, dy; };   // per block: [K * T, width] each
   std::vector<WinBlock> win;
   size_t s_ids = 0, s_tgt = 0, s_y = 0, s_meanf = 0, s_rstdf = 0, s_nf = 0, s_z = 0, s_lse_ce = 0;
+  // fused LM head: no logits per slot; (max, sum) per row and 64 columns, target logits
+  bool fused_head = false;
+  int ngroups = 0;
+  size_t w_cepart = 0, w_zt = 0;
   // workspace
   size_t w_dyA, w_dyB, w_du, w_dn, w_dx1, w_do, w_dqkv, w_D, w_part, w_dz = 0, w_dnf = 0, w_loss = 0;
   size_t total;
@@ -349,7 +358,8 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
     L.s_meanf = sl.take(4 * T);
     L.s_rstdf = sl.take(4 * T);
     L.s_nf = sl.take(esz * T * d);
-    L.s_z = sl.take(4 * T * L.ldz);
+    L.fused_head = s.fused_head != 0;
+    if (!L.fused_head) L.s_z = sl.take(4 * T * L.ldz);
     L.s_lse_ce = sl.take(4 * T);
   }
   L.slot_bytes = (sl.off + 255) & ~(size_t)255;
@@ -393,6 +403,11 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
     part = std::max(part, paci::ce_part_floats((int)T));
     L.w_dz = a.take(esz * T * L.ldz);
     L.w_dnf = a.take(esz * T * d);
+    if (L.fused_head) {
+      L.ngroups = (int)(L.ldz / 64);
+      L.w_cepart = a.take(8 * T * (int64_t)L.ngroups);
+      L.w_zt = a.take(4 * T);
+    }
   }
   L.w_part = a.take(4 * part);
   L.w_loss = a.take(256);
@@ -744,8 +759,24 @@ int stage_forward_into(paci_stage* h, char* A, const void* in, void* x0_copy, co
   TRY(blocks_fwd(h, A, in, x0_copy, A + L.s_y));
   float* meanf = reinterpret_cast<float*>(A + L.s_meanf);
   float* rstdf = reinterpret_cast<float*>(A + L.s_rstdf);
-  float* z = reinterpret_cast<float*>(A + L.s_z);
   TRY(ln_fwd(h, A + L.s_y, A + L.s_nf, meanf, rstdf, h->p.lnf_g, h->p.lnf_b, nullptr));
+  if (L.fused_head) {
+    // logits reduced to (max, sum) per 64 columns inside the product, then per row
+    paci::GemmArgs a{A + L.s_nf, d, h->W(h->p.w_lm), d, T, s.vocab, d, nullptr, 0, nullptr, nullptr, 0, nullptr,
+                     h->arena + L.zeros};
+    a.row_tgt = tgt;
+    a.ce_part = reinterpret_cast<float*>(h->ws(L.w_cepart));
+    a.ld_part = L.ngroups;
+    a.ce_zt = reinterpret_cast<float*>(h->ws(L.w_zt));
+    TRY(run(h, F_GEMM_FWD, 2.0 * T * s.vocab * d,
+            [&] { return paci::gemm(h->dt, true, paci::GEMM_NT, paci::EPI_CE_STATS, a, 1, h->st); }));
+    return run(h, F_CE, 8.0 * T * L.ngroups + 16.0 * T, [&] {
+      return paci::ce_combine(a.ce_part, L.ngroups, L.ngroups, a.ce_zt, tgt, s.vocab,
+                              reinterpret_cast<float*>(A + L.s_lse_ce), reinterpret_cast<float*>(out),
+                              reinterpret_cast<float*>(h->ws(L.w_part)), T, h->st);
+    });
+  }
+  float* z = reinterpret_cast<float*>(A + L.s_z);
   paci::GemmArgs a{A + L.s_nf, d, h->W(h->p.w_lm), d, T, s.vocab, d, z, L.ldz, nullptr, nullptr, 0, nullptr,
                    h->arena + L.zeros};
   TRY(run(h, F_GEMM_FWD, 2.0 * T * s.vocab * d,
@@ -831,6 +862,8 @@ extern "C" int paci_stage_init(const paci_shapes* s, int K, int delay, void* dev
       chunks.push_back(0);
     }
   hipError_t e = hipMemsetAsync(h->arena, 0, h->L.stash, h->st);  // theta, G, m, v, bf16 copy
+  if (e == hipSuccess && h->L.fused_head)   // dz columns V .. ldz-1 stay zero (the dgrad reads them)
+    e = hipMemsetAsync(h->arena + h->L.w_dz, 0, (size_t)h->esz * h->L.T * h->L.ldz, h->st);
   if (e == hipSuccess)
     e = hipMemcpyAsync(h->arena + h->L.chunks, chunks.data(), chunks.size() * sizeof(int32_t),
                        hipMemcpyHostToDevice, h->st);
@@ -968,14 +1001,25 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
                              : stage_forward_into(h, A, sl + L.c_x, A + L.blk[0].x, nullptr, tgt, out);
   }
   if (!r && s.kind == PACI_LAST) {
-    const float* z = reinterpret_cast<const float*>(A + L.s_z);
     char* dz = h->ws(L.w_dz);
     char* dnf = h->ws(L.w_dnf);
     const float scale = 1.0f / ((float)T * (float)h->fsm.K);
-    r = run(h, F_CE, (double)T * L.ldz * (4 + h->esz), [&] {
-      return paci::ce_bwd(h->dt, z, L.ldz, tgt, reinterpret_cast<const float*>(A + L.s_lse_ce), dz, T, s.vocab,
-                          scale, h->st);
-    });
+    if (L.fused_head) {
+      // the logits again (the parameters are those of the forward), into dL/dz
+      paci::GemmArgs a{A + L.s_nf, d, h->W(h->p.w_lm), d, T, s.vocab, d, dz, L.ldz, nullptr, nullptr, 0, nullptr,
+                       h->arena + L.zeros};
+      a.row_tgt = tgt;
+      a.row_lse = reinterpret_cast<const float*>(A + L.s_lse_ce);
+      a.alpha = scale;
+      r = run(h, F_GEMM_FWD, 2.0 * T * s.vocab * d,
+              [&] { return paci::gemm(h->dt, false, paci::GEMM_NT, paci::EPI_CE_GRAD, a, 1, h->st); });
+    } else {
+      const float* z = reinterpret_cast<const float*>(A + L.s_z);
+      r = run(h, F_CE, (double)T * L.ldz * (4 + h->esz), [&] {
+        return paci::ce_bwd(h->dt, z, L.ldz, tgt, reinterpret_cast<const float*>(A + L.s_lse_ce), dz, T, s.vocab,
+                            scale, h->st);
+      });
+    }
     if (!r) r = linear_wgrad(h, dz, L.ldz, A + L.s_nf, d, s.vocab, d, T, h->p.w_lm);
     if (!r) r = linear_dgrad(h, dz, L.ldz, h->p.w_lm, T, d, s.vocab, paci::EPI_STORE, dnf, nullptr, -1, false);
     if (!r)   // the last block's output gradient; G_b2 of that block += its column sums

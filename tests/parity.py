@@ -75,11 +75,16 @@ def rel_err(x, r):
 def small_cfg(name, **kw):
     """Parity workloads small enough for the oracle (seconds), spanning several
     tiles with ragged tails. ``ckpt_<name>``: workload <name> on an
-    activation-checkpointed stage."""
+    activation-checkpointed stage; ``fused_<name>``: a last stage whose LM head
+    keeps no logits (the oracle is the same function)."""
     if name.startswith("ckpt_"):
         base = name[len("ckpt_"):]
         c = configs.get(base) if base == "tiny_fp32" else small_cfg(base)
         c.update(recompute=1, **kw)
+        return c
+    if name.startswith("fused_"):
+        c = small_cfg(name[len("fused_"):])
+        c.update(fused_head=1, **kw)
         return c
     base = {
         # ragged in tokens (T = 400), model width (192 = 1.5 GEMM tiles) and keys (S = 200)

@@ -192,3 +192,29 @@ def test_flush_schedule_matches_oracle(M, K, delay):
         assert binding.lib.paci_schedule_flush(M, K, delay, p, p, 1, ctypes.byref(n)) == binding.E_INVAL
         assert n.value == len(ev)
     assert binding.lib.paci_schedule_flush(M, 0, delay, p, p, 1, ctypes.byref(n)) == binding.E_INVAL
+
+
+def test_fused_head_validation_and_memory():
+    """The fused LM head keeps no [T, V] logits: the GPT-2-medium-shaped last
+    stage's arena shrinks by the fp32 logits of every slot; it is refused off
+    a bf16 last stage and for a stage with delay > 0."""
+    out = ctypes.c_size_t(0)
+    c = configs.get("gpt2m_last_bf16")
+    s = binding.shapes(c)
+    assert binding.lib.paci_stage_arena_bytes(ctypes.byref(s), c["K"], c["delay"], ctypes.byref(out)) == 0
+    plain = out.value
+    s = binding.shapes(dict(c, fused_head=1))
+    assert binding.lib.paci_stage_arena_bytes(ctypes.byref(s), c["K"], c["delay"], ctypes.byref(out)) == 0
+    fused = out.value
+    T, ldz = c["micro_batch"] * c["seq"], (c["vocab"] + 63) // 64 * 64
+    slots = c["K"] + c["delay"]        # windowed weight gradients at these shapes
+    partials = 8 * T * (ldz // 64) + 4 * T
+    assert plain - fused >= slots * 4 * T * ldz - partials - 4096
+    assert plain - fused <= slots * 4 * T * ldz
+    for over, code in [(dict(kind="middle"), binding.E_UNSUPPORTED), (dict(dtype="fp32"), binding.E_UNSUPPORTED),
+                       (dict(fused_head=2), binding.E_INVAL)]:
+        s = binding.shapes(dict(dict(c, fused_head=1), **over))
+        s.fused_head = over.get("fused_head", 1)
+        assert binding.lib.paci_stage_arena_bytes(ctypes.byref(s), 8, 0, ctypes.byref(out)) == code
+    s = binding.shapes(dict(c, fused_head=1))
+    assert binding.lib.paci_stage_arena_bytes(ctypes.byref(s), 8, 1, ctypes.byref(out)) == binding.E_INVAL

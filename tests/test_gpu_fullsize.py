@@ -33,7 +33,8 @@ from paper_2606_07881_amd import configs, inputs
 pytestmark = pytest.mark.gpu
 
 FULL = ["gpt2s_mid_bf16", "gpt2m_mid_bf16", "gpt2m_first_bf16", "gpt2m_last_bf16", "gpt1p3b_pos0_bf16",
-        "gpt2m_mid_bf16+ckpt"]   # +ckpt: the same workload on an activation-checkpointed stage
+        "gpt2m_mid_bf16+ckpt",   # +ckpt: the same workload on an activation-checkpointed stage
+        "gpt2m_last_bf16+fused"]  # +fused: the last stage with the fused LM head (no logits kept)
 PREFIX = 256   # tokens of a sequence whose forward is checked where the whole one is not needed
 
 
@@ -81,7 +82,8 @@ def oracle_grad_in(c, theta_f, theta_b, x_seq, dy_seq, tgt_seq):
 @pytest.mark.parametrize("name", FULL)
 def test_fullsize_sampled(binding, name):
     import torch
-    c = configs.get(name.split("+")[0], **({"recompute": 1} if name.endswith("+ckpt") else {}))
+    extra = {"+ckpt": {"recompute": 1}, "+fused": {"fused_head": 1}}
+    c = configs.get(name.split("+")[0], **next((v for k, v in extra.items() if name.endswith(k)), {}))
     K, delay, seed = c["K"], c["delay"], 0
     T, d, mu = c["micro_batch"] * c["seq"], c["d_model"], c["micro_batch"]
     kind = c["kind"]

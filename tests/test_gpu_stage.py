@@ -24,7 +24,7 @@ def _one_event_pair(binding, c, seed=0):
     """F_0 then B_0 at version 0; returns GPU and oracle (out, grad_in, G)."""
     import torch
     inp = Inputs(c, seed, 1)
-    st = binding.Stage(c, K=2, delay=1)
+    st = binding.Stage(c, K=2, delay=0 if c.get("fused_head") else 1)   # a fused head needs delay 0
     st.load_params(inp.params)
     T, d = c["micro_batch"] * c["seq"], c["d_model"]
     x = to_torch(inp.x_dev[0])
@@ -49,7 +49,8 @@ def _one_event_pair(binding, c, seed=0):
 
 
 @pytest.mark.parametrize("name", ["tiny_fp32", "ragged_bf16", "ragged_fp32", "win_bf16", "dh128_bf16", "dh32_bf16",
-                                  "dh64_fp32", "first_bf16", "last_bf16", "first_fp32", "last_fp32"])
+                                  "dh64_fp32", "first_bf16", "last_bf16", "first_fp32", "last_fp32",
+                                  "fused_last_bf16"])
 def test_first_forward_backward(binding, name):
     c = configs.get("tiny_fp32") if name == "tiny_fp32" else small_cfg(name)
     (g_out, g_in, G), (o_out, o_in, o_G) = _one_event_pair(binding, c)
@@ -69,7 +70,7 @@ def test_first_forward_backward(binding, name):
 @pytest.mark.parametrize("name", ["tiny_fp32", "ragged_bf16", "ragged_fp32", "win_bf16", "win8_bf16", "dh128_bf16",
                                   "dh32_bf16", "first_bf16", "last_bf16", "first_fp32", "last_fp32",
                                   "ckpt_tiny_fp32", "ckpt_ragged_bf16", "ckpt_win_bf16", "ckpt_first_bf16",
-                                  "ckpt_last_bf16", "sched_bf16"])
+                                  "ckpt_last_bf16", "sched_bf16", "fused_last_bf16", "ckpt_fused_last_bf16"])
 def test_replay_parity(binding, name):
     """The whole asynchronous 1F1B replay: stamps bit-exact, every output, input
     gradient, accumulated G and the state after every AdamW update."""
