@@ -99,11 +99,12 @@ def _merge(o):
     return o.transpose(0, 2, 1, 3).reshape(mu * S, H * dh)
 
 
-def attention_fwd(qkv, mu, S, n_heads, head_dim):
+def attention_fwd(qkv, mu, S, n_heads, head_dim, keep=None, drop_scale=1.0):
     """o = softmax(q k^T / sqrt(dh) + causal mask) v for every sequence and head.
 
-    Returns o as [T, d] and the per-row log-sum-exp of the scaled scores,
-    lse [mu, H, S].
+    With ``keep`` [mu, H, S, S] (dropout on the probabilities) the product
+    uses P * keep * drop_scale. Returns o as [T, d] and the per-row
+    log-sum-exp of the scaled scores, lse [mu, H, S] (of the undropped ones).
     """
     q, k, v = _heads(qkv, mu, S, n_heads, head_dim)
     scale = 1.0 / math.sqrt(head_dim)
@@ -117,17 +118,21 @@ def attention_fwd(qkv, mu, S, n_heads, head_dim):
             smax = s.max(axis=1, keepdims=True)
             e = np.exp(s - smax)
             rowsum = e.sum(axis=1, keepdims=True)
-            o[b, h] = (e / rowsum) @ v[b, h]
+            P = e / rowsum
+            if keep is not None:
+                P = P * keep[b, h] * drop_scale
+            o[b, h] = P @ v[b, h]
             lse[b, h] = (smax + np.log(rowsum))[:, 0]
     return _merge(o), lse
 
 
-def attention_bwd(do_, qkv, lse, mu, S, n_heads, head_dim):
+def attention_bwd(do_, qkv, lse, mu, S, n_heads, head_dim, keep=None, drop_scale=1.0):
     """Backward of attention_fwd; returns d(qkv) as [T, 3d].
 
     P is rebuilt from q, k and the saved log-sum-exp (it holds no parameter).
     With dP = dO V^T: dV = P^T dO, dS = P * (dP - rowsum(dP * P)),
-    dQ = dS K / sqrt(dh), dK = dS^T Q / sqrt(dh).
+    dQ = dS K / sqrt(dh), dK = dS^T Q / sqrt(dh). With dropout (``keep``),
+    M = keep * drop_scale: dV = (P M)^T dO and dP = (dO V^T) M.
     """
     q, k, v = _heads(qkv, mu, S, n_heads, head_dim)
     d = n_heads * head_dim
@@ -140,8 +145,9 @@ def attention_bwd(do_, qkv, lse, mu, S, n_heads, head_dim):
             s = (q[b, h] @ k[b, h].T) * scale
             s[future] = -np.inf
             P = np.exp(s - lse[b, h][:, None])
-            dv[b, h] = P.T @ dO[b, h]
-            dP = dO[b, h] @ v[b, h].T
+            Mk = 1.0 if keep is None else keep[b, h] * drop_scale
+            dv[b, h] = (P * Mk).T @ dO[b, h]
+            dP = (dO[b, h] @ v[b, h].T) * Mk
             dS = P * (dP - (dP * P).sum(axis=1, keepdims=True))
             dq[b, h] = (dS @ k[b, h]) * scale
             dk[b, h] = (dS.T @ q[b, h]) * scale
@@ -155,24 +161,31 @@ def attention_bwd(do_, qkv, lse, mu, S, n_heads, head_dim):
 # ----------------------------------------------------------------------------
 # one pre-LN decoder block
 # ----------------------------------------------------------------------------
-def block_fwd(x, p, cfg):
+def block_fwd(x, p, cfg, drop=None):
     """y = x1 + W2 gelu(W1 LN2(x1) + b1) + b2,  x1 = x + Wo attn(Wqkv LN1(x) + bqkv) + bo.
 
     ``p`` maps the block's parameter names (ln1_g, ln1_b, w_qkv, b_qkv, w_o,
-    b_o, ln2_g, ln2_b, w_1, b_1, w_2, b_2) to arrays. Returns (y, saved), where
-    ``saved`` holds every activation the backward reads.
+    b_o, ln2_g, ln2_b, w_1, b_1, w_2, b_2) to arrays. ``drop`` (optional) holds
+    the dropout keep masks of this block and micro-batch, {"attn", "proj",
+    "ffn"}, and their scale: the attention probabilities and the two branch
+    outputs (before their residual adds) are multiplied by keep * scale.
+    Returns (y, saved), where ``saved`` holds every activation (and mask) the
+    backward reads.
     """
     mu, S, H, dh, eps = cfg["micro_batch"], cfg["seq"], cfg["n_heads"], cfg["head_dim"], cfg["ln_eps"]
+    sc = 1.0 if drop is None else drop["scale"]
     n1, mean1, rstd1 = layernorm_fwd(x, p["ln1_g"], p["ln1_b"], eps)
     qkv = n1 @ p["w_qkv"].T + p["b_qkv"]
-    o, lse = attention_fwd(qkv, mu, S, H, dh)
-    x1 = x + o @ p["w_o"].T + p["b_o"]
+    o, lse = attention_fwd(qkv, mu, S, H, dh, None if drop is None else drop["attn"], sc)
+    z1 = o @ p["w_o"].T + p["b_o"]
+    x1 = x + (z1 if drop is None else z1 * drop["proj"] * sc)
     n2, mean2, rstd2 = layernorm_fwd(x1, p["ln2_g"], p["ln2_b"], eps)
     u = n2 @ p["w_1"].T + p["b_1"]
     a = gelu(u)
-    y = x1 + a @ p["w_2"].T + p["b_2"]
+    z2 = a @ p["w_2"].T + p["b_2"]
+    y = x1 + (z2 if drop is None else z2 * drop["ffn"] * sc)
     saved = dict(x=x, mean1=mean1, rstd1=rstd1, n1=n1, qkv=qkv, o=o, lse=lse,
-                 x1=x1, mean2=mean2, rstd2=rstd2, n2=n2, u=u, a=a)
+                 x1=x1, mean2=mean2, rstd2=rstd2, n2=n2, u=u, a=a, drop=drop)
     return y, saved
 
 
@@ -185,22 +198,26 @@ def block_bwd(dy, s, p, cfg):
     from ``p``.
     """
     mu, S, H, dh = cfg["micro_batch"], cfg["seq"], cfg["n_heads"], cfg["head_dim"]
+    drop = s.get("drop")
     g = {}
-    # y = x1 + a W2^T + b2
-    g["w_2"] = dy.T @ s["a"]
-    g["b_2"] = dy.sum(axis=0)
-    du = (dy @ p["w_2"]) * gelu_grad(s["u"])
+    # y = x1 + drop(a W2^T + b2): the branch sees dy * keep * scale
+    g2 = dy if drop is None else dy * drop["ffn"] * drop["scale"]
+    g["w_2"] = g2.T @ s["a"]
+    g["b_2"] = g2.sum(axis=0)
+    du = (g2 @ p["w_2"]) * gelu_grad(s["u"])
     # u = n2 W1^T + b1
     g["w_1"] = du.T @ s["n2"]
     g["b_1"] = du.sum(axis=0)
     dn2 = du @ p["w_1"]
     dx1_ln, g["ln2_g"], g["ln2_b"] = layernorm_bwd(dn2, s["x1"], s["mean2"], s["rstd2"], p["ln2_g"])
     dx1 = dy + dx1_ln
-    # x1 = x + o Wo^T + bo
-    g["w_o"] = dx1.T @ s["o"]
-    g["b_o"] = dx1.sum(axis=0)
-    do_ = dx1 @ p["w_o"]
-    dqkv = attention_bwd(do_, s["qkv"], s["lse"], mu, S, H, dh)
+    # x1 = x + drop(o Wo^T + bo)
+    g1 = dx1 if drop is None else dx1 * drop["proj"] * drop["scale"]
+    g["w_o"] = g1.T @ s["o"]
+    g["b_o"] = g1.sum(axis=0)
+    do_ = g1 @ p["w_o"]
+    dqkv = attention_bwd(do_, s["qkv"], s["lse"], mu, S, H, dh, None if drop is None else drop["attn"],
+                         1.0 if drop is None else drop["scale"])
     # qkv = n1 Wqkv^T + bqkv
     g["w_qkv"] = dqkv.T @ s["n1"]
     g["b_qkv"] = dqkv.sum(axis=0)

@@ -31,7 +31,7 @@ parameters or embeddings, appendix "Detailed experimental setup").
 """
 import numpy as np
 
-from . import adamw, model
+from . import adamw, dropout, model
 from .schedule import StageCounters, canonical_events
 
 BLOCK_PARAMS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
@@ -58,20 +58,41 @@ def decayed(name):
     return name.split(".")[-1].startswith("w_")
 
 
-def stage_fwd(cfg, theta, inp, targets=None):
+def _drop_masks(cfg, mb, block):
+    """Keep masks of one block for micro-batch ``mb`` (None without dropout)."""
+    p = cfg.get("dropout", 0.0)
+    if not p:
+        return None
+    seed, mu, S, H, d = cfg.get("dropout_seed", 0), cfg["micro_batch"], cfg["seq"], cfg["n_heads"], cfg["d_model"]
+    T = mu * S
+    return dict(scale=dropout.scale(p),
+                attn=dropout.keep_attention(seed, mb, block, mu, H, S, p),
+                proj=dropout.keep_elementwise(seed, mb, block, dropout.SITE_PROJ, T, d, p),
+                ffn=dropout.keep_elementwise(seed, mb, block, dropout.SITE_FFN, T, d, p))
+
+
+def stage_fwd(cfg, theta, inp, targets=None, mb=0):
     """F_i at parameters ``theta``. Returns (output, saved).
 
     middle: inp is x [T, d], output y [T, d]; first: inp is ids [mu, S];
-    last: output is the mean cross-entropy of the micro-batch.
+    last: output is the mean cross-entropy of the micro-batch. With
+    cfg["dropout"] = p > 0 the masks of micro-batch ``mb`` are applied
+    (oracle/dropout.py); the embedding sum of a first stage is dropped too.
     """
+    saved = {"blocks": []}
     if cfg["kind"] == "first":
         x = model.embed_fwd(inp, theta["wte"], theta["wpe"])
+        if cfg.get("dropout", 0.0):
+            p = cfg["dropout"]
+            keep = dropout.keep_elementwise(cfg.get("dropout_seed", 0), mb, 0, dropout.SITE_EMBED, x.shape[0],
+                                            x.shape[1], p)
+            saved["embed_drop"] = keep * dropout.scale(p)
+            x = x * saved["embed_drop"]
     else:
         x = inp
-    saved = {"blocks": []}
     for l in range(cfg["n_layers"]):
         p = {n: theta[f"h{l}.{n}"] for n in BLOCK_PARAMS}
-        x, s = model.block_fwd(x, p, cfg)
+        x, s = model.block_fwd(x, p, cfg, _drop_masks(cfg, mb, l))
         saved["blocks"].append(s)
     if cfg["kind"] == "last":
         loss, saved["head"] = model.head_fwd(x, targets, theta["lnf_g"], theta["lnf_b"],
@@ -101,6 +122,8 @@ def stage_bwd(cfg, theta, saved, grad_out, K, ids=None):
         for n, v in gl.items():
             g[f"h{l}.{n}"] = v
     if cfg["kind"] == "first":
+        if "embed_drop" in saved:
+            dy = dy * saved["embed_drop"]
         g["wte"], g["wpe"] = model.embed_bwd(dy, ids, cfg["vocab"], cfg["max_pos"])
         return None, g
     return dy, g
@@ -128,7 +151,7 @@ class Stage:
     def forward(self, mb, inp, targets=None):
         """F_mb: returns (output, t^F). Stores the activations until B_mb."""
         version = self.counters.forward(mb)
-        out, saved = stage_fwd(self.cfg, self.theta, inp, targets)
+        out, saved = stage_fwd(self.cfg, self.theta, inp, targets, mb=mb)
         # checkpointed: keep the input only (the activations are dropped here)
         self.saved[mb] = (inp, targets) if self.recompute else saved
         if self.cfg["kind"] == "first":
@@ -139,8 +162,8 @@ class Stage:
         """B_mb at the current parameters: returns (grad_in, t^B, update_due)."""
         version = self.counters.backward(mb)
         saved = self.saved.pop(mb)
-        if self.recompute:   # the activations again, under the current version
-            _, saved = stage_fwd(self.cfg, self.theta, saved[0], saved[1])
+        if self.recompute:   # the activations again (same dropout masks), under the current version
+            _, saved = stage_fwd(self.cfg, self.theta, saved[0], saved[1], mb=mb)
         grad_in, g = stage_bwd(self.cfg, self.theta, saved, grad_out, self.K, ids=self.ids.pop(mb, None))
         for n, v in g.items():
             self.G[n] += v
@@ -241,10 +264,10 @@ def replay_with_version_store(cfg, params, K, delay, inputs, grad_outs=None, tar
         if kind == "F":
             tF[i] = t
             tgt = targets[i] if targets is not None else None
-            out[i], _ = stage_fwd(cfg, versions[t], inputs[i], tgt)
+            out[i], _ = stage_fwd(cfg, versions[t], inputs[i], tgt, mb=i)
         elif kind == "B":
             tgt = targets[i] if targets is not None else None
-            _, saved = stage_fwd(cfg, versions[tF[i]], inputs[i], tgt)
+            _, saved = stage_fwd(cfg, versions[tF[i]], inputs[i], tgt, mb=i)
             at = versions[t] if backward_at == "current" else versions[tF[i]]
             go = grad_outs[i] if grad_outs is not None else None
             ids = inputs[i] if cfg["kind"] == "first" else None
