@@ -83,6 +83,14 @@ typedef struct paci_shapes {
                            logit as it goes, and the backward recomputes the product (same parameters,
                            since a delay-0 stage's backward follows its forward before any update) and
                            turns it into dL/dz inside the same kernel. 0: fp32 logits per slot */
+  float dropout;        /* rate p in [0, 1) of inverted dropout at GPT-2's four places (appendix
+                           "Detailed experimental setup": 0.1): the embedding sum (first stage), the
+                           attention probabilities, and the attention-projection and FFN outputs
+                           before their residual adds; kept values are scaled by 1 / (1 - p). 0: off */
+  uint32_t dropout_seed; /* masks are a pure function of (dropout_seed, micro-batch index, block,
+                           site, element) through Philox4x32-10, so a backward (and a recomputed
+                           forward) uses its forward's masks; the element -> bits map is given with
+                           paci_stage_forward */
 } paci_shapes;
 
 typedef struct paci_counters {

@@ -35,7 +35,8 @@ class PaciShapes(ctypes.Structure):
                                               "micro_batch", "vocab", "max_pos", "kind", "dtype")] + \
                [(n, ctypes.c_float) for n in ("lr", "beta1", "beta2", "eps", "weight_decay", "ln_eps")] + \
                [("recompute", ctypes.c_int32), ("lr_warmup", ctypes.c_int32), ("lr_total", ctypes.c_int32),
-                ("lr_min_ratio", ctypes.c_float), ("fused_head", ctypes.c_int32)]
+                ("lr_min_ratio", ctypes.c_float), ("fused_head", ctypes.c_int32), ("dropout", ctypes.c_float),
+                ("dropout_seed", ctypes.c_uint32)]
 
 
 class PaciCounters(ctypes.Structure):
@@ -141,6 +142,8 @@ def shapes(cfg):
     s.lr_total = int(cfg.get("lr_total", 0))
     s.lr_min_ratio = float(cfg.get("lr_min_ratio", 0.1))
     s.fused_head = int(bool(cfg.get("fused_head", False)))
+    s.dropout = float(cfg.get("dropout", 0.0))
+    s.dropout_seed = int(cfg.get("dropout_seed", 0)) & 0xFFFFFFFF
     return s
 
 

@@ -34,7 +34,7 @@ constexpr float LOG2E = 1.4426950408889634f;
 // ---------------------------------------------------------------------------------------
 template <typename T, int DH>
 __global__ void __launch_bounds__(NT) attn_fwd_kernel(const T* qkv, T* out, float* lse2, int S, int H, int d,
-                                                       float scale_log2) {
+                                                       float scale_log2, DropArgs drop) {
   constexpr int V = Vec<T>::V;
   constexpr int BQ = 64;
   constexpr int DKV = DH / V;           // 16-byte vectors per head row
@@ -107,6 +107,14 @@ __global__ void __launch_bounds__(NT) attn_fwd_kernel(const T* qkv, T* out, floa
     rs = group4_sum(rs);
     l_run = l_run * alpha + rs;
     m_run = m_new;
+    if (drop.thr) {   // dropout: the product uses P * keep * scale, the normalizer all of P
+#pragma unroll
+      for (int kt = 0; kt < BKV / 16; ++kt) {
+        const uint32_t bits = drop_row4(drop, bh, qrow, k0 + kt * 16 + 4 * (l >> 4));
+#pragma unroll
+        for (int r = 0; r < 4; ++r) st[kt][r] = ((bits >> r) & 1) ? st[kt][r] * drop.scale : 0.f;
+      }
+    }
 #pragma unroll
     for (int t = 0; t < DH / 16; ++t) acc[t] *= alpha;
 #pragma unroll
@@ -201,7 +209,7 @@ template <int DH> struct FwdRing {
 
 template <int DH>
 __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(const bf16* qkv, bf16* out, float* lse2, int S, int H,
-                                                               int d, float scale_log2) {
+                                                               int d, float scale_log2, DropArgs drop) {
   using C = FwdRing<DH>;
   constexpr int QS = C::QS, KS = C::KS, NS = C::NS, CPR = C::CPR;
   __shared__ u32x4 ring[NS * 2 * C::BLK];
@@ -302,6 +310,14 @@ __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(cons
         }
       l_run[qs] = l_run[qs] * alpha + group4_sum(rs);
       m_run[qs] = m_new;
+      if (drop.thr) {   // dropout: the product uses P * keep * scale, the normalizer all of P
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) {
+          const uint32_t bits = drop_row4(drop, bh, qrow, k0 + kt * 16 + 4 * g);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sc[qs][kt][r] = ((bits >> r) & 1) ? sc[qs][kt][r] * drop.scale : 0.f;
+        }
+      }
 #pragma unroll
       for (int t = 0; t < DH / 16; ++t) acc[qs][t] *= alpha;
       pf[qs][0] = acc_to_frag<bf16>(sc[qs], 0);
@@ -364,7 +380,7 @@ __global__ void __launch_bounds__(NT) attn_dsum_kernel(const T* o, const T* dO, 
 template <typename T, int DH>
 __global__ void __launch_bounds__(NT) attn_bwd_dkdv_kernel(const T* qkv, const T* dO, const float* lse2,
                                                             const float* Dsum, T* dqkv, int S, int H, int d,
-                                                            float scale_log2, float scale) {
+                                                            float scale_log2, float scale, DropArgs drop) {
   constexpr int V = Vec<T>::V;
   constexpr int BQ = (DH >= 128) ? 32 : 64;  // queries per staged block (LDS budget)
   constexpr int DKV = DH / V;
@@ -421,14 +437,17 @@ __global__ void __launch_bounds__(NT) attn_bwd_dkdv_kernel(const T* qkv, const T
         mma_step<T>(s, lds_frag<BQ>(sQ, st, qt * 16), kf[st]);
         mma_step<T>(dp, lds_frag<BQ>(sdO, st, qt * 16), vf[st]);
       }
+      const uint32_t bits = drop.thr ? drop_col4(drop, bh, q0 + qt * 16 + 4 * (l >> 4), key) : 0xfu;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int qi = qt * 16 + 4 * (l >> 4) + r;
         const int q = q0 + qi;
         const bool ok = (key <= q) && (q < S) && (key < S);
         const float p = ok ? exp2f(s[r] * scale_log2 - sL[qi]) : 0.f;
-        P[qt][r] = p;
-        dS[qt][r] = p * (dp[r] - sD[qi]);
+        // dropout M = keep * scale: dV takes P M, dP = (dO V^T) M
+        const float mk = drop.thr ? (((bits >> r) & 1) ? drop.scale : 0.f) : 1.f;
+        P[qt][r] = p * mk;
+        dS[qt][r] = p * (dp[r] * mk - sD[qi]);
       }
     }
 #pragma unroll
@@ -459,7 +478,7 @@ __global__ void __launch_bounds__(NT) attn_bwd_dkdv_kernel(const T* qkv, const T
 template <typename T, int DH>
 __global__ void __launch_bounds__(NT) attn_bwd_dq_kernel(const T* qkv, const T* dO, const float* lse2,
                                                           const float* Dsum, T* dqkv, int S, int H, int d,
-                                                          float scale_log2, float scale) {
+                                                          float scale_log2, float scale, DropArgs drop) {
   constexpr int V = Vec<T>::V;
   constexpr int BQ = 64;
   constexpr int DKV = DH / V;
@@ -512,12 +531,14 @@ __global__ void __launch_bounds__(NT) attn_bwd_dq_kernel(const T* qkv, const T* 
         mma_step<T>(s, lds_frag<BKV>(sK, st, kt * 16), qf[st]);
         mma_step<T>(dp, lds_frag<BKV>(sV, st, kt * 16), gf[st]);
       }
+      const uint32_t bits = drop.thr ? drop_row4(drop, bh, qrow, k0 + kt * 16 + 4 * (l >> 4)) : 0xfu;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int key = k0 + kt * 16 + 4 * (l >> 4) + r;
         const bool ok = qok && (key <= qrow) && (key < S);
         const float p = ok ? exp2f(s[r] * scale_log2 - lq) : 0.f;
-        dS[kt][r] = p * (dp[r] - Dq);
+        const float mk = drop.thr ? (((bits >> r) & 1) ? drop.scale : 0.f) : 1.f;
+        dS[kt][r] = p * (dp[r] * mk - Dq);
       }
     }
 #pragma unroll
@@ -624,7 +645,8 @@ __device__ __forceinline__ void colsum_tiles(float (&v)[NCOL / 16][4], float* re
 template <int DH>
 __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn_dkdv_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
                                                                 bf16* dqkv, int S, int S_pad, int H, int d,
-                                                                float scale_log2, float scale, float* gbias) {
+                                                                float scale_log2, float scale, float* gbias,
+                                                                DropArgs drop) {
   using C = BwdRing<DH>;
   constexpr int SUB = C::SUB, KST = C::KST, NS = C::NS, CPR = C::CPR;
   __shared__ u32x4 ring[NS * C::STAGE];
@@ -703,7 +725,16 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
           }
         }
       }
-      // P = 2^(s * scale * log2 e - lse2), dS = P (dP - D); masked entries get P = 0
+      // P = 2^(s * scale * log2 e - lse2), dS = P (dP - D); masked entries get P = 0.
+      // Dropout M = keep * scale: dV takes P M, and dP = (dO V^T) M.
+      uint32_t dbits[2][SUB];
+      if (drop.thr) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int ks = 0; ks < SUB; ++ks)
+            dbits[u][ks] = drop_col4(drop, bh, q0 + (2 * s + u) * 16 + 4 * g, kw0 + 16 * ks + (l & 15));
+      }
       auto softmax = [&](auto masked) {
 #pragma unroll
         for (int u = 0; u < 2; ++u)
@@ -719,8 +750,14 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
                 x = (key <= q0 + qi && q0 + qi < S && key < S) ? x : -INFINITY;
               }
               const float p = fast_exp2(x);
-              sc[ks][u][r] = p;
-              dp[ks][u][r] = p * (dp[ks][u][r] - Dq);
+              if (drop.thr) {
+                const float mk = ((dbits[u][ks] >> r) & 1) ? drop.scale : 0.f;
+                sc[ks][u][r] = p * mk;
+                dp[ks][u][r] = p * (dp[ks][u][r] * mk - Dq);
+              } else {
+                sc[ks][u][r] = p;
+                dp[ks][u][r] = p * (dp[ks][u][r] - Dq);
+              }
             }
           }
       };
@@ -783,7 +820,8 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
 template <int DH>
 __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn_dq_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
                                                               bf16* dqkv, int S, int S_pad, int H, int d,
-                                                              float scale_log2, float scale, float* gbias) {
+                                                              float scale_log2, float scale, float* gbias,
+                                                              DropArgs drop) {
   using C = BwdRing<DH>;
   constexpr int SUB = C::SUB, KST = C::KST, NS = C::NS, CPR = C::CPR;
   __shared__ u32x4 ring[NS * 2 * C::BLK];
@@ -869,7 +907,9 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
         for (int qs = 0; qs < SUB; ++qs) {
           const int q = qw0 + 16 * qs + (l & 15);
 #pragma unroll
-          for (int u = 0; u < 2; ++u)
+          for (int u = 0; u < 2; ++u) {
+            // dropout M = keep * scale on dP = dO V^T
+            const uint32_t bits = drop.thr ? drop_row4(drop, bh, q, k0 + (2 * s + u) * 16 + 4 * g) : 0xfu;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               float x = fmaf(sc[qs][u][r], scale_log2, -lq[qs]);
@@ -878,8 +918,10 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
                 x = (key <= q && key < S && q < S) ? x : -INFINITY;
               }
               const float p = fast_exp2(x);
-              dp[qs][u][r] = p * (dp[qs][u][r] - Dq[qs]);
+              const float mk = drop.thr ? (((bits >> r) & 1) ? drop.scale : 0.f) : 1.f;
+              dp[qs][u][r] = p * (dp[qs][u][r] * mk - Dq[qs]);
             }
+          }
         }
       };
       if (edge) softmax(std::true_type());
@@ -924,25 +966,26 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
 }
 
 template <typename T, int DH>
-hipError_t fwd_launch(const void* qkv, void* o, float* lse2, int mu, int S, int H, hipStream_t st) {
+hipError_t fwd_launch(const void* qkv, void* o, float* lse2, int mu, int S, int H, const DropArgs& drop,
+                      hipStream_t st) {
   const int d = H * DH;
   const float scale_log2 = LOG2E / sqrtf((float)DH);
   if constexpr (sizeof(T) == 2) {
     using C = FwdRing<DH>;
     dim3 grid(mu * H, (S + C::BQ - 1) / C::BQ);   // x fastest: every head's heaviest query block first
     hipLaunchKernelGGL((attn_fwd_ring_kernel<DH>), grid, dim3(C::NTF), 0, st, reinterpret_cast<const bf16*>(qkv),
-                       reinterpret_cast<bf16*>(o), lse2, S, H, d, scale_log2);
+                       reinterpret_cast<bf16*>(o), lse2, S, H, d, scale_log2, drop);
     return hipGetLastError();
   }
   dim3 grid((S + 63) / 64, mu * H);
   hipLaunchKernelGGL((attn_fwd_kernel<T, DH>), grid, dim3(NT), 0, st, reinterpret_cast<const T*>(qkv),
-                     reinterpret_cast<T*>(o), lse2, S, H, d, scale_log2);
+                     reinterpret_cast<T*>(o), lse2, S, H, d, scale_log2, drop);
   return hipGetLastError();
 }
 
 template <typename T, int DH>
 hipError_t bwd_launch(const void* qkv, const void* o, const void* dO, const float* lse2, float* Dbuf, void* dqkv,
-                      float* gbias, int mu, int S, int H, hipStream_t st) {
+                      float* gbias, int mu, int S, int H, const DropArgs& drop, hipStream_t st) {
   const int d = H * DH;
   const float scale = 1.f / sqrtf((float)DH);
   const float scale_log2 = LOG2E * scale;
@@ -961,11 +1004,11 @@ hipError_t bwd_launch(const void* qkv, const void* o, const void* dO, const floa
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((attn_dkdv_ring_kernel<DH>), dim3(mu * H, (S + C::BR - 1) / C::BR), dim3(C::NTB), 0, st, q, g,
-                       Dbuf, dq, S, S_pad, H, d, scale_log2, scale, gbias);
+                       Dbuf, dq, S, S_pad, H, d, scale_log2, scale, gbias, drop);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((attn_dq_ring_kernel<DH>), dim3(mu * H, (S + C::BR - 1) / C::BR), dim3(C::NTB), 0, st, q, g, Dbuf,
-                       dq, S, S_pad, H, d, scale_log2, scale, gbias);
+                       dq, S, S_pad, H, d, scale_log2, scale, gbias, drop);
     return hipGetLastError();
   }
   constexpr int LPR = DH / Vec<T>::V;
@@ -977,25 +1020,26 @@ hipError_t bwd_launch(const void* qkv, const void* o, const void* dO, const floa
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, DH>), dim3((S + BKV - 1) / BKV, mu * H), dim3(NT), 0, st,
                      reinterpret_cast<const T*>(qkv), reinterpret_cast<const T*>(dO), lse2, Dbuf,
-                     reinterpret_cast<T*>(dqkv), S, H, d, scale_log2, scale);
+                     reinterpret_cast<T*>(dqkv), S, H, d, scale_log2, scale, drop);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attn_bwd_dq_kernel<T, DH>), dim3((S + 63) / 64, mu * H), dim3(NT), 0, st,
                      reinterpret_cast<const T*>(qkv), reinterpret_cast<const T*>(dO), lse2, Dbuf,
-                     reinterpret_cast<T*>(dqkv), S, H, d, scale_log2, scale);
+                     reinterpret_cast<T*>(dqkv), S, H, d, scale_log2, scale, drop);
   e = hipGetLastError();
   if (e != hipSuccess || gbias == nullptr) return e;
   return colsum_acc(sizeof(T) == 2 ? DT_BF16 : DT_F32, dqkv, 3 * d, mu * S, 3 * d, gbias, st);
 }
 
 template <typename T>
-hipError_t fwd_dh(const void* qkv, void* o, float* lse2, int mu, int S, int H, int dh, hipStream_t st) {
+hipError_t fwd_dh(const void* qkv, void* o, float* lse2, int mu, int S, int H, int dh, const DropArgs& drop,
+                  hipStream_t st) {
   switch (dh) {
-    case 32: return fwd_launch<T, 32>(qkv, o, lse2, mu, S, H, st);
-    case 64: return fwd_launch<T, 64>(qkv, o, lse2, mu, S, H, st);
+    case 32: return fwd_launch<T, 32>(qkv, o, lse2, mu, S, H, drop, st);
+    case 64: return fwd_launch<T, 64>(qkv, o, lse2, mu, S, H, drop, st);
     case 128:
       // fp32 at head_dim 128 would exceed the 64 KiB LDS budget of these tilings
-      if constexpr (sizeof(T) == 2) return fwd_launch<T, 128>(qkv, o, lse2, mu, S, H, st);
+      if constexpr (sizeof(T) == 2) return fwd_launch<T, 128>(qkv, o, lse2, mu, S, H, drop, st);
       break;
   }
   return hipErrorInvalidValue;
@@ -1003,13 +1047,13 @@ hipError_t fwd_dh(const void* qkv, void* o, float* lse2, int mu, int S, int H, i
 
 template <typename T>
 hipError_t bwd_dh(const void* qkv, const void* o, const void* dO, const float* lse2, float* Dbuf, void* dqkv,
-                  float* gbias, int mu, int S, int H, int dh, hipStream_t st) {
+                  float* gbias, int mu, int S, int H, int dh, const DropArgs& drop, hipStream_t st) {
   switch (dh) {
-    case 32: return bwd_launch<T, 32>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, st);
-    case 64: return bwd_launch<T, 64>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, st);
+    case 32: return bwd_launch<T, 32>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, drop, st);
+    case 64: return bwd_launch<T, 64>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, drop, st);
     case 128:
       if constexpr (sizeof(T) == 2)
-        return bwd_launch<T, 128>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, st);
+        return bwd_launch<T, 128>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, drop, st);
       break;
   }
   return hipErrorInvalidValue;
@@ -1017,10 +1061,11 @@ hipError_t bwd_dh(const void* qkv, const void* o, const void* dO, const float* l
 
 }  // namespace
 
-hipError_t attn_fwd(DType dt, const void* qkv, void* o, float* lse2, int mu, int S, int H, int dh, hipStream_t st) {
+hipError_t attn_fwd(DType dt, const void* qkv, void* o, float* lse2, int mu, int S, int H, int dh, const DropArgs& drop,
+                    hipStream_t st) {
   if (mu <= 0 || S <= 0 || H <= 0) return hipErrorInvalidValue;
-  if (dt == DT_BF16) return fwd_dh<bf16>(qkv, o, lse2, mu, S, H, dh, st);
-  return fwd_dh<float>(qkv, o, lse2, mu, S, H, dh, st);
+  if (dt == DT_BF16) return fwd_dh<bf16>(qkv, o, lse2, mu, S, H, dh, drop, st);
+  return fwd_dh<float>(qkv, o, lse2, mu, S, H, dh, drop, st);
 }
 
 int64_t attn_bwd_workspace_floats(DType dt, int mu, int S, int H) {
@@ -1029,10 +1074,10 @@ int64_t attn_bwd_workspace_floats(DType dt, int mu, int S, int H) {
 }
 
 hipError_t attn_bwd(DType dt, const void* qkv, const void* o, const void* dO, const float* lse2, float* Dbuf,
-                    void* dqkv, float* gbias, int mu, int S, int H, int dh, hipStream_t st) {
+                    void* dqkv, float* gbias, int mu, int S, int H, int dh, const DropArgs& drop, hipStream_t st) {
   if (mu <= 0 || S <= 0 || H <= 0) return hipErrorInvalidValue;
-  if (dt == DT_BF16) return bwd_dh<bf16>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, dh, st);
-  return bwd_dh<float>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, dh, st);
+  if (dt == DT_BF16) return bwd_dh<bf16>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, dh, drop, st);
+  return bwd_dh<float>(qkv, o, dO, lse2, Dbuf, dqkv, gbias, mu, S, H, dh, drop, st);
 }
 
 }  // namespace paci

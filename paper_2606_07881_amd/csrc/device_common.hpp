@@ -25,6 +25,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kernels.hpp"
+
 namespace paci {
 
 typedef __bf16 bf16;
@@ -325,5 +327,63 @@ __device__ __forceinline__ void wait_lds_reads() {
 // loads of the tile about to be read (wait_loads) and for its LDS reads of the
 // stage about to be refilled (wait_lds_reads).
 __device__ __forceinline__ void barrier_no_fence() { asm volatile("s_barrier" ::: "memory"); }
+
+// ---- dropout masks ---------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as easy
+// as 1, 2, 3", SC 2011): ten rounds of two 32 x 32 -> 64-bit products on a
+// 4-word counter, the 2-word key bumped by the Weyl constants between rounds.
+__device__ __forceinline__ u32x4 philox10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
+                                          uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c0), lo0 = 0xD2511F53u * c0;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c2), lo1 = 0xCD9E8D57u * c2;
+    c0 = hi1 ^ c1 ^ k0;
+    c2 = hi0 ^ c3 ^ k1;
+    c1 = lo1;
+    c3 = lo0;
+  }
+  return u32x4{c0, c1, c2, c3};
+}
+
+// Keep bits of a dropout site. Key (seed, micro-batch); `word` = (block << 2) |
+// site; a 16-bit value v keeps its element when v >= thr.
+//   attention probability (bh, q, k): counter (k >> 2, q >> 1, bh, word), value
+//     (k & 1) of output word 2 (q & 1) + ((k >> 1) & 1);
+//   element e of an element-wise site: counter (e >> 3, e >> 35, 0, word), value
+//     (e & 1) of output word (e >> 1) & 3.
+__device__ __forceinline__ uint32_t keep16(uint32_t w, int half, uint32_t thr) {
+  return ((half ? (w >> 16) : (w & 0xffffu)) >= thr) ? 1u : 0u;
+}
+// bit i: probability (q, k4 + i), i < 4, k4 % 4 == 0 (one draw)
+__device__ __forceinline__ uint32_t drop_row4(const DropArgs& a, uint32_t bh, int q, int k4) {
+  const u32x4 w = philox10((uint32_t)k4 >> 2, (uint32_t)q >> 1, bh, a.word, a.seed, a.mb);
+  const uint32_t x = (q & 1) ? w[2] : w[0], y = (q & 1) ? w[3] : w[1];
+  return keep16(x, 0, a.thr) | (keep16(x, 1, a.thr) << 1) | (keep16(y, 0, a.thr) << 2) | (keep16(y, 1, a.thr) << 3);
+}
+// bit i: probability (q4 + i, k), i < 4, q4 % 4 == 0 (two draws)
+__device__ __forceinline__ uint32_t drop_col4(const DropArgs& a, uint32_t bh, int q4, int k) {
+  const int kb = (k >> 1) & 1, half = k & 1;
+  uint32_t bits = 0;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {   // queries q4 + 2j + e share the counter of (q4 >> 1) + j
+    const u32x4 w = philox10((uint32_t)k >> 2, ((uint32_t)q4 >> 1) + j, bh, a.word, a.seed, a.mb);
+    bits |= keep16(kb ? w[1] : w[0], half, a.thr) << (2 * j);
+    bits |= keep16(kb ? w[3] : w[2], half, a.thr) << (2 * j + 1);
+  }
+  return bits;
+}
+// bit i: element e8 + i, i < 8, e8 % 8 == 0 (one draw)
+__device__ __forceinline__ uint32_t drop_elem8(const DropArgs& a, uint64_t e8) {
+  const u32x4 w = philox10((uint32_t)(e8 >> 3), (uint32_t)(e8 >> 35), 0u, a.word, a.seed, a.mb);
+  uint32_t bits = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) bits |= keep16(w[i >> 1], i & 1, a.thr) << i;
+  return bits;
+}
 
 }  // namespace paci

@@ -8,6 +8,15 @@ namespace paci {
 
 enum DType { DT_F32 = 0, DT_BF16 = 1 };
 
+// Dropout at one site of one micro-batch: key (seed, mb), site word
+// (block << 2) | site (0 embedding, 1 attention probabilities, 2 projection
+// output, 3 FFN output); an element is kept when its 16-bit Philox value is
+// >= thr (thr 0: no dropout) and then scaled by `scale` = 1 / (1 - p).
+struct DropArgs {
+  uint32_t seed = 0, mb = 0, word = 0, thr = 0;
+  float scale = 1.f;
+};
+
 // ---- GEMM: C[m][n] = sum_k A(m, k) B(k, n) -------------------------------------------
 // Operand layouts (ld in elements):
 //   GEMM_NT (forward, y = x W^T):      A(m,k) = A[m*lda + k], B(k,n) = B[n*ldb + k]
@@ -68,13 +77,14 @@ void gemm_set_tile_override(int cfg);
 
 // ---- causal attention over the fused projection qkv [T, 3d] --------------------------
 // Forward: o [T, d]; lse2 [mu*H*S] = log2-sum-exp2 of the scaled scores in log2 units.
-hipError_t attn_fwd(DType dt, const void* qkv, void* o, float* lse2, int mu, int S, int H, int dh, hipStream_t st);
+hipError_t attn_fwd(DType dt, const void* qkv, void* o, float* lse2, int mu, int S, int H, int dh, const DropArgs& drop,
+                    hipStream_t st);
 // Backward: D = rowsum(dO * O) per (b, h, query), then dK, dV and dQ into dqkv [T, 3d].
 // Dbuf is workspace of attn_bwd_workspace_floats() floats. gbias (optional, fp32 [3d]):
 // += the column sums of dqkv, i.e. the gradient of the qkv projection's bias.
 int64_t attn_bwd_workspace_floats(DType dt, int mu, int S, int H);
 hipError_t attn_bwd(DType dt, const void* qkv, const void* o, const void* dO, const float* lse2, float* Dbuf,
-                    void* dqkv, float* gbias, int mu, int S, int H, int dh, hipStream_t st);
+                    void* dqkv, float* gbias, int mu, int S, int H, int dh, const DropArgs& drop, hipStream_t st);
 
 // ---- LayerNorm -----------------------------------------------------------------------
 // n = (x - mean) * rstd * gamma + beta, per row of d; xcopy (optional) receives x.
@@ -86,6 +96,12 @@ hipError_t layernorm_fwd(DType dt, const void* x, void* n, float* mean, float* r
 hipError_t layernorm_bwd(DType dt, const void* dn, const void* x, const float* mean, const float* rstd,
                          const float* gamma, const void* res, void* dx, float* Ggamma, float* Gbeta, float* Gdx,
                          int rows, int d, hipStream_t st);
+
+// ---- dropout at the element-wise sites ----------------------------------------------------
+// out = res + z * keep * scale over rows x cols (cols % 8 == 0; res nullable:
+// out = z * keep * scale; out may alias z). Element e = r * cols + c.
+hipError_t dropout_fwd(DType dt, const void* z, const void* res, void* out, int rows, int cols, const DropArgs& drop,
+                       hipStream_t st);
 
 // ---- column sums accumulated into fp32 (bias gradients) ---------------------------------
 // G[c] += sum_r Y[r*ld + c], c < ncols (fp32 atomics).

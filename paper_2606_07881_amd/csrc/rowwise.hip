@@ -286,6 +286,41 @@ hipError_t layernorm_bwd(DType dt, const void* dn, const void* x, const float* m
   return ln_bwd_t<float>(dn, x, mean, rstd, gamma, res, dx, Gg, Gb, Gd, rows, d, st);
 }
 
+namespace {
+// out = res + z * keep * scale, 8 consecutive elements per thread (one Philox draw).
+template <typename T>
+__global__ void __launch_bounds__(NT) dropout_kernel(const T* z, const T* res, T* out,
+                                                     int64_t n8, DropArgs drop) {
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (i >= n8) return;
+  const uint64_t e8 = (uint64_t)i * 8;
+  const uint32_t bits = drop_elem8(drop, e8);
+  float v[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    float x = ((bits >> j) & 1) ? to_f32(z[e8 + j]) * drop.scale : 0.f;
+    if (res != nullptr) x += to_f32(res[e8 + j]);
+    v[j] = x;
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) out[e8 + j] = from_f32<T>(v[j]);
+}
+}  // namespace
+
+hipError_t dropout_fwd(DType dt, const void* z, const void* res, void* out, int rows, int cols, const DropArgs& drop,
+                       hipStream_t st) {
+  if (rows <= 0 || cols <= 0 || cols % 8 || drop.thr == 0) return hipErrorInvalidValue;
+  const int64_t n8 = (int64_t)rows * cols / 8;
+  const dim3 grid((unsigned)((n8 + NT - 1) / NT));
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL(dropout_kernel<bf16>, grid, dim3(NT), 0, st, reinterpret_cast<const bf16*>(z),
+                       reinterpret_cast<const bf16*>(res), reinterpret_cast<bf16*>(out), n8, drop);
+  else
+    hipLaunchKernelGGL(dropout_kernel<float>, grid, dim3(NT), 0, st, reinterpret_cast<const float*>(z),
+                       reinterpret_cast<const float*>(res), reinterpret_cast<float*>(out), n8, drop);
+  return hipGetLastError();
+}
+
 hipError_t colsum_acc(DType dt, const void* Y, int64_t ld, int rows, int ncols, float* G, hipStream_t st) {
   if (rows <= 0 || ncols <= 0 || ncols % 8 || ld % 8) return hipErrorInvalidValue;
   const int V = (dt == DT_BF16) ? 8 : 4;

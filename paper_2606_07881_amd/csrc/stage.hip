@@ -208,6 +208,7 @@ int validate_shapes(const paci_shapes* s, int K, int delay) {
   if (s->dtype != PACI_FP32 && s->dtype != PACI_BF16) return PACI_E_UNSUPPORTED;
   if (s->recompute != 0 && s->recompute != 1) return PACI_E_INVAL;
   if (s->fused_head != 0 && s->fused_head != 1) return PACI_E_INVAL;
+  if (!(s->dropout >= 0.f && s->dropout < 1.f)) return PACI_E_INVAL;
   if (s->fused_head) {
     if (s->kind != PACI_LAST || s->dtype != PACI_BF16 || s->d_model % 8) return PACI_E_UNSUPPORTED;
     if (delay != 0) return PACI_E_INVAL;   // the recomputed logits must see the forward's parameters
@@ -292,6 +293,11 @@ struct Layout {
   struct WinBlock { size_t dqkv, dx1, du, dy; };   // per block: [K * T, width] each
   std::vector<WinBlock> win;
   size_t s_ids = 0, s_tgt = 0, s_y = 0, s_meanf = 0, s_rstdf = 0, s_nf = 0, s_z = 0, s_lse_ce = 0;
+  // dropout: the unmasked output gradient of a block (windowed stages), the
+  // unmasked x1 gradient, the masked FFN-branch gradient (stages without the
+  // window), and the pre-dropout branch output in the forward
+  bool dropout = false;
+  size_t w_dyu = 0, w_dx1u = 0, w_g2 = 0, w_zdrop = 0;
   // fused LM head: no logits per slot; (max, sum) per row and 64 columns, target logits
   bool fused_head = false;
   int ngroups = 0;
@@ -302,6 +308,10 @@ struct Layout {
 };
 
 constexpr int64_t CHUNK = 16384;  // AdamW elements per workgroup
+
+// Dropout: a 16-bit Philox value v keeps its element when v >= thr (0: off)
+uint32_t drop_threshold(const paci_shapes& s) { return (uint32_t)std::floor((double)s.dropout * 65536.0 + 0.5); }
+enum DropSite { SITE_EMBED = 0, SITE_ATTN = 1, SITE_PROJ = 2, SITE_FFN = 3 };
 
 int count_chunks(const ParamTable& p) {
   int n = 0;
@@ -411,6 +421,13 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
   }
   L.w_part = a.take(4 * part);
   L.w_loss = a.take(256);
+  L.dropout = drop_threshold(s) > 0;
+  if (L.dropout) {
+    L.w_dyu = a.take(esz * T * d);
+    L.w_dx1u = a.take(esz * T * d);
+    L.w_g2 = a.take(esz * T * d);
+    L.w_zdrop = a.take(esz * T * d);
+  }
   L.total = (a.off + 255) & ~(size_t)255;
   return L;
 }
@@ -418,11 +435,11 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
 // ---- kernel timing families -------------------------------------------------------------------
 enum Family {
   F_GEMM_FWD = 0, F_GEMM_DGRAD, F_GEMM_WGRAD, F_ATTN_FWD, F_ATTN_BWD, F_LN_FWD, F_LN_BWD, F_BIAS_GRAD, F_ADAMW,
-  F_EMBED, F_CE, F_COPY, F_COUNT
+  F_EMBED, F_CE, F_COPY, F_DROPOUT, F_COUNT
 };
 const char* kFamilyNames[F_COUNT] = {"gemm_fwd", "gemm_dgrad", "gemm_wgrad_acc", "attn_fwd", "attn_bwd",
                                      "layernorm_fwd", "layernorm_bwd", "bias_grad", "adamw", "embedding",
-                                     "cross_entropy", "copy"};
+                                     "cross_entropy", "copy", "dropout"};
 
 }  // namespace
 
@@ -450,6 +467,17 @@ struct paci_stage {
   int64_t launches[F_COUNT] = {};
   double ms[F_COUNT] = {}, work[F_COUNT] = {};
 
+  // dropout at one site of micro-batch mb (thr 0 when the stage has none)
+  paci::DropArgs drop(int mb, int block, int site) const {
+    paci::DropArgs a;
+    if (!L.dropout) return a;
+    a.seed = s.dropout_seed;
+    a.mb = (uint32_t)mb;
+    a.word = ((uint32_t)block << 2) | (uint32_t)site;
+    a.thr = drop_threshold(s);
+    a.scale = 1.f / (1.f - s.dropout);
+    return a;
+  }
   float* theta() const { return reinterpret_cast<float*>(arena + L.theta); }
   float* G() const { return reinterpret_cast<float*>(arena + L.G); }
   float* m() const { return reinterpret_cast<float*>(arena + L.m); }
@@ -585,6 +613,13 @@ int bias_grad(paci_stage* h, const void* Y, int64_t ld, int rows, int ncols, int
   });
 }
 
+// out = res + z * keep * scale over [T, d] (res nullable)
+int dropout(paci_stage* h, const void* z, const void* res, void* out, const paci::DropArgs& a) {
+  const int T = (int)h->L.T, d = h->s.d_model;
+  return run(h, F_DROPOUT, (double)T * d * h->esz * (res ? 3 : 2),
+             [&] { return paci::dropout_fwd(h->dt, z, res, out, T, d, a, h->st); });
+}
+
 int ln_fwd(paci_stage* h, const void* x, void* n, float* mean, float* rstd, int64_t g_off, int64_t b_off,
            void* xcopy) {
   const int T = (int)h->L.T, d = h->s.d_model;
@@ -612,7 +647,7 @@ double attn_pairs(const paci_shapes& s) {
 // ---- forward of the block stack -----------------------------------------------------------------
 // in: block-0 input (stage input or embedding output); x0_copy: where to store a
 // copy of it (nullptr: `in` stays valid), which block 0's residual then reads.
-int blocks_fwd(paci_stage* h, char* sl, const void* in, void* x0_copy, void* out) {
+int blocks_fwd(paci_stage* h, char* sl, const void* in, void* x0_copy, void* out, int mb) {
   const paci_shapes& s = h->s;
   const int T = (int)h->L.T, d = s.d_model, f = s.d_ff;
   for (int l = 0; l < s.n_layers; ++l) {
@@ -625,15 +660,26 @@ int blocks_fwd(paci_stage* h, char* sl, const void* in, void* x0_copy, void* out
     TRY(linear_fwd(h, sl + o.n1, b.w_qkv, b.b_qkv, T, 3 * d, d, paci::EPI_BIAS, sl + o.qkv, nullptr, nullptr));
     TRY(run(h, F_ATTN_FWD, 4.0 * attn_pairs(s) * s.head_dim, [&] {
       return paci::attn_fwd(h->dt, sl + o.qkv, sl + o.o, reinterpret_cast<float*>(sl + o.lse2), s.micro_batch, s.seq,
-                            s.n_heads, s.head_dim, h->st);
+                            s.n_heads, s.head_dim, h->drop(mb, l, SITE_ATTN), h->st);
     }));
     const void* res = l > 0 ? (const void*)(sl + o.x) : (x0_copy ? (const void*)x0_copy : in);
-    TRY(linear_fwd(h, sl + o.o, b.w_o, b.b_o, T, d, d, paci::EPI_BIAS_RES, sl + o.x1, res, nullptr));
+    char* zd = h->L.dropout ? h->ws(h->L.w_zdrop) : nullptr;   // a branch output before its dropout
+    if (zd) {
+      TRY(linear_fwd(h, sl + o.o, b.w_o, b.b_o, T, d, d, paci::EPI_BIAS, zd, nullptr, nullptr));
+      TRY(dropout(h, zd, res, sl + o.x1, h->drop(mb, l, SITE_PROJ)));
+    } else {
+      TRY(linear_fwd(h, sl + o.o, b.w_o, b.b_o, T, d, d, paci::EPI_BIAS_RES, sl + o.x1, res, nullptr));
+    }
     TRY(ln_fwd(h, sl + o.x1, sl + o.n2, reinterpret_cast<float*>(sl + o.mean2), reinterpret_cast<float*>(sl + o.rstd2),
                b.ln2_g, b.ln2_b, nullptr));
     TRY(linear_fwd(h, sl + o.n2, b.w_1, b.b_1, T, f, d, paci::EPI_BIAS_GELU, sl + o.u, nullptr, sl + o.a));
     void* y = (l + 1 < s.n_layers) ? (void*)(sl + h->L.blk[l + 1].x) : out;
-    TRY(linear_fwd(h, sl + o.a, b.w_2, b.b_2, T, d, f, paci::EPI_BIAS_RES, y, sl + o.x1, nullptr));
+    if (zd) {
+      TRY(linear_fwd(h, sl + o.a, b.w_2, b.b_2, T, d, f, paci::EPI_BIAS, zd, nullptr, nullptr));
+      TRY(dropout(h, zd, sl + o.x1, y, h->drop(mb, l, SITE_FFN)));
+    } else {
+      TRY(linear_fwd(h, sl + o.a, b.w_2, b.b_2, T, d, f, paci::EPI_BIAS_RES, y, sl + o.x1, nullptr));
+    }
   }
   return PACI_OK;
 }
@@ -643,46 +689,67 @@ int blocks_fwd(paci_stage* h, char* sl, const void* in, void* x0_copy, void* out
 // LayerNorm backward that produced dy)
 // j: the micro-batch's position in its window (windowed weight gradients: the
 // block's output gradients go to the window buffer and G_W waits for the flush)
-int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx, bool dy_bias_done, int j) {
+int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx, bool dy_bias_done, int j, int mb) {
   const paci_shapes& s = h->s;
   const int T = (int)h->L.T, d = s.d_model, f = s.d_ff;
   const BlockRefs& b = h->p.blocks[l];
   const BlockSlot& o = h->L.blk[l];
   const Layout& L = h->L;
-  const bool win = L.window;
+  const bool win = L.window, drop = L.dropout;
   char* du = win ? h->win(L.win[l].du, j, f) : h->ws(L.w_du);
   char* dn = h->ws(L.w_dn);
   char* dx1 = win ? h->win(L.win[l].dx1, j, d) : h->ws(L.w_dx1);
   char* dO = h->ws(L.w_do);
   char* dqkv = win ? h->win(L.win[l].dqkv, j, 3 * d) : h->ws(L.w_dqkv);
-  // y = x1 + a W2^T + b2
-  if (!win) TRY(linear_wgrad(h, dy, d, sl + o.a, f, d, f, T, b.w_2));
-  if (!dy_bias_done) TRY(bias_grad(h, dy, d, T, d, b.b_2));
-  // du = (dy W2) * gelu'(u), and G_b1 += sum du in the same epilogue
-  TRY(linear_dgrad(h, dy, d, b.w_2, T, f, d, paci::EPI_GELU_GRAD, du, sl + o.u, b.b_1));
+  // y = x1 + drop(a W2^T + b2): the branch gets g2 = dy * keep * scale (without
+  // dropout g2 = dy); the residual path keeps dy. A windowed stage's window
+  // slot must end up holding g2 (the flush contracts it), so dy moves aside.
+  const void* dyu = dy;
+  const void* g2 = dy;
+  if (drop) {
+    char* g2buf = win ? h->win(L.win[l].dy, j, d) : h->ws(L.w_g2);
+    if (win) {
+      TRY(run(h, F_COPY, 2.0 * T * d * h->esz, [&] {
+        return hipMemcpyAsync(h->ws(L.w_dyu), dy, (size_t)T * d * h->esz, hipMemcpyDeviceToDevice, h->st);
+      }));
+      dyu = h->ws(L.w_dyu);
+    }
+    TRY(dropout(h, dyu, nullptr, g2buf, h->drop(mb, l, SITE_FFN)));
+    g2 = g2buf;
+  }
+  if (!win) TRY(linear_wgrad(h, g2, d, sl + o.a, f, d, f, T, b.w_2));
+  if (!dy_bias_done || drop) TRY(bias_grad(h, g2, d, T, d, b.b_2));
+  // du = (g2 W2) * gelu'(u), and G_b1 += sum du in the same epilogue
+  TRY(linear_dgrad(h, g2, d, b.w_2, T, f, d, paci::EPI_GELU_GRAD, du, sl + o.u, b.b_1));
   // u = n2 W1^T + b1
   if (!win) TRY(linear_wgrad(h, du, f, sl + o.n2, d, f, d, T, b.w_1));
   TRY(linear_dgrad(h, du, f, b.w_1, T, d, f, paci::EPI_STORE, dn, nullptr));
-  // n2 = LN2(x1); dx1 = dy + LN2 backward, and G_bo += sum dx1
+  // n2 = LN2(x1); dL/dx1 = dy + LN2 backward (and G_bo += its column sums when
+  // there is no dropout: then it is also the projection branch's gradient)
+  char* dx1u = drop ? h->ws(L.w_dx1u) : dx1;
   TRY(ln_bwd(h, dn, sl + o.x1, reinterpret_cast<const float*>(sl + o.mean2),
-             reinterpret_cast<const float*>(sl + o.rstd2), b.ln2_g, b.ln2_b, dy, dx1, b.b_o));
-  // x1 = x + o Wo^T + bo
+             reinterpret_cast<const float*>(sl + o.rstd2), b.ln2_g, b.ln2_b, dyu, dx1u, drop ? -1 : b.b_o));
+  // x1 = x + drop(o Wo^T + bo): the branch gets g1 = dL/dx1 * keep * scale, in dx1
+  if (drop) {
+    TRY(dropout(h, dx1u, nullptr, dx1, h->drop(mb, l, SITE_PROJ)));
+    TRY(bias_grad(h, dx1, d, T, d, b.b_o));
+  }
   if (!win) TRY(linear_wgrad(h, dx1, d, sl + o.o, d, d, d, T, b.w_o));
   TRY(linear_dgrad(h, dx1, d, b.w_o, T, d, d, paci::EPI_STORE, dO, nullptr));
   // attention; G_bqkv += sum dqkv in the same kernels
   TRY(run(h, F_ATTN_BWD, 8.0 * attn_pairs(s) * s.head_dim, [&] {
     return paci::attn_bwd(h->dt, sl + o.qkv, sl + o.o, dO, reinterpret_cast<const float*>(sl + o.lse2),
                           reinterpret_cast<float*>(h->ws(L.w_D)), dqkv, h->g(b.b_qkv), s.micro_batch, s.seq,
-                          s.n_heads, s.head_dim, h->st);
+                          s.n_heads, s.head_dim, h->drop(mb, l, SITE_ATTN), h->st);
   }));
   // qkv = n1 Wqkv^T + bqkv
   if (!win) TRY(linear_wgrad(h, dqkv, 3 * d, sl + o.n1, d, 3 * d, d, T, b.w_qkv));
   TRY(linear_dgrad(h, dqkv, 3 * d, b.w_qkv, T, d, 3 * d, paci::EPI_STORE, dn, nullptr));
-  // n1 = LN1(x); dx = dx1 + LN1 backward; dx is the output gradient of block l - 1,
-  // so G_b2 of that block += sum dx
+  // n1 = LN1(x); dx = dL/dx1 + LN1 backward; dx is the output gradient of block
+  // l - 1, so (without dropout) G_b2 of that block += sum dx
   TRY(ln_bwd(h, dn, sl + o.x, reinterpret_cast<const float*>(sl + o.mean1),
-             reinterpret_cast<const float*>(sl + o.rstd1), b.ln1_g, b.ln1_b, dx1, dx,
-             l > 0 ? h->p.blocks[l - 1].b_2 : -1));
+             reinterpret_cast<const float*>(sl + o.rstd1), b.ln1_g, b.ln1_b, dx1u, dx,
+             (l > 0 && !drop) ? h->p.blocks[l - 1].b_2 : -1));
   return PACI_OK;
 }
 
@@ -744,7 +811,7 @@ int flush_window(paci_stage* h) {
 // stage) and targets (last stage) as stored; out: the stage output (last stage:
 // the loss).
 int stage_forward_into(paci_stage* h, char* A, const void* in, void* x0_copy, const int32_t* ids,
-                       const int32_t* tgt, void* out) {
+                       const int32_t* tgt, void* out, int mb) {
   const paci_shapes& s = h->s;
   const Layout& L = h->L;
   const int T = (int)L.T, d = s.d_model;
@@ -753,10 +820,11 @@ int stage_forward_into(paci_stage* h, char* A, const void* in, void* x0_copy, co
       return paci::embed_fwd(h->dt, ids, h->th(h->p.wte), h->th(h->p.wpe), A + L.blk[0].x, s.micro_batch, s.seq, d,
                              s.vocab, h->st);
     }));
-    return blocks_fwd(h, A, A + L.blk[0].x, nullptr, out);
+    if (L.dropout) TRY(dropout(h, A + L.blk[0].x, nullptr, A + L.blk[0].x, h->drop(mb, 0, SITE_EMBED)));
+    return blocks_fwd(h, A, A + L.blk[0].x, nullptr, out, mb);
   }
-  if (s.kind == PACI_MIDDLE) return blocks_fwd(h, A, in, x0_copy, out);
-  TRY(blocks_fwd(h, A, in, x0_copy, A + L.s_y));
+  if (s.kind == PACI_MIDDLE) return blocks_fwd(h, A, in, x0_copy, out, mb);
+  TRY(blocks_fwd(h, A, in, x0_copy, A + L.s_y, mb));
   float* meanf = reinterpret_cast<float*>(A + L.s_meanf);
   float* rstdf = reinterpret_cast<float*>(A + L.s_rstdf);
   TRY(ln_fwd(h, A + L.s_y, A + L.s_nf, meanf, rstdf, h->p.lnf_g, h->p.lnf_b, nullptr));
@@ -954,15 +1022,15 @@ extern "C" int paci_stage_forward(paci_stage* h, int mb, const void* dev_in, con
     r = run(h, F_COPY, 8.0 * T, [&] {
       return hipMemcpyAsync(ids, dev_in, 4 * (size_t)T, hipMemcpyDeviceToDevice, h->st);
     });
-    if (!r) r = stage_forward_into(h, A, nullptr, nullptr, ids, nullptr, dev_out);
+    if (!r) r = stage_forward_into(h, A, nullptr, nullptr, ids, nullptr, dev_out, mb);
   } else if (s.kind == PACI_MIDDLE) {
-    r = stage_forward_into(h, A, dev_in, x0, nullptr, nullptr, dev_out);
+    r = stage_forward_into(h, A, dev_in, x0, nullptr, nullptr, dev_out, mb);
   } else {
     int32_t* tgt = reinterpret_cast<int32_t*>(sl + (L.recompute ? L.c_tgt : L.s_tgt));
     r = run(h, F_COPY, 8.0 * T, [&] {
       return hipMemcpyAsync(tgt, dev_targets, 4 * (size_t)T, hipMemcpyDeviceToDevice, h->st);
     });
-    if (!r) r = stage_forward_into(h, A, dev_in, x0, nullptr, tgt, dev_out);
+    if (!r) r = stage_forward_into(h, A, dev_in, x0, nullptr, tgt, dev_out, mb);
   }
   if (r) return r;
   const int t = fsm_commit_forward(h->fsm);
@@ -997,8 +1065,8 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
     // checkpointed: the activations again, from the stored input, under the
     // parameters current now (the output, or loss, is discarded)
     void* out = s.kind == PACI_LAST ? (void*)h->ws(L.w_loss) : (void*)bufB;
-    r = s.kind == PACI_FIRST ? stage_forward_into(h, A, nullptr, nullptr, ids, nullptr, out)
-                             : stage_forward_into(h, A, sl + L.c_x, A + L.blk[0].x, nullptr, tgt, out);
+    r = s.kind == PACI_FIRST ? stage_forward_into(h, A, nullptr, nullptr, ids, nullptr, out, mb)
+                             : stage_forward_into(h, A, sl + L.c_x, A + L.blk[0].x, nullptr, tgt, out, mb);
   }
   if (!r && s.kind == PACI_LAST) {
     char* dz = h->ws(L.w_dz);
@@ -1025,7 +1093,7 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
     if (!r)   // the last block's output gradient; G_b2 of that block += its column sums
       r = ln_bwd(h, dnf, A + L.s_y, reinterpret_cast<const float*>(A + L.s_meanf),
                  reinterpret_cast<const float*>(A + L.s_rstdf), h->p.lnf_g, h->p.lnf_b, nullptr, dy_last,
-                 h->p.blocks[s.n_layers - 1].b_2);
+                 L.dropout ? -1 : h->p.blocks[s.n_layers - 1].b_2);
     dy = dy_last;
   } else if (!r && win) {
     r = run(h, F_COPY, 2.0 * act_bytes(h), [&] {
@@ -1042,8 +1110,12 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
     else
       dx = (dy == bufA) ? bufB : bufA;
     // every block's dy but the given stage output gradient came out of a LayerNorm backward
-    r = block_bwd(h, A, l, dy, dx, l < s.n_layers - 1 || s.kind == PACI_LAST, j);
+    r = block_bwd(h, A, l, dy, dx, l < s.n_layers - 1 || s.kind == PACI_LAST, j, mb);
     dy = dx;
+  }
+  if (!r && s.kind == PACI_FIRST && L.dropout) {   // through the embedding dropout
+    r = dropout(h, dy, nullptr, h->ws(L.w_g2), h->drop(mb, 0, SITE_EMBED));
+    dy = h->ws(L.w_g2);
   }
   if (!r && s.kind == PACI_FIRST) {
     r = run(h, F_EMBED, (double)T * d * (h->esz + 8), [&] {

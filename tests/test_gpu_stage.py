@@ -50,7 +50,7 @@ def _one_event_pair(binding, c, seed=0):
 
 @pytest.mark.parametrize("name", ["tiny_fp32", "ragged_bf16", "ragged_fp32", "win_bf16", "dh128_bf16", "dh32_bf16",
                                   "dh64_fp32", "first_bf16", "last_bf16", "first_fp32", "last_fp32",
-                                  "fused_last_bf16"])
+                                  "fused_last_bf16", "drop_ragged_fp32", "drop_first_bf16"])
 def test_first_forward_backward(binding, name):
     c = configs.get("tiny_fp32") if name == "tiny_fp32" else small_cfg(name)
     (g_out, g_in, G), (o_out, o_in, o_G) = _one_event_pair(binding, c)
@@ -70,7 +70,10 @@ def test_first_forward_backward(binding, name):
 @pytest.mark.parametrize("name", ["tiny_fp32", "ragged_bf16", "ragged_fp32", "win_bf16", "win8_bf16", "dh128_bf16",
                                   "dh32_bf16", "first_bf16", "last_bf16", "first_fp32", "last_fp32",
                                   "ckpt_tiny_fp32", "ckpt_ragged_bf16", "ckpt_win_bf16", "ckpt_first_bf16",
-                                  "ckpt_last_bf16", "sched_bf16", "fused_last_bf16", "ckpt_fused_last_bf16"])
+                                  "ckpt_last_bf16", "sched_bf16", "fused_last_bf16", "ckpt_fused_last_bf16",
+                                  "drop_tiny_fp32", "drop_ragged_bf16", "drop_ragged_fp32", "drop_win_bf16",
+                                  "drop_dh128_bf16", "drop_dh32_bf16", "drop_first_bf16", "drop_last_bf16",
+                                  "drop_first_fp32", "drop_last_fp32", "ckpt_drop_ragged_bf16"])
 def test_replay_parity(binding, name):
     """The whole asynchronous 1F1B replay: stamps bit-exact, every output, input
     gradient, accumulated G and the state after every AdamW update."""
@@ -267,3 +270,26 @@ def test_flush_schedule_parity(binding, name):
     assert st.counters()["next_f"] == 0
     assert np.array_equal(st.read(binding.PARAMS), before)
     st.close()
+
+
+@pytest.mark.parametrize("name", ["drop_ragged_fp32", "drop_win_bf16", "drop_first_fp32"])
+def test_dropout_masks_in_every_window(binding, name):
+    """lr = 0 keeps the parameters fixed, so every window's G, output and input
+    gradient must match the oracle at the base tolerance with no allowance for
+    downstream drift: the masks of every micro-batch (keyed by its index) agree."""
+    c = small_cfg(name, lr=0.0)
+    inp = Inputs(c, 3, c["M"])
+    g = gpu_replay(c, inp)
+    o = oracle_replay(c, inp)
+    ta, tg = tol(c, "act"), tol(c, "grad")
+    for i in range(c["M"]):
+        assert rel_err(np.atleast_1d(g["out"][i]), np.atleast_1d(o["out"][i])) <= ta, f"out[{i}]"
+        if o["grad_in"][i] is not None:
+            assert rel_err(g["grad_in"][i], o["grad_in"][i]) <= ta, f"grad_in[{i}]"
+    worst = 0.0
+    for s in range(len(o["G"])):
+        for n in o["G"][s]:
+            e = rel_err(g["G"][s][n], o["G"][s][n])
+            worst = max(worst, e)
+            assert e <= tg, f"G[{n}] of window {s + 1}: {e:.3e}"
+    print(name, "lr=0 worst G over all windows", f"{worst:.2e}", flush=True)
