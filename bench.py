@@ -109,6 +109,9 @@ def main():
                          "in each backward under the current parameters")
     ap.add_argument("--fused-head", action="store_true",
                     help="last stage: the fused LM head (no [T, V] logits kept; the backward recomputes them)")
+    ap.add_argument("--dropout", type=float, default=0.0,
+                    help="dropout rate at the embedding, attention-probability and residual-branch sites "
+                         "(the paper trains with 0.1; the headline workload has none)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy a 256 MiB device buffer 3 times (a kernel of known traffic, for scaling "
                          "hardware byte counters)")
@@ -128,6 +131,9 @@ def main():
         over["recompute"] = 1
     if args.fused_head:
         over["fused_head"] = 1
+    if args.dropout > 0:
+        over["dropout"] = args.dropout
+        over["dropout_seed"] = 2606
     c = configs.get(name, **over)
     name = c["name"]
     M, K, delay = c["M"], c["K"], c["delay"]
@@ -254,6 +260,7 @@ def main():
                                f"{M} micro-batches, delay {delay}, AdamW every K={K}"
                                + ("; activation-checkpointed (forward recomputed in each backward)"
                                   if c.get("recompute") else "")
+                               + (f"; dropout {c['dropout']} at every site" if c.get("dropout") else "")
                                + (f"; LM head over V={c['vocab']} with softmax cross-entropy"
                                   + (", fused (no logits kept)" if c.get("fused_head") else ", fp32 logits kept")
                                   if c["kind"] == "last" else ""),

@@ -32,7 +32,7 @@ constexpr int BKV = 64;   // keys per block
 constexpr float LOG2E = 1.4426950408889634f;
 
 // ---------------------------------------------------------------------------------------
-template <typename T, int DH>
+template <typename T, int DH, bool DROP>
 __global__ void __launch_bounds__(NT) attn_fwd_kernel(const T* qkv, T* out, float* lse2, int S, int H, int d,
                                                        float scale_log2, DropArgs drop) {
   constexpr int V = Vec<T>::V;
@@ -107,7 +107,7 @@ __global__ void __launch_bounds__(NT) attn_fwd_kernel(const T* qkv, T* out, floa
     rs = group4_sum(rs);
     l_run = l_run * alpha + rs;
     m_run = m_new;
-    if (drop.thr) {   // dropout: the product uses P * keep * scale, the normalizer all of P
+    if constexpr (DROP) {   // dropout: the product uses P * keep * scale, the normalizer all of P
 #pragma unroll
       for (int kt = 0; kt < BKV / 16; ++kt) {
         const uint32_t bits = drop_row4(drop, bh, qrow, k0 + kt * 16 + 4 * (l >> 4));
@@ -207,7 +207,7 @@ template <int DH> struct FwdRing {
   static constexpr int L = 2 * BLK / NTF;       // loads per thread per stage (K and V)
 };
 
-template <int DH>
+template <int DH, bool DROP>
 __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(const bf16* qkv, bf16* out, float* lse2, int S, int H,
                                                                int d, float scale_log2, DropArgs drop) {
   using C = FwdRing<DH>;
@@ -310,7 +310,7 @@ __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(cons
         }
       l_run[qs] = l_run[qs] * alpha + group4_sum(rs);
       m_run[qs] = m_new;
-      if (drop.thr) {   // dropout: the product uses P * keep * scale, the normalizer all of P
+      if constexpr (DROP) {   // dropout: the product uses P * keep * scale, the normalizer all of P
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt) {
           const uint32_t bits = drop_row4(drop, bh, qrow, k0 + kt * 16 + 4 * g);
@@ -377,7 +377,7 @@ __global__ void __launch_bounds__(NT) attn_dsum_kernel(const T* o, const T* dO, 
 }
 
 // ---------------------------------------------------------------------------------------
-template <typename T, int DH>
+template <typename T, int DH, bool DROP>
 __global__ void __launch_bounds__(NT) attn_bwd_dkdv_kernel(const T* qkv, const T* dO, const float* lse2,
                                                             const float* Dsum, T* dqkv, int S, int H, int d,
                                                             float scale_log2, float scale, DropArgs drop) {
@@ -437,7 +437,7 @@ __global__ void __launch_bounds__(NT) attn_bwd_dkdv_kernel(const T* qkv, const T
         mma_step<T>(s, lds_frag<BQ>(sQ, st, qt * 16), kf[st]);
         mma_step<T>(dp, lds_frag<BQ>(sdO, st, qt * 16), vf[st]);
       }
-      const uint32_t bits = drop.thr ? drop_col4(drop, bh, q0 + qt * 16 + 4 * (l >> 4), key) : 0xfu;
+      const uint32_t bits = DROP ? drop_col4(drop, bh, q0 + qt * 16 + 4 * (l >> 4), key) : 0xfu;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int qi = qt * 16 + 4 * (l >> 4) + r;
@@ -445,7 +445,7 @@ __global__ void __launch_bounds__(NT) attn_bwd_dkdv_kernel(const T* qkv, const T
         const bool ok = (key <= q) && (q < S) && (key < S);
         const float p = ok ? exp2f(s[r] * scale_log2 - sL[qi]) : 0.f;
         // dropout M = keep * scale: dV takes P M, dP = (dO V^T) M
-        const float mk = drop.thr ? (((bits >> r) & 1) ? drop.scale : 0.f) : 1.f;
+        const float mk = DROP ? (((bits >> r) & 1) ? drop.scale : 0.f) : 1.f;
         P[qt][r] = p * mk;
         dS[qt][r] = p * (dp[r] * mk - sD[qi]);
       }
@@ -475,7 +475,7 @@ __global__ void __launch_bounds__(NT) attn_bwd_dkdv_kernel(const T* qkv, const T
   }
 }
 
-template <typename T, int DH>
+template <typename T, int DH, bool DROP>
 __global__ void __launch_bounds__(NT) attn_bwd_dq_kernel(const T* qkv, const T* dO, const float* lse2,
                                                           const float* Dsum, T* dqkv, int S, int H, int d,
                                                           float scale_log2, float scale, DropArgs drop) {
@@ -531,13 +531,13 @@ __global__ void __launch_bounds__(NT) attn_bwd_dq_kernel(const T* qkv, const T* 
         mma_step<T>(s, lds_frag<BKV>(sK, st, kt * 16), qf[st]);
         mma_step<T>(dp, lds_frag<BKV>(sV, st, kt * 16), gf[st]);
       }
-      const uint32_t bits = drop.thr ? drop_row4(drop, bh, qrow, k0 + kt * 16 + 4 * (l >> 4)) : 0xfu;
+      const uint32_t bits = DROP ? drop_row4(drop, bh, qrow, k0 + kt * 16 + 4 * (l >> 4)) : 0xfu;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int key = k0 + kt * 16 + 4 * (l >> 4) + r;
         const bool ok = qok && (key <= qrow) && (key < S);
         const float p = ok ? exp2f(s[r] * scale_log2 - lq) : 0.f;
-        const float mk = drop.thr ? (((bits >> r) & 1) ? drop.scale : 0.f) : 1.f;
+        const float mk = DROP ? (((bits >> r) & 1) ? drop.scale : 0.f) : 1.f;
         dS[kt][r] = p * (dp[r] * mk - Dq);
       }
     }
@@ -642,7 +642,7 @@ __device__ __forceinline__ void colsum_tiles(float (&v)[NCOL / 16][4], float* re
   }
 }
 
-template <int DH>
+template <int DH, bool DROP>
 __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn_dkdv_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
                                                                 bf16* dqkv, int S, int S_pad, int H, int d,
                                                                 float scale_log2, float scale, float* gbias,
@@ -728,7 +728,7 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
       // P = 2^(s * scale * log2 e - lse2), dS = P (dP - D); masked entries get P = 0.
       // Dropout M = keep * scale: dV takes P M, and dP = (dO V^T) M.
       uint32_t dbits[2][SUB];
-      if (drop.thr) {
+      if constexpr (DROP) {
 #pragma unroll
         for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -750,7 +750,7 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
                 x = (key <= q0 + qi && q0 + qi < S && key < S) ? x : -INFINITY;
               }
               const float p = fast_exp2(x);
-              if (drop.thr) {
+              if constexpr (DROP) {
                 const float mk = ((dbits[u][ks] >> r) & 1) ? drop.scale : 0.f;
                 sc[ks][u][r] = p * mk;
                 dp[ks][u][r] = p * (dp[ks][u][r] * mk - Dq);
@@ -817,7 +817,7 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
   }
 }
 
-template <int DH>
+template <int DH, bool DROP>
 __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn_dq_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
                                                               bf16* dqkv, int S, int S_pad, int H, int d,
                                                               float scale_log2, float scale, float* gbias,
@@ -909,7 +909,7 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
 #pragma unroll
           for (int u = 0; u < 2; ++u) {
             // dropout M = keep * scale on dP = dO V^T
-            const uint32_t bits = drop.thr ? drop_row4(drop, bh, q, k0 + (2 * s + u) * 16 + 4 * g) : 0xfu;
+            const uint32_t bits = DROP ? drop_row4(drop, bh, q, k0 + (2 * s + u) * 16 + 4 * g) : 0xfu;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               float x = fmaf(sc[qs][u][r], scale_log2, -lq[qs]);
@@ -918,7 +918,7 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
                 x = (key <= q && key < S && q < S) ? x : -INFINITY;
               }
               const float p = fast_exp2(x);
-              const float mk = drop.thr ? (((bits >> r) & 1) ? drop.scale : 0.f) : 1.f;
+              const float mk = DROP ? (((bits >> r) & 1) ? drop.scale : 0.f) : 1.f;
               dp[qs][u][r] = p * (dp[qs][u][r] * mk - Dq[qs]);
             }
           }
@@ -973,13 +973,21 @@ hipError_t fwd_launch(const void* qkv, void* o, float* lse2, int mu, int S, int 
   if constexpr (sizeof(T) == 2) {
     using C = FwdRing<DH>;
     dim3 grid(mu * H, (S + C::BQ - 1) / C::BQ);   // x fastest: every head's heaviest query block first
-    hipLaunchKernelGGL((attn_fwd_ring_kernel<DH>), grid, dim3(C::NTF), 0, st, reinterpret_cast<const bf16*>(qkv),
-                       reinterpret_cast<bf16*>(o), lse2, S, H, d, scale_log2, drop);
+    if (drop.thr)
+      hipLaunchKernelGGL((attn_fwd_ring_kernel<DH, true>), grid, dim3(C::NTF), 0, st,
+                         reinterpret_cast<const bf16*>(qkv), reinterpret_cast<bf16*>(o), lse2, S, H, d, scale_log2, drop);
+    else
+      hipLaunchKernelGGL((attn_fwd_ring_kernel<DH, false>), grid, dim3(C::NTF), 0, st,
+                         reinterpret_cast<const bf16*>(qkv), reinterpret_cast<bf16*>(o), lse2, S, H, d, scale_log2, drop);
     return hipGetLastError();
   }
   dim3 grid((S + 63) / 64, mu * H);
-  hipLaunchKernelGGL((attn_fwd_kernel<T, DH>), grid, dim3(NT), 0, st, reinterpret_cast<const T*>(qkv),
-                     reinterpret_cast<T*>(o), lse2, S, H, d, scale_log2, drop);
+  if (drop.thr)
+    hipLaunchKernelGGL((attn_fwd_kernel<T, DH, true>), grid, dim3(NT), 0, st, reinterpret_cast<const T*>(qkv),
+                       reinterpret_cast<T*>(o), lse2, S, H, d, scale_log2, drop);
+  else
+    hipLaunchKernelGGL((attn_fwd_kernel<T, DH, false>), grid, dim3(NT), 0, st, reinterpret_cast<const T*>(qkv),
+                       reinterpret_cast<T*>(o), lse2, S, H, d, scale_log2, drop);
   return hipGetLastError();
 }
 
@@ -1003,12 +1011,21 @@ hipError_t bwd_launch(const void* qkv, const void* o, const void* dO, const floa
                        reinterpret_cast<const bf16*>(o), g, lse2, Dbuf, S, S_pad, H, d, rows);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((attn_dkdv_ring_kernel<DH>), dim3(mu * H, (S + C::BR - 1) / C::BR), dim3(C::NTB), 0, st, q, g,
-                       Dbuf, dq, S, S_pad, H, d, scale_log2, scale, gbias, drop);
+    const dim3 grid(mu * H, (S + C::BR - 1) / C::BR);
+    if (drop.thr)
+      hipLaunchKernelGGL((attn_dkdv_ring_kernel<DH, true>), grid, dim3(C::NTB), 0, st, q, g, Dbuf, dq, S, S_pad, H, d,
+                         scale_log2, scale, gbias, drop);
+    else
+      hipLaunchKernelGGL((attn_dkdv_ring_kernel<DH, false>), grid, dim3(C::NTB), 0, st, q, g, Dbuf, dq, S, S_pad, H, d,
+                         scale_log2, scale, gbias, drop);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((attn_dq_ring_kernel<DH>), dim3(mu * H, (S + C::BR - 1) / C::BR), dim3(C::NTB), 0, st, q, g, Dbuf,
-                       dq, S, S_pad, H, d, scale_log2, scale, gbias, drop);
+    if (drop.thr)
+      hipLaunchKernelGGL((attn_dq_ring_kernel<DH, true>), grid, dim3(C::NTB), 0, st, q, g, Dbuf, dq, S, S_pad, H, d,
+                         scale_log2, scale, gbias, drop);
+    else
+      hipLaunchKernelGGL((attn_dq_ring_kernel<DH, false>), grid, dim3(C::NTB), 0, st, q, g, Dbuf, dq, S, S_pad, H, d,
+                         scale_log2, scale, gbias, drop);
     return hipGetLastError();
   }
   constexpr int LPR = DH / Vec<T>::V;
@@ -1018,12 +1035,14 @@ hipError_t bwd_launch(const void* qkv, const void* o, const void* dO, const floa
                      reinterpret_cast<const T*>(o), reinterpret_cast<const T*>(dO), Dbuf, S, H, d, rows);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, DH>), dim3((S + BKV - 1) / BKV, mu * H), dim3(NT), 0, st,
+  auto dkdv = drop.thr ? attn_bwd_dkdv_kernel<T, DH, true> : attn_bwd_dkdv_kernel<T, DH, false>;
+  hipLaunchKernelGGL(dkdv, dim3((S + BKV - 1) / BKV, mu * H), dim3(NT), 0, st,
                      reinterpret_cast<const T*>(qkv), reinterpret_cast<const T*>(dO), lse2, Dbuf,
                      reinterpret_cast<T*>(dqkv), S, H, d, scale_log2, scale, drop);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<T, DH>), dim3((S + 63) / 64, mu * H), dim3(NT), 0, st,
+  auto dqk = drop.thr ? attn_bwd_dq_kernel<T, DH, true> : attn_bwd_dq_kernel<T, DH, false>;
+  hipLaunchKernelGGL(dqk, dim3((S + 63) / 64, mu * H), dim3(NT), 0, st,
                      reinterpret_cast<const T*>(qkv), reinterpret_cast<const T*>(dO), lse2, Dbuf,
                      reinterpret_cast<T*>(dqkv), S, H, d, scale_log2, scale, drop);
   e = hipGetLastError();

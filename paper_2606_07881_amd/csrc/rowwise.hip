@@ -287,23 +287,61 @@ hipError_t layernorm_bwd(DType dt, const void* dn, const void* x, const float* m
 }
 
 namespace {
-// out = res + z * keep * scale, 8 consecutive elements per thread (one Philox draw).
-template <typename T>
-__global__ void __launch_bounds__(NT) dropout_kernel(const T* z, const T* res, T* out,
-                                                     int64_t n8, DropArgs drop) {
+// out = res + z * keep * scale, 8 consecutive elements per thread (one Philox
+// draw). VEC: every pointer is 16-byte aligned, so the 8 elements move as
+// 16-byte vectors (one for bf16, two for fp32).
+template <typename T, bool VEC>
+__global__ void __launch_bounds__(NT) dropout_kernel(const T* z, const T* res, T* out, int64_t n8, DropArgs drop) {
   const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
   if (i >= n8) return;
   const uint64_t e8 = (uint64_t)i * 8;
   const uint32_t bits = drop_elem8(drop, e8);
+  float zv[8], rv[8];
+  if constexpr (VEC) {
+    constexpr int NV = 8 * sizeof(T) / 16;   // 16-byte vectors per 8 elements
+#pragma unroll
+    for (int q = 0; q < NV; ++q) {
+      const u32x4 a = ld16(z + e8 + q * (16 / sizeof(T)));
+      const u32x4 b = res != nullptr ? ld16(res + e8 + q * (16 / sizeof(T))) : u32x4{0, 0, 0, 0};
+#pragma unroll
+      for (int j = 0; j < 16 / (int)sizeof(T); ++j) {
+        zv[q * (16 / sizeof(T)) + j] = vget<T>(a, j);
+        rv[q * (16 / sizeof(T)) + j] = vget<T>(b, j);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      zv[j] = to_f32(z[e8 + j]);
+      rv[j] = res != nullptr ? to_f32(res[e8 + j]) : 0.f;
+    }
+  }
   float v[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    float x = ((bits >> j) & 1) ? to_f32(z[e8 + j]) * drop.scale : 0.f;
-    if (res != nullptr) x += to_f32(res[e8 + j]);
-    v[j] = x;
-  }
+  for (int j = 0; j < 8; ++j) v[j] = (((bits >> j) & 1) ? zv[j] * drop.scale : 0.f) + rv[j];
+  if constexpr (VEC && sizeof(T) == 2) {
+    st16(out + e8, u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                         pack_bf16x2(v[6], v[7])});
+  } else if constexpr (VEC) {
+    st16(out + e8, __builtin_bit_cast(u32x4, floatx4{v[0], v[1], v[2], v[3]}));
+    st16(out + e8 + 4, __builtin_bit_cast(u32x4, floatx4{v[4], v[5], v[6], v[7]}));
+  } else {
 #pragma unroll
-  for (int j = 0; j < 8; ++j) out[e8 + j] = from_f32<T>(v[j]);
+    for (int j = 0; j < 8; ++j) out[e8 + j] = from_f32<T>(v[j]);
+  }
+}
+
+template <typename T>
+void launch_dropout(const void* z, const void* res, void* out, int64_t n8, const DropArgs& drop, hipStream_t st) {
+  auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+  const dim3 grid((unsigned)((n8 + NT - 1) / NT));
+  const T* zt = reinterpret_cast<const T*>(z);
+  const T* rt = reinterpret_cast<const T*>(res);
+  T* ot = reinterpret_cast<T*>(out);
+  if (al16(z) && al16(out) && (res == nullptr || al16(res)))
+    hipLaunchKernelGGL((dropout_kernel<T, true>), grid, dim3(NT), 0, st, zt, rt, ot, n8, drop);
+  else
+    hipLaunchKernelGGL((dropout_kernel<T, false>), grid, dim3(NT), 0, st, zt, rt, ot, n8, drop);
 }
 }  // namespace
 
@@ -311,13 +349,8 @@ hipError_t dropout_fwd(DType dt, const void* z, const void* res, void* out, int 
                        hipStream_t st) {
   if (rows <= 0 || cols <= 0 || cols % 8 || drop.thr == 0) return hipErrorInvalidValue;
   const int64_t n8 = (int64_t)rows * cols / 8;
-  const dim3 grid((unsigned)((n8 + NT - 1) / NT));
-  if (dt == DT_BF16)
-    hipLaunchKernelGGL(dropout_kernel<bf16>, grid, dim3(NT), 0, st, reinterpret_cast<const bf16*>(z),
-                       reinterpret_cast<const bf16*>(res), reinterpret_cast<bf16*>(out), n8, drop);
-  else
-    hipLaunchKernelGGL(dropout_kernel<float>, grid, dim3(NT), 0, st, reinterpret_cast<const float*>(z),
-                       reinterpret_cast<const float*>(res), reinterpret_cast<float*>(out), n8, drop);
+  if (dt == DT_BF16) launch_dropout<bf16>(z, res, out, n8, drop, st);
+  else launch_dropout<float>(z, res, out, n8, drop, st);
   return hipGetLastError();
 }
 
