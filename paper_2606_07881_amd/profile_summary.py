@@ -37,7 +37,7 @@ FAMILIES = {
     "layernorm_fwd": ["ln_fwd_kernel"],
     "layernorm_bwd": ["ln_bwd_kernel", "colsum_atomic_kernel<bool _Accum, bool, E>"],
     "bias_grad": ["colsum_atomic_kernelIDF16bLb0E"],
-    "adamw": ["adamw_kernel"],
+    "adamw": ["adamw_kernel", "guard_kernel", "ctl_kernel", "transpose16_kernel"],
 }
 # families whose launch runs each of its kernels once; every other family runs
 # one of its kernels (an epilogue or shape variant) per launch
