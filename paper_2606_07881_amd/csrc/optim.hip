@@ -27,9 +27,9 @@ __device__ double lr_at(const AdamwArgs& a, int t) {
 }
 
 __global__ void __launch_bounds__(NT) adamw_kernel(float* __restrict__ theta, float* __restrict__ G,
-                                                    float* __restrict__ m, float* __restrict__ v, bf16* theta16,
-                                                    const int4* __restrict__ chunks, AdamwArgs a,
-                                                    const int* __restrict__ ctl) {
+                                                    float* __restrict__ m, float* __restrict__ v,
+                                                    bf16* __restrict__ theta16, const int4* __restrict__ chunks,
+                                                    AdamwArgs a, const int* __restrict__ ctl) {
   const int4 ch = chunks[blockIdx.x];
   if (ctl[0] != 0) {   // non-finite G: no update, G cleared
     for (int64_t i = (int64_t)ch.x + 4 * (int64_t)threadIdx.x; i < ch.y; i += 4 * NT)
@@ -43,11 +43,7 @@ __global__ void __launch_bounds__(NT) adamw_kernel(float* __restrict__ theta, fl
   const float decay = ch.z ? (1.f - lr * a.weight_decay) : 1.f;
   const float step = lr / bc1;
   const float rbc2 = 1.f / sqrtf(bc2);
-  for (int64_t i = (int64_t)ch.x + 4 * (int64_t)threadIdx.x; i < ch.y; i += 4 * NT) {
-    const floatx4 g = *reinterpret_cast<const floatx4*>(G + i);
-    floatx4 th = *reinterpret_cast<const floatx4*>(theta + i);
-    floatx4 mm = *reinterpret_cast<const floatx4*>(m + i);
-    floatx4 vv = *reinterpret_cast<const floatx4*>(v + i);
+  auto update = [&](int64_t i, floatx4 g, floatx4 th, floatx4 mm, floatx4 vv) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       mm[j] = a.beta1 * mm[j] + (1.f - a.beta1) * g[j];
@@ -60,7 +56,21 @@ __global__ void __launch_bounds__(NT) adamw_kernel(float* __restrict__ theta, fl
     *reinterpret_cast<floatx4*>(v + i) = vv;
     *reinterpret_cast<floatx4*>(G + i) = floatx4{0.f, 0.f, 0.f, 0.f};
     if (theta16) *reinterpret_cast<u32x2*>(theta16 + i) = u32x2{pack_bf16x2(th[0], th[1]), pack_bf16x2(th[2], th[3])};
+  };
+  // two vectors per operand in flight per thread (the second one 4 NT elements on)
+  int64_t i = (int64_t)ch.x + 4 * (int64_t)threadIdx.x;
+  for (; i + 4 * NT < ch.y; i += 8 * NT) {
+    const int64_t k = i + 4 * NT;
+    const floatx4 g0 = *reinterpret_cast<const floatx4*>(G + i), g1 = *reinterpret_cast<const floatx4*>(G + k);
+    const floatx4 t0 = *reinterpret_cast<const floatx4*>(theta + i), t1 = *reinterpret_cast<const floatx4*>(theta + k);
+    const floatx4 m0 = *reinterpret_cast<const floatx4*>(m + i), m1 = *reinterpret_cast<const floatx4*>(m + k);
+    const floatx4 v0 = *reinterpret_cast<const floatx4*>(v + i), v1 = *reinterpret_cast<const floatx4*>(v + k);
+    update(i, g0, t0, m0, v0);
+    update(k, g1, t1, m1, v1);
   }
+  if (i < ch.y)
+    update(i, *reinterpret_cast<const floatx4*>(G + i), *reinterpret_cast<const floatx4*>(theta + i),
+           *reinterpret_cast<const floatx4*>(m + i), *reinterpret_cast<const floatx4*>(v + i));
 }
 
 __global__ void __launch_bounds__(NT) f32_to_bf16_kernel(const float* __restrict__ src, bf16* dst, int64_t n) {

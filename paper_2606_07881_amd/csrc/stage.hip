@@ -307,7 +307,7 @@ struct Layout {
   size_t total;
 };
 
-constexpr int64_t CHUNK = 16384;  // AdamW elements per workgroup
+constexpr int64_t CHUNK = 4096;   // AdamW elements per workgroup (many small workgroups: a short last round)
 
 // Dropout: a 16-bit Philox value v keeps its element when v >= thr (0: off)
 uint32_t drop_threshold(const paci_shapes& s) { return (uint32_t)std::floor((double)s.dropout * 65536.0 + 0.5); }
