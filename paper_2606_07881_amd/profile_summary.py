@@ -113,6 +113,48 @@ def traffic(fetch_csv, write_csv, copy_bytes=COPY_BYTES):
     return "\n".join(lines), record
 
 
+SIMD_NUM = 256 * 4   # MI355X: 256 CUs of 4 SIMDs
+XCC_NUM = 8          # GRBM_GUI_ACTIVE comes summed over the 8 XCDs (each counts the same cycles)
+
+
+def mfma(counters_csv):
+    """Per-kernel MFMA busy fraction SQ_VALU_MFMA_BUSY_CYCLES (summed over
+    SIMDs) / (GPU-active cycles x SIMD_NUM), GPU-active cycles being
+    GRBM_GUI_ACTIVE / XCC_NUM; the executed bf16 MFMA FLOP
+    (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) and their rate against the dense
+    peak of 1024 FLOP per SIMD and cycle; and the same per family (summed
+    over its dispatches). Returns markdown."""
+    rows = collections.defaultdict(lambda: collections.defaultdict(list))
+    for r in csv.DictReader(open(counters_csv)):
+        rows[r["Kernel_Name"]][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    need = ("SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE", "SQ_INSTS_VALU_MFMA_MOPS_BF16")
+    fam_busy, fam_active, fam_flop = (collections.defaultdict(float) for _ in range(3))
+    lines = ["| kernel | family | dispatches | MFMA busy % | bf16 MFMA GFLOP / dispatch | GPU-active kcycles / dispatch |",
+             "|---|---|---|---|---|---|"]
+    order = sorted(rows, key=lambda k: -sum(rows[k].get("GRBM_GUI_ACTIVE", [0.0])))
+    for k in order:
+        c = rows[k]
+        if any(n not in c for n in need):
+            continue
+        n = len(c["GRBM_GUI_ACTIVE"])
+        busy, active, mops = sum(c[need[0]]), sum(c[need[1]]) / XCC_NUM, sum(c[need[2]])
+        if mops == 0:
+            continue
+        fam = family_of(k)
+        if fam:
+            fam_busy[fam] += busy
+            fam_active[fam] += active
+            fam_flop[fam] += mops * 512
+        lines.append(f"| `{k.replace('|', '/')[:100]}` | {fam or '-'} | {n} | {100 * busy / (active * SIMD_NUM):.1f} | "
+                     f"{mops * 512 / n / 1e9:.1f} | {active / n / 1e3:.0f} |")
+    lines += ["", "| family | MFMA busy % | executed bf16 MFMA FLOP per GPU-active cycle, fraction of the dense peak |",
+              "|---|---|---|"]
+    for fam in sorted(fam_busy, key=lambda f: -fam_active[f]):
+        lines.append(f"| {fam} | {100 * fam_busy[fam] / (fam_active[fam] * SIMD_NUM):.1f} | "
+                     f"{fam_flop[fam] / (fam_active[fam] * SIMD_NUM * 1024) * 100:.1f}% |")
+    return "\n".join(lines)
+
+
 def read_record(md_path):
     """The traffic record line of a committed summary, or None."""
     try:
@@ -128,6 +170,8 @@ def read_record(md_path):
 if __name__ == "__main__":
     if len(sys.argv) >= 3 and sys.argv[1] == "kernels":
         print(kernels_md(sys.argv[2]))
+    elif len(sys.argv) >= 3 and sys.argv[1] == "mfma":
+        print(mfma(sys.argv[2]))
     elif len(sys.argv) >= 4 and sys.argv[1] == "traffic":
         md, rec = traffic(sys.argv[2], sys.argv[3], float(sys.argv[4]) if len(sys.argv) > 4 else COPY_BYTES)
         print(md)
