@@ -43,6 +43,10 @@ __global__ void __launch_bounds__(NT) adamw_kernel(float* __restrict__ theta, fl
   const float decay = ch.z ? (1.f - lr * a.weight_decay) : 1.f;
   const float step = lr / bc1;
   const float rbc2 = 1.f / sqrtf(bc2);
+  // every element is touched once: non-temporal loads and stores keep the
+  // stream from displacing cached data
+  auto ld = [](const float* p) { return __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(p)); };
+  auto st = [](float* p, floatx4 x) { __builtin_nontemporal_store(x, reinterpret_cast<floatx4*>(p)); };
   auto update = [&](int64_t i, floatx4 g, floatx4 th, floatx4 mm, floatx4 vv) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -51,26 +55,26 @@ __global__ void __launch_bounds__(NT) adamw_kernel(float* __restrict__ theta, fl
       const float denom = sqrtf(vv[j]) * rbc2 + a.eps;
       th[j] = th[j] * decay - step * mm[j] / denom;
     }
-    *reinterpret_cast<floatx4*>(theta + i) = th;
-    *reinterpret_cast<floatx4*>(m + i) = mm;
-    *reinterpret_cast<floatx4*>(v + i) = vv;
-    *reinterpret_cast<floatx4*>(G + i) = floatx4{0.f, 0.f, 0.f, 0.f};
-    if (theta16) *reinterpret_cast<u32x2*>(theta16 + i) = u32x2{pack_bf16x2(th[0], th[1]), pack_bf16x2(th[2], th[3])};
+    st(theta + i, th);
+    st(m + i, mm);
+    st(v + i, vv);
+    st(G + i, floatx4{0.f, 0.f, 0.f, 0.f});
+    if (theta16)
+      __builtin_nontemporal_store(u32x2{pack_bf16x2(th[0], th[1]), pack_bf16x2(th[2], th[3])},
+                                  reinterpret_cast<u32x2*>(theta16 + i));
   };
   // two vectors per operand in flight per thread (the second one 4 NT elements on)
   int64_t i = (int64_t)ch.x + 4 * (int64_t)threadIdx.x;
   for (; i + 4 * NT < ch.y; i += 8 * NT) {
     const int64_t k = i + 4 * NT;
-    const floatx4 g0 = *reinterpret_cast<const floatx4*>(G + i), g1 = *reinterpret_cast<const floatx4*>(G + k);
-    const floatx4 t0 = *reinterpret_cast<const floatx4*>(theta + i), t1 = *reinterpret_cast<const floatx4*>(theta + k);
-    const floatx4 m0 = *reinterpret_cast<const floatx4*>(m + i), m1 = *reinterpret_cast<const floatx4*>(m + k);
-    const floatx4 v0 = *reinterpret_cast<const floatx4*>(v + i), v1 = *reinterpret_cast<const floatx4*>(v + k);
+    const floatx4 g0 = ld(G + i), g1 = ld(G + k);
+    const floatx4 t0 = ld(theta + i), t1 = ld(theta + k);
+    const floatx4 m0 = ld(m + i), m1 = ld(m + k);
+    const floatx4 v0 = ld(v + i), v1 = ld(v + k);
     update(i, g0, t0, m0, v0);
     update(k, g1, t1, m1, v1);
   }
-  if (i < ch.y)
-    update(i, *reinterpret_cast<const floatx4*>(G + i), *reinterpret_cast<const floatx4*>(theta + i),
-           *reinterpret_cast<const floatx4*>(m + i), *reinterpret_cast<const floatx4*>(v + i));
+  if (i < ch.y) update(i, ld(G + i), ld(theta + i), ld(m + i), ld(v + i));
 }
 
 __global__ void __launch_bounds__(NT) f32_to_bf16_kernel(const float* __restrict__ src, bf16* dst, int64_t n) {
