@@ -267,7 +267,10 @@ int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, const int32_t* 
  * used). Host arrays. The list is checked first (kinds in {0, 1, 2}, idx >= 0
  * for forwards and backwards: else E_INVAL and nothing runs); each event then
  * goes through the protocol, and the first error is returned with the events
- * before it done. The handle must be fresh, as for paci_stage_run. */
+ * before it done. Micro-batch indices are absolute: the handle may be in any
+ * state the list continues (e.g. after paci_stage_resume), and the buffers are
+ * indexed by them. host_stamps[3 i + 2] (Delta) is valid for micro-batches whose
+ * forward ran in the same call. */
 int paci_stage_run_events(paci_stage* h, int n, const int32_t* kinds, const int32_t* idx,
                           const void* dev_in_all, const int32_t* dev_targets_all,
                           const void* dev_grad_out_all, void* dev_out_all, void* dev_grad_in_all,
@@ -278,6 +281,17 @@ int paci_stage_run_events(paci_stage* h, int n, const int32_t* kinds, const int3
  * windowed weight gradients are added to G first); used to replay again from
  * the current state. */
 int paci_stage_reset_counters(paci_stage* h);
+
+/* Checkpoint / resume. A checkpoint of a drained stage (q = 0, c = 0) is
+ * PARAMS, EXP_AVG and EXP_AVG_SQ (paci_stage_read), its counters and its
+ * update counts (paci_stage_updates). To resume, load the three arrays into a
+ * stage of the same shapes, K and delay, then call paci_stage_resume: it sets
+ * the version t, the index of the next micro-batch (next_f = next_b; dropout
+ * masks are keyed by it) and the applied / skipped update counts (AdamW's bias
+ * correction and the rate schedule continue from applied + 1). Synchronizes
+ * the stream. Errors: E_INVAL (a negative value), E_ORDER (micro-batches in
+ * flight or a window partly accumulated; nothing changes), E_HIP. */
+int paci_stage_resume(paci_stage* h, int32_t version, int32_t next_mb, int32_t applied, int32_t skipped);
 
 /* Number of updates paci_stage_step applied and skipped (non-finite G) since
  * creation or the last paci_stage_reset_counters, which clears both.

@@ -90,6 +90,7 @@ def _load():
         "paci_stage_run_events": (I, [P, I, I32P, I32P, P, P, P, P, P, I32P]),
         "paci_stage_reset_counters": (I, [P]),
         "paci_stage_updates": (I, [P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
+        "paci_stage_resume": (I, [P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
         "paci_stage_counters": (I, [P, ctypes.POINTER(PaciCounters)]),
         "paci_stage_sync": (I, [P]),
         "paci_last_hip_error": (I, [P]),
@@ -346,6 +347,10 @@ class Stage:
 
     def reset_counters(self):
         _check(lib.paci_stage_reset_counters(self.h), "paci_stage_reset_counters")
+
+    def resume(self, version, next_mb, applied, skipped=0):
+        """paci_stage_resume: continue a checkpoint of a drained stage."""
+        _check(lib.paci_stage_resume(self.h, version, next_mb, applied, skipped), "paci_stage_resume")
 
     def updates(self):
         """(applied, skipped): updates the step applied and skipped (non-finite G)."""

@@ -1172,7 +1172,6 @@ extern "C" int paci_stage_run_events(paci_stage* h, int n, const int32_t* kinds,
   const paci_shapes& s = h->s;
   if (s.kind == PACI_LAST && !dev_targets_all) return PACI_E_INVAL;
   if (s.kind != PACI_LAST && !dev_grad_out_all) return PACI_E_INVAL;
-  if (h->fsm.next_f != 0 || h->fsm.next_b != 0 || h->fsm.c != 0) return PACI_E_ORDER;
   const int64_t T = h->L.T;
   const size_t act = act_bytes(h);
   const size_t in_stride = s.kind == PACI_FIRST ? 4 * (size_t)T : act;
@@ -1216,6 +1215,7 @@ extern "C" int paci_stage_run(paci_stage* h, int M, const void* dev_in_all, cons
                               const void* dev_grad_out_all, void* dev_out_all, void* dev_grad_in_all,
                               int32_t* host_stamps) {
   if (!h || M < 0) return PACI_E_INVAL;
+  if (h->fsm.next_f != 0 || h->fsm.next_b != 0 || h->fsm.c != 0) return PACI_E_ORDER;   // a fresh replay
   std::vector<int32_t> kinds(2 * (size_t)M + M / h->fsm.K + 1), idx(kinds.size());
   int n = 0;
   const int r = paci_schedule(M, h->fsm.K, h->fsm.delay, kinds.data(), idx.data(), (int)kinds.size(), &n);
@@ -1236,6 +1236,24 @@ extern "C" int paci_stage_updates(paci_stage* h, int32_t* applied, int32_t* skip
   }
   *applied = ctl[1];
   *skipped = ctl[2];
+  return PACI_OK;
+}
+
+extern "C" int paci_stage_resume(paci_stage* h, int32_t version, int32_t next_mb, int32_t applied,
+                                 int32_t skipped) {
+  if (!h || version < 0 || next_mb < 0 || applied < 0 || skipped < 0) return PACI_E_INVAL;
+  if (h->broken) return PACI_E_HIP;
+  if (h->fsm.q != 0 || h->fsm.c != 0 || h->fsm.next_f != h->fsm.next_b) return PACI_E_ORDER;   // drained only
+  const int ctl[4] = {0, applied, skipped, 0};
+  hipError_t e = hipMemcpyAsync(h->arena + h->L.ctl, ctl, sizeof(ctl), hipMemcpyHostToDevice, h->st);
+  if (e == hipSuccess) e = hipStreamSynchronize(h->st);
+  if (e != hipSuccess) {
+    h->last_hip = (int)e;
+    return PACI_E_HIP;
+  }
+  h->fsm.t = version;
+  h->fsm.next_f = h->fsm.next_b = next_mb;
+  h->win_done = 0;
   return PACI_OK;
 }
 

@@ -324,3 +324,60 @@ def test_trailing_partial_window(binding, name):
     for n, ref in o["stage"].G.items():
         e = rel_err(G[n], ref)
         assert e <= tg, f"pending G[{n}]: {e:.3e}"
+
+
+@pytest.mark.parametrize("name", ["drop_ragged_fp32", "win_bf16"])
+def test_checkpoint_resume_continues_the_run(binding, name):
+    """A drained stage saved (parameters, moments, counters, update counts) and
+    restored into a fresh stage with paci_stage_resume continues as the
+    original: the same stamps and update counts, and the same parameters up to
+    the run-to-run spread of fp32 atomic sums (dropout masks follow the
+    micro-batch index, the AdamW step count follows the applied updates)."""
+    import torch
+    c = small_cfg(name)
+    K, delay = c["K"], c["delay"]
+    M1, M2 = 2 * K, K
+    inp = Inputs(c, 8, M1 + M2)
+    x_all = torch.stack([to_torch(a) for a in inp.x_dev])
+    dy_all = torch.stack([to_torch(a) for a in inp.dy_dev])
+    kinds, idx = binding.schedule(M2, K, delay)
+    idx = np.where(kinds < 2, idx + M1, idx).astype(np.int32)   # micro-batches M1 .. M1 + M2 - 1
+
+    a = binding.Stage(c, K, delay)
+    a.load_params(inp.params)
+    a.run(M1, x_all, dy_all)
+    ck = {w: a.read(w) for w in (binding.PARAMS, binding.EXP_AVG, binding.EXP_AVG_SQ)}
+    cnt, upd = a.counters(), a.updates()
+    assert cnt["q"] == 0 and cnt["c"] == 0 and cnt["version"] == M1 // K and upd == (M1 // K, 0)
+    st_a = a.run_events(kinds, idx, x_all, dy_all)
+
+    b = binding.Stage(c, K, delay)
+    for w, arr in ck.items():
+        b.load(w, arr)
+    b.resume(cnt["version"], cnt["next_f"], *upd)
+    st_b = b.run_events(kinds, idx, x_all, dy_all)
+    assert np.array_equal(st_a[M1:], st_b[M1:])
+    assert a.counters() == b.counters() and a.updates() == b.updates() == ((M1 + M2) // K, 0)
+    th_a, th_b = a.read(binding.PARAMS).astype(np.float64), b.read(binding.PARAMS).astype(np.float64)
+    # where rounding flips the sign of a near-zero G element, AdamW moves it by up to 2 lr
+    d_ab = np.abs(th_a - th_b)
+    assert d_ab.max() <= 2 * c["lr"] * (M2 // K) + 1e-6
+    # AdamW's step count went on: resuming at step 1 instead changes the
+    # update of every parameter (bias correction 1 - beta^1 against 1 - beta^3)
+    cfresh = binding.Stage(c, K, delay)
+    for w, arr in ck.items():
+        cfresh.load(w, arr)
+    cfresh.resume(cnt["version"], cnt["next_f"], 0, 0)
+    cfresh.run_events(kinds, idx, x_all, dy_all)
+    d_ac = np.abs(cfresh.read(binding.PARAMS).astype(np.float64) - th_a)
+    print(name, f"resume vs run: mean |dtheta| {d_ab.mean():.2e}; wrong step count: {d_ac.mean():.2e}", flush=True)
+    assert d_ac.mean() > 20 * d_ab.mean() + 1e-6
+    # resuming is refused while micro-batches are in flight
+    with pytest.raises(binding.PaciError) as ei:
+        d = binding.Stage(c, K, delay)
+        d.load_params(inp.params)
+        d.forward(0, x_all[0], torch.zeros_like(x_all[0]))
+        d.resume(0, 0, 0)
+    assert ei.value.code == binding.E_ORDER
+    for s in (a, b, cfresh, d):
+        s.close()
