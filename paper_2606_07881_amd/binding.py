@@ -18,7 +18,10 @@ import torch  # noqa: F401
 
 from . import inputs
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpaci_stage.so")
+# PACI_STAGE_LIB: another build of the same library (e.g. one with host-side
+# sanitizers for the host-only tests); the in-tree build otherwise
+LIB_PATH = os.environ.get("PACI_STAGE_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                             "libpaci_stage.so")
 HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "paci_stage.h")
 
 OK, STEP_DUE = 0, 1

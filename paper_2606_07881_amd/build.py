@@ -73,5 +73,38 @@ def build(verbose=False):
     return LIB
 
 
+SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined", "-Xarch_host",
+            "-fno-omit-frame-pointer"]
+
+
+def build_host_sanitized(out_dir):
+    """The library with AddressSanitizer and UBSan on its host code only (device
+    code is built as usual), for the host-only tests:
+    LD_PRELOAD=<clang asan runtime> ASAN_OPTIONS=detect_leaks=0 PACI_STAGE_LIB=<out_dir>/libpaci_stage.so
+    python -m pytest tests/test_abi_host.py tests/test_planner_host.py"""
+    os.makedirs(out_dir, exist_ok=True)
+    flags = [f for f in FLAGS if f != "-O3"] + ["-O1", "-g"] + SANITIZE
+
+    def one(src):
+        obj = os.path.join(out_dir, os.path.splitext(src)[0] + ".o")
+        r = subprocess.run([hipcc()] + flags + ["-c", os.path.join(CSRC, src), "-o", obj], capture_output=True,
+                           text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")
+        return obj
+
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
+        objs = list(ex.map(one, SOURCES))
+    lib = os.path.join(out_dir, "libpaci_stage.so")
+    r = subprocess.run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC"] + SANITIZE[:4] + ["-o", lib] + objs,
+                       capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("link failed:\n" + r.stdout + r.stderr)
+    return lib
+
+
 if __name__ == "__main__":
-    print(build(verbose=True))
+    if len(sys.argv) == 3 and sys.argv[1] == "--host-sanitize":
+        print(build_host_sanitized(sys.argv[2]))
+    else:
+        print(build(verbose=True))
