@@ -118,7 +118,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one pipeline stage on one GPU; --gpus {args.gpus} is not supported "
-              "(stages on several GPUs exchange activations point to point and are outside this build)",
+              "(stages on several GPUs exchange activations point to point; this benchmark runs one stage)",
               file=sys.stderr)
         sys.exit(2)
 
