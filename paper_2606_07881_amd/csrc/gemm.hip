@@ -118,8 +118,8 @@ struct TileLoader {
   }
 };
 
-// tanh(z) = 1 - 2 / (exp(2z) + 1), exact in form and saturating to +-1.
-// tanh z = 1 - 2 / (e^(2z) + 1), with the hardware exp2 and reciprocal (about 1 ulp each)
+// tanh z = 1 - 2 / (e^(2z) + 1), saturating to +-1, with the hardware exp2 and
+// reciprocal (about 1 ulp each)
 __device__ __forceinline__ float tanh_f(float z) {
   return 1.0f - 2.0f * __builtin_amdgcn_rcpf(fast_exp2(2.8853900817779268f * z) + 1.0f);
 }
