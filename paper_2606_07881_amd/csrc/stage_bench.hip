@@ -15,7 +15,7 @@
 //
 // usage: stage_bench [--layers L] [--d D] [--heads H] [--ff F] [--seq S] [--mu U]
 //                    [--K K] [--delay N] [--M M] [--steps n] [--warmup n] [--fp32] [--timing]
-//                    [--copy-probe]
+//                    [--copy-probe] [--hbm-probe]
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -76,6 +76,14 @@ __global__ void fill_normal(void* p, int64_t n, uint64_t seed, float std, int bf
 __global__ void copy16(const uint4* src, uint4* dst, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
     dst[i] = src[i];
+}
+// the same copy with non-temporal loads and stores (each byte is touched once)
+typedef unsigned int u32v4 __attribute__((ext_vector_type(4)));
+__global__ void copy16_nt(const uint4* src, uint4* dst, int64_t n) {
+  const u32v4* s = reinterpret_cast<const u32v4*>(src);
+  u32v4* d = reinterpret_cast<u32v4*>(dst);
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
 }
 
 __global__ void fill_const(float* p, int64_t n, float v) {
@@ -177,6 +185,39 @@ int main(int argc, char** argv) {
     CHECK_HIP(hipFree(b));
     printf("stage_bench: copy probe done (3 x 256 MiB, kernel copy16)\n");
     fflush(stdout);
+  }
+
+  if (arg_flag(argc, argv, "--hbm-probe")) {   // attainable HBM bandwidth: copies of 1 GiB, timed
+    const int64_t n16 = (1ll << 30) / 16;
+    uint4 *a = nullptr, *b = nullptr;
+    CHECK_HIP(hipMalloc(&a, n16 * 16));
+    CHECK_HIP(hipMalloc(&b, n16 * 16));
+    CHECK_HIP(hipMemsetAsync(a, 0, n16 * 16, st));
+    hipEvent_t e0, e1;
+    CHECK_HIP(hipEventCreate(&e0));
+    CHECK_HIP(hipEventCreate(&e1));
+    for (int nt = 0; nt < 2; ++nt) {
+      for (int grid : {2048, 8192, 32768}) {
+        auto launch = [&] {
+          if (nt) hipLaunchKernelGGL(copy16_nt, dim3(grid), dim3(256), 0, st, a, b, n16);
+          else hipLaunchKernelGGL(copy16, dim3(grid), dim3(256), 0, st, a, b, n16);
+        };
+        launch();
+        CHECK_HIP(hipEventRecord(e0, st));
+        for (int i = 0; i < 10; ++i) launch();
+        CHECK_HIP(hipEventRecord(e1, st));
+        CHECK_HIP(hipEventSynchronize(e1));
+        float ms = 0.f;
+        CHECK_HIP(hipEventElapsedTime(&ms, e0, e1));
+        printf("stage_bench: hbm probe %s grid %5d: %.0f GB/s (1 GiB read + 1 GiB written per copy)\n",
+               nt ? "copy16_nt" : "copy16   ", grid, 10.0 * 2.0 * n16 * 16 / (ms * 1e-3) / 1e9);
+      }
+    }
+    fflush(stdout);
+    CHECK_HIP(hipEventDestroy(e0));
+    CHECK_HIP(hipEventDestroy(e1));
+    CHECK_HIP(hipFree(a));
+    CHECK_HIP(hipFree(b));
   }
 
   std::vector<int32_t> stamps((size_t)M * 3);
