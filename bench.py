@@ -112,6 +112,9 @@ def main():
     ap.add_argument("--dropout", type=float, default=0.0,
                     help="dropout rate at the embedding, attention-probability and residual-branch sites "
                          "(the paper trains with 0.1; the headline workload has none)")
+    ap.add_argument("--micro-batch", type=int, default=0,
+                    help="sequences per micro-batch instead of the workload's (the paper trains with 16 or 32)")
+    ap.add_argument("--K", type=int, default=0, help="accumulation factor instead of the workload's")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy a 256 MiB device buffer 3 times (a kernel of known traffic, for scaling "
                          "hardware byte counters)")
@@ -134,6 +137,10 @@ def main():
     if args.dropout > 0:
         over["dropout"] = args.dropout
         over["dropout_seed"] = 2606
+    if args.micro_batch > 0:
+        over["micro_batch"] = args.micro_batch
+    if args.K > 0:
+        over["K"] = args.K
     c = configs.get(name, **over)
     name = c["name"]
     M, K, delay = c["M"], c["K"], c["delay"]
