@@ -123,6 +123,9 @@ def small_cfg(name, **kw):
                            micro_batch=2, vocab=301, max_pos=64, K=2, delay=1, M=4, dtype="fp32"),
         "last_fp32": dict(kind="last", n_layers=1, d_model=64, n_heads=2, head_dim=32, d_ff=128, seq=40,
                           micro_batch=2, vocab=301, max_pos=64, K=2, delay=0, M=4, dtype="fp32"),
+        # a vocabulary smaller than one 64-column group of the fused head's statistics
+        "lastv_bf16": dict(kind="last", n_layers=1, d_model=128, n_heads=2, head_dim=64, d_ff=256, seq=72,
+                           micro_batch=2, vocab=37, max_pos=128, K=2, delay=0, M=4, dtype="bf16"),
     }[name]
     c = configs.get("tiny_fp32")
     c.update(vocab=0, max_pos=0)

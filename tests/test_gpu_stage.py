@@ -74,7 +74,7 @@ def test_first_forward_backward(binding, name):
                                   "drop_tiny_fp32", "drop_ragged_bf16", "drop_ragged_fp32", "drop_win_bf16",
                                   "drop_dh128_bf16", "drop_dh32_bf16", "drop_first_bf16", "drop_last_bf16",
                                   "drop_first_fp32", "drop_last_fp32", "ckpt_drop_ragged_bf16",
-                                  "drop_fused_last_bf16"])
+                                  "drop_fused_last_bf16", "lastv_bf16", "fused_lastv_bf16"])
 def test_replay_parity(binding, name):
     """The whole asynchronous 1F1B replay: stamps bit-exact, every output, input
     gradient, accumulated G and the state after every AdamW update."""
