@@ -202,11 +202,18 @@ template <int DH> struct FwdRing {
   static constexpr int CPR = DH / 8, KS = DH / 32;
   static constexpr int QS = DH == 32 ? 4 : (DH == 64 ? 2 : 1), WAVES = DH == 32 ? 4 : 8, NTF = 64 * WAVES;
   static constexpr int WQ = 16 * QS, BQ = WAVES * WQ;
-  static constexpr int NS = DH <= 64 ? 3 : 2;
+  // blocks kb (V) and kb + 1 (K) are read in the same iteration, kb + 2 loads
+  static constexpr int NS = 4;
   static constexpr int BLK = 64 * CPR;          // 16-byte slots per block
   static constexpr int L = 2 * BLK / NTF;       // loads per thread per stage (K and V)
 };
 
+// The key loop is software-pipelined: while a wavefront runs the online
+// softmax of key block kb on its vector ALUs, the MFMAs of the scores of block
+// kb + 1 are interleaved with it, so the matrix unit is not idle during the
+// exponentials. A wavefront's queries start at a multiple of 16 * QS, which
+// divides 64, so every key block before its last one ends before its first
+// query and inside the sequence: only the last block is masked.
 template <int DH, bool DROP>
 __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(const bf16* qkv, bf16* out, float* lse2, int S, int H,
                                                                int d, float scale_log2, DropArgs drop) {
@@ -251,20 +258,9 @@ __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(cons
     blk_fill<CPR, C::NTF>(Kp + (int64_t)k0 * ld, ld, S - k0, st, wu, l);
     blk_fill<CPR, C::NTF>(Vp + (int64_t)k0 * ld, ld, S - k0, st + C::BLK * 16, wu, l);
   };
-#pragma unroll
-  for (int t = 0; t < NS - 1; ++t)
-    if (t < nkb) fill(t);
-  for (int kb = 0; kb < nkb; ++kb) {
-    wait_loads<C::L, NS - 2>(min(nkb - 1, kb + NS - 2) - kb);
-    wait_lds_reads();
-    barrier_no_fence();
-    if (kb + NS - 1 < nkb) fill(kb + NS - 1);   // into the stage of block kb - 1, read by now
-    if (kb > my_last) continue;
+  // raw scores q k^T of key block kb
+  auto scores = [&](int kb, floatx4 (&sc)[QS][4]) {
     const u32x4* sK = ring + (kb % NS) * 2 * C::BLK;
-    const u32x4* sV = sK + C::BLK;
-    const int k0 = kb * BKV;
-
-    floatx4 sc[QS][4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
       u32x4 kf[KS];
@@ -277,11 +273,15 @@ __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(cons
         for (int s = 0; s < KS; ++s) mma_step<bf16>(sc[qs][kt], kf[s], qf[qs][s]);
       }
     }
-    u32x4 pf[QS][2];
+  };
+  // online softmax of block kb's scores: running max and sum, rescaled
+  // accumulators, and the probabilities (dropped ones zeroed) as bf16 fragments
+  auto softmax = [&](auto masked, int kb, floatx4 (&sc)[QS][4], u32x4 (&pf)[QS][2]) {
+    const int k0 = kb * BKV;
 #pragma unroll
     for (int qs = 0; qs < QS; ++qs) {
       const int qrow = qw0 + 16 * qs + (l & 15);
-      if (k0 + BKV - 1 > qw0 + 16 * qs || k0 + BKV > S) {   // block crosses the diagonal or the end
+      if constexpr (decltype(masked)::value) {
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
@@ -323,6 +323,9 @@ __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(cons
       pf[qs][0] = acc_to_frag<bf16>(sc[qs], 0);
       pf[qs][1] = acc_to_frag<bf16>(sc[qs], 1);
     }
+  };
+  auto pv = [&](int kb, const u32x4 (&pf)[QS][2]) {
+    const u32x4* sV = ring + (kb % NS) * 2 * C::BLK + C::BLK;
 #pragma unroll
     for (int s = 0; s < 2; ++s)
 #pragma unroll
@@ -331,6 +334,46 @@ __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(cons
 #pragma unroll
         for (int qs = 0; qs < QS; ++qs) mma_step<bf16>(acc[qs][t], vf, pf[qs][s]);
       }
+  };
+  // iteration kb: blocks up to min(nkb - 1, kb + NS - 2) have been issued;
+  // wait for block kb + 1, whose keys this iteration reads, then refill the
+  // stage of block kb - 1, which every wavefront has finished with
+  auto step = [&](int kb, floatx4 (&cur)[QS][4], floatx4 (&nxt)[QS][4]) {
+    if (kb + 1 < nkb) wait_loads<C::L, NS - 2>(min(nkb - 1, kb + NS - 2) - (kb + 1));
+    wait_lds_reads();
+    barrier_no_fence();
+    if (kb + NS - 1 < nkb) fill(kb + NS - 1);
+    if (kb > my_last) return;
+    u32x4 pf[QS][2];
+    if (kb < my_last) {
+      scores(kb + 1, nxt);
+      softmax(std::false_type{}, kb, cur, pf);
+      // interleave: the fragment reads first, then one MFMA per few ALU instructions
+      __builtin_amdgcn_sched_group_barrier(0x100, 4 * KS, 0);
+#pragma unroll
+      for (int i = 0; i < 4 * KS * QS; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+      }
+    } else {
+      softmax(std::true_type{}, kb, cur, pf);
+    }
+    pv(kb, pf);
+  };
+
+#pragma unroll
+  for (int t = 0; t < NS - 1; ++t)
+    if (t < nkb) fill(t);
+  floatx4 sA[QS][4], sB[QS][4];
+  // every load so far, the query fragments included, through a wait the
+  // compiler sees: it then knows qf has landed and puts no vmcnt(0) in the
+  // loop, which would also wait for the ring's prefetches
+  wait_vmcnt_all();
+  barrier_no_fence();
+  if (my_last >= 0) scores(0, sA);
+  for (int kb = 0; kb < nkb; kb += 2) {
+    step(kb, sA, sB);
+    if (kb + 1 < nkb) step(kb + 1, sB, sA);
   }
 #pragma unroll
   for (int qs = 0; qs < QS; ++qs) {
@@ -576,7 +619,7 @@ template <int DH> struct BwdRing {
   static constexpr int CPR = DH / 8, KST = DH / 32;
   static constexpr int SUB = DH == 32 ? 4 : (DH == 64 ? 2 : 1), WAVES = DH == 32 ? 4 : 8, NTB = 64 * WAVES;
   static constexpr int WR = 16 * SUB, BR = WAVES * WR;
-  static constexpr int NS = DH <= 64 ? 3 : 2;
+  static constexpr int NS = 4;
   static constexpr int BLK = 64 * CPR;
   static constexpr int PAIR_SLOTS = 32;            // 64 (lse2, D) pairs
   static constexpr int STAGE = 2 * BLK + PAIR_SLOTS;
@@ -692,6 +735,7 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
 #pragma unroll
   for (int t = 0; t < NS - 1; ++t)
     if (t < njobs) fill(t);
+  wait_vmcnt_all();   // kf and vf known complete: no vmcnt(0) inside the loop
   for (int j = 0; j < njobs; ++j) {
     wait_loads<C::L, NS - 2>(min(njobs - 1, j + NS - 2) - j);
     wait_lds_reads();
@@ -871,6 +915,7 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
 #pragma unroll
   for (int t = 0; t < NS - 1; ++t)
     if (t < nkb) fill(t);
+  wait_vmcnt_all();   // qf, gf, lq and Dq known complete: no vmcnt(0) inside the loop
   for (int kb = 0; kb < nkb; ++kb) {
     wait_loads<C::L, NS - 2>(min(nkb - 1, kb + NS - 2) - kb);
     wait_lds_reads();

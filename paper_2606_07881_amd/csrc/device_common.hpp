@@ -312,6 +312,9 @@ template <int L, int MAXN> __device__ __forceinline__ void wait_loads(int newer)
     wait_vmcnt<0>();
   }
 }
+// vmcnt(0), other counters left alone, through the builtin: the compiler counts
+// it, so register loads issued before it are known complete afterwards.
+__device__ __forceinline__ void wait_vmcnt_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 // lgkmcnt(0), other counters left alone. Issued through the builtin, not inline
 // asm, so that the compiler's own wait insertion knows the reads are complete:
 // it then never has to cover the 16 LDS reads of two MFMA steps at once, which
