@@ -61,6 +61,49 @@ def make_device_inputs(torch, c, M, seed):
     return x, dy, tgt
 
 
+def gemm_reference(torch, c, reps=20):
+    """The vendor BLAS (torch's bf16 matmul) on this stage's GEMM shapes, as a yardstick.
+
+    Plain products only: no bias, GELU or residual epilogue, no accumulation
+    into G, and the weight gradients over one contiguous window of K * T rows.
+    Returned per family in the stage's own units (ms per replay of M
+    micro-batches over all blocks), to set beside the gemm_* kernel families.
+    """
+    T, d, f, KT = c["micro_batch"] * c["seq"], c["d_model"], c["d_ff"], c["K"] * c["micro_batch"] * c["seq"]
+    fams = {"gemm_fwd": [(T, 3 * d, d), (T, d, d), (T, f, d), (T, d, f)],
+            "gemm_dgrad": [(T, f, d), (T, d, f), (T, d, d), (T, d, 3 * d)],
+            "gemm_wgrad_acc": [(3 * d, d, KT), (d, d, KT), (f, d, KT), (d, f, KT)]}
+    per_mb = c["n_layers"] * c["M"]
+    out = {}
+    for fam, shapes in fams.items():
+        us_total, flop = 0.0, 0.0
+        for M_, N_, K_ in shapes:
+            if fam == "gemm_wgrad_acc":   # dY^T X, both stored token-major
+                a = torch.randn(K_, M_, device="cuda", dtype=torch.bfloat16)
+                b = torch.randn(K_, N_, device="cuda", dtype=torch.bfloat16)
+                fn = lambda: torch.matmul(a.t(), b)
+            else:                         # X W^T with W stored [out, in]
+                a = torch.randn(M_, K_, device="cuda", dtype=torch.bfloat16)
+                b = torch.randn(N_, K_, device="cuda", dtype=torch.bfloat16)
+                fn = lambda: torch.matmul(a, b.t())
+            for _ in range(3):
+                fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / reps
+            us_total += us / (c["K"] if fam == "gemm_wgrad_acc" else 1)
+            flop += 2.0 * M_ * N_ * K_ / (c["K"] if fam == "gemm_wgrad_acc" else 1)
+            del a, b
+        out[fam] = {"ms_per_step": round(us_total * per_mb / 1e3, 3),
+                    "tflops": round(flop / (us_total * 1e-6) / 1e12, 1)}
+    return out
+
+
 def cpu_baseline(c, seed=0, budget_s=20.0):
     """The oracle (float64 NumPy) on a bounded sample of the same workload:
     forward and backward of one sequence of seq tokens through every block of
@@ -115,6 +158,8 @@ def main():
     ap.add_argument("--micro-batch", type=int, default=0,
                     help="sequences per micro-batch instead of the workload's (the paper trains with 16 or 32)")
     ap.add_argument("--K", type=int, default=0, help="accumulation factor instead of the workload's")
+    ap.add_argument("--gemm-reference", action="store_true",
+                    help="time only the vendor BLAS on this stage's GEMM shapes (plain products) and exit")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy a 256 MiB device buffer 3 times (a kernel of known traffic, for scaling "
                          "hardware byte counters)")
@@ -147,6 +192,11 @@ def main():
     T = c["micro_batch"] * c["seq"]
     log(f"bench: {name} M={M} K={K} delay={delay} T={T}")
     torch.cuda.set_device(0)
+    if args.gemm_reference:
+        print(json.dumps({"workload": name, "gemm_reference": gemm_reference(torch, c),
+                          "what": "torch bf16 matmul on the stage's GEMM shapes; plain products, ms per step"}),
+              flush=True)
+        return
     st = binding.Stage(c)
     st.load_params(inputs.make_params(c, args.seed))
     x_all, dy_all, tgt_all = make_device_inputs(torch, c, M, args.seed)
