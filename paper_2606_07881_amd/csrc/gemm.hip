@@ -118,19 +118,18 @@ struct TileLoader {
   }
 };
 
-// tanh z = 1 - 2 / (e^(2z) + 1), saturating to +-1, with the hardware exp2 and
-// reciprocal (about 1 ulp each)
-__device__ __forceinline__ float tanh_f(float z) {
-  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(fast_exp2(2.8853900817779268f * z) + 1.0f);
+// GELU, tanh form: gelu(u) = u (1 + tanh z) / 2 with z = c (u + a u^3). Since
+// (1 + tanh z) / 2 is the logistic function of 2z, s = 1 / (1 + 2^(-2 z log2 e)),
+// it is u s, and its derivative s + 2 c u s (1 - s) (1 + 3 a u^2). One hardware
+// exp2 and one reciprocal (about 1 ulp each); s saturates to 0 or 1.
+__device__ __forceinline__ float gelu_sig(float u, float u2) {
+  const float k = -2.0f * 1.4426950408889634f * 0.7978845608028654f;   // -2 c log2 e
+  return __builtin_amdgcn_rcpf(1.0f + fast_exp2(k * u * fmaf(0.044715f, u2, 1.0f)));
 }
-__device__ __forceinline__ float gelu_f(float u) {
-  const float c = 0.7978845608028654f, a = 0.044715f;
-  return 0.5f * u * (1.0f + tanh_f(c * (u + a * u * u * u)));
-}
+__device__ __forceinline__ float gelu_f(float u) { return u * gelu_sig(u, u * u); }
 __device__ __forceinline__ float gelu_grad_f(float u) {
-  const float c = 0.7978845608028654f, a = 0.044715f;
-  const float th = tanh_f(c * (u + a * u * u * u));
-  return 0.5f * (1.0f + th) + 0.5f * u * (1.0f - th * th) * c * (1.0f + 3.0f * a * u * u);
+  const float u2 = u * u, sg = gelu_sig(u, u2);
+  return fmaf(2.0f * 0.7978845608028654f * fmaf(-sg, sg, sg), u * fmaf(3.0f * 0.044715f, u2, 1.0f), sg);
 }
 
 // Four consecutive elements [i, i+4) of a T array as floats (one 8- or 16-byte load).
