@@ -208,10 +208,10 @@ template <int DH> struct FwdRing {
   static constexpr int L = 2 * BLK / NTF;       // loads per thread per stage (K and V)
 };
 
-// The key loop is software-pipelined: while a wavefront runs the online
-// softmax of key block kb on its vector ALUs, the MFMAs of the scores of block
-// kb + 1 are interleaved with it, so the matrix unit is not idle during the
-// exponentials. A wavefront's queries start at a multiple of 16 * QS, which
+// The key loop is software-pipelined (at head dim 64 and 128): while a
+// wavefront runs the online softmax of key block kb on its vector ALUs, the
+// MFMAs of the scores of block kb + 1 are interleaved with it, so the matrix
+// unit is not idle during the exponentials. A wavefront's queries start at a multiple of 16 * QS, which
 // divides 64, so every key block before its last one ends before its first
 // query and inside the sequence: only the last block is masked.
 template <int DH, bool DROP>
@@ -243,11 +243,17 @@ __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(cons
       qf[qs][s] = (row < S) ? ld16(Qp + (int64_t)row * ld + s * 32 + 8 * g) : u32x4{0, 0, 0, 0};
   }
   floatx4 acc[QS][DH / 16];
+  // the softmax normalizer: without dropout an MFMA of the probability
+  // fragments against ones (the same bf16 P as the numerator, no cross-lane
+  // sums); with dropout a running sum of all of P in fp32
+  floatx4 lacc[QS];
+  const u32x4 ones = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};   // bf16 1.0 pairs
   float m_run[QS], l_run[QS];
 #pragma unroll
   for (int qs = 0; qs < QS; ++qs) {
     m_run[qs] = -INFINITY;
     l_run[qs] = 0.f;
+    lacc[qs] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int t = 0; t < DH / 16; ++t) acc[qs][t] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
@@ -299,16 +305,20 @@ __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(cons
       const float m_new = fmaxf(m_run[qs], mx * scale_log2);
       const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
       const float alpha = fast_exp2(m_run[qs] - m_use);
-      float rs = 0.f;
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float p = fast_exp2(fmaf(sc[qs][kt][r], scale_log2, -m_use));
-          sc[qs][kt][r] = p;
-          rs += p;
-        }
-      l_run[qs] = l_run[qs] * alpha + group4_sum(rs);
+        for (int r = 0; r < 4; ++r) sc[qs][kt][r] = fast_exp2(fmaf(sc[qs][kt][r], scale_log2, -m_use));
+      if constexpr (DROP) {
+        float rs = 0.f;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) rs += sc[qs][kt][r];
+        l_run[qs] = l_run[qs] * alpha + group4_sum(rs);
+      } else {
+        lacc[qs] *= alpha;
+      }
       m_run[qs] = m_new;
       if constexpr (DROP) {   // dropout: the product uses P * keep * scale, the normalizer all of P
 #pragma unroll
@@ -334,18 +344,32 @@ __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(cons
 #pragma unroll
         for (int qs = 0; qs < QS; ++qs) mma_step<bf16>(acc[qs][t], vf, pf[qs][s]);
       }
+    if constexpr (!DROP) {
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int qs = 0; qs < QS; ++qs) mma_step<bf16>(lacc[qs], ones, pf[qs][s]);
+    }
   };
   // iteration kb: blocks up to min(nkb - 1, kb + NS - 2) have been issued;
   // wait for block kb + 1, whose keys this iteration reads, then refill the
   // stage of block kb - 1, which every wavefront has finished with
+  // (at 4 query sub-tiles per wavefront the two score arrays would not fit in
+  // registers: that variant reads and computes block kb only)
+  constexpr bool PIPE = QS <= 2;
   auto step = [&](int kb, floatx4 (&cur)[QS][4], floatx4 (&nxt)[QS][4]) {
-    if (kb + 1 < nkb) wait_loads<C::L, NS - 2>(min(nkb - 1, kb + NS - 2) - (kb + 1));
+    const int newest = PIPE ? kb + 1 : kb;   // the newest block this iteration reads
+    if (newest < nkb) wait_loads<C::L, NS - 2>(min(nkb - 1, kb + NS - 2) - newest);
     wait_lds_reads();
     barrier_no_fence();
     if (kb + NS - 1 < nkb) fill(kb + NS - 1);
     if (kb > my_last) return;
     u32x4 pf[QS][2];
-    if (kb < my_last) {
+    if constexpr (!PIPE) {
+      scores(kb, cur);
+      if (kb < my_last) softmax(std::false_type{}, kb, cur, pf);
+      else softmax(std::true_type{}, kb, cur, pf);
+    } else if (kb < my_last) {
       scores(kb + 1, nxt);
       softmax(std::false_type{}, kb, cur, pf);
       // interleave: the fragment reads first, then one MFMA per few ALU instructions
@@ -370,7 +394,7 @@ __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(cons
   // loop, which would also wait for the ring's prefetches
   wait_vmcnt_all();
   barrier_no_fence();
-  if (my_last >= 0) scores(0, sA);
+  if (PIPE && my_last >= 0) scores(0, sA);
   for (int kb = 0; kb < nkb; kb += 2) {
     step(kb, sA, sB);
     if (kb + 1 < nkb) step(kb + 1, sB, sA);
@@ -379,6 +403,7 @@ __global__ void __launch_bounds__(FwdRing<DH>::NTF, 2) attn_fwd_ring_kernel(cons
   for (int qs = 0; qs < QS; ++qs) {
     const int qrow = qw0 + 16 * qs + (l & 15);
     if (qrow < S) {
+      if constexpr (!DROP) l_run[qs] = lacc[qs][0];   // every row of the product holds the row sum
       const float inv = 1.f / l_run[qs];
       bf16* op = out + ((int64_t)b * S + qrow) * d + h * DH;
 #pragma unroll
