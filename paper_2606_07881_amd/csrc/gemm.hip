@@ -376,9 +376,32 @@ __device__ __forceinline__ void pipe_fill_one(int p, const bf16* src, int64_t ld
 // is one 16-byte store: 8 bf16 or 4 fp32 columns. Each thread keeps the same
 // unit column for all its rows, so the bias is loaded once; the aux rows of
 // all passes are loaded before any store, so their latencies overlap.
-template <typename TO, int EPI, int BN, int PR, int NT>
+template <typename TO, int BN, int PR, int NT> struct EpiGeom {
+  static constexpr int U = 16 / sizeof(TO), UPR = BN / U, RPI = NT / UPR, P = PR / RPI;
+};
+// The bf16 aux rows (residual or u) of a one-panel epilogue, loaded before the
+// main loop so that their latency hides behind it: the same units staged_out
+// gives this thread, one 16-byte load per row; zeros where staged_out will not
+// use them (it then loads for itself).
+template <typename TO, int BN, int PR, int NT>
+__device__ __forceinline__ void prefetch_aux(const GemmArgs& a, int m0, int n0, int tid,
+                                             u32x4 (&pre)[EpiGeom<TO, BN, PR, NT>::P]) {
+  using G = EpiGeom<TO, BN, PR, NT>;
+  static_assert(G::U == 8, "bf16 output units");
+  const int n = n0 + (tid % G::UPR) * G::U, r0 = tid / G::UPR;
+  const bf16* ap = reinterpret_cast<const bf16*>(a.aux);
+  const bool ok = n + G::U <= a.N && a.ld_aux % 8 == 0 && (reinterpret_cast<uintptr_t>(ap) & 15) == 0;
+#pragma unroll
+  for (int p = 0; p < G::P; ++p) {
+    const int m = m0 + r0 + p * G::RPI;
+    pre[p] = (ok && m < a.M) ? ld16(ap + (int64_t)m * a.ld_aux + n) : u32x4{0, 0, 0, 0};
+  }
+}
+
+template <typename TO, int EPI, int BN, int PR, int NT, bool PRE>
 __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, int mb, int n0, int tid,
-                                           float (&csum)[16 / sizeof(TO)]) {
+                                           float (&csum)[16 / sizeof(TO)],
+                                           const u32x4 (&pre)[EpiGeom<TO, BN, PR, NT>::P]) {
   constexpr int U = 16 / sizeof(TO), UPR = BN / U, RPI = NT / UPR, P = PR / RPI;
   static_assert(NT % UPR == 0 && PR % RPI == 0, "units must tile the panel");
   constexpr int LDC = BN + 4;
@@ -402,7 +425,10 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
       const int m = mb + r0 + p * RPI;
       if (m < a.M) {
         const int64_t off = (int64_t)m * a.ld_aux + n;
-        if (vec) {
+        if (PRE && vec) {
+#pragma unroll
+          for (int j = 0; j < U; ++j) aux[p][j] = vget<bf16>(pre[p], j);
+        } else if (vec) {
 #pragma unroll
           for (int h = 0; h < U / 8 + (U < 8 ? 1 : 0); ++h) {
             if constexpr (U >= 8) {
@@ -534,9 +560,10 @@ __device__ __forceinline__ void ce_stats_panel(const GemmArgs& a, const float* c
 // covers whole 256-byte row segments with each store, and each atomic add
 // covers 64 consecutive floats. Tiles larger than the ring are done in row
 // panels of PR rows.
-template <typename TO, int EPI, class CF, int N_I, int N_J>
+template <typename TO, int EPI, class CF, bool PRE, int N_I, int N_J>
 __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, float* cl, int m0, int n0, int wm0, int wn0,
-                                                const floatx4 (&acc)[N_I][N_J]) {
+                                                const floatx4 (&acc)[N_I][N_J],
+                                                const u32x4 (&pre)[EpiGeom<TO, CF::BN, CF::PR, CF::NT>::P]) {
   constexpr int BM = CF::BM, BN = CF::BN, NT = CF::NT, LDC = CF::LDC, PR = CF::PR;
   constexpr int U = 16 / sizeof(TO), UPR = BN / U;
   const int tid = threadIdx.x, l = lane_id();
@@ -566,7 +593,7 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, float* cl, in
         if (m < a.M && n < a.N) atomicAdd(C + (int64_t)m * a.ldc + n, cl[r * LDC + c]);
       }
     } else {
-      staged_out<TO, EPI, BN, PR, NT>(a, cl, mb, n0, tid, csum);
+      staged_out<TO, EPI, BN, PR, NT, PRE>(a, cl, mb, n0, tid, csum, pre);
     }
   }
   if constexpr (EPI != EPI_ATOMIC && EPI != EPI_CE_STATS && UPR <= 64 && 64 % UPR == 0) {
@@ -659,6 +686,10 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
   for (int i = 0; i < WM / 16; ++i)
 #pragma unroll
     for (int j = 0; j < WN / 16; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // bf16 residual or u rows of a one-panel epilogue: loaded now, used after the loop
+  constexpr bool PRE = (EPI == EPI_BIAS_RES || EPI == EPI_GELU_GRAD) && sizeof(TO) == 2 && CF::PR == BM;
+  u32x4 pre[EpiGeom<TO, BN, CF::PR, NT>::P];
+  if constexpr (PRE) prefetch_aux<TO, BN, CF::PR, NT>(a, m0, n0, tid, pre);
 
   // Fragments are double-buffered in registers: the LDS reads of the next
   // MFMA step are issued before the MFMAs of the current one. The barrier that
@@ -748,7 +779,7 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
     }
   }
   wait_vmcnt<0>();   // the fills past the last tile, before the ring is reused
-  staged_epilogue<TO, EPI, CF>(a, reinterpret_cast<float*>(smem), m0, n0, wm0, wn0, acc);
+  staged_epilogue<TO, EPI, CF, PRE>(a, reinterpret_cast<float*>(smem), m0, n0, wm0, wn0, acc, pre);
 }
 
 // Tile configurations; the choice per call is made in launch().
