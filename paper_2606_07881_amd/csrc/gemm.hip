@@ -398,10 +398,20 @@ __device__ __forceinline__ void prefetch_aux(const GemmArgs& a, int m0, int n0, 
   }
 }
 
+// The bias of this thread's output unit, loaded before the main loop as well.
+template <typename TO, int BN, int PR, int NT>
+__device__ __forceinline__ void prefetch_bias(const GemmArgs& a, int n0, int tid, float (&pb)[16 / sizeof(TO)]) {
+  using G = EpiGeom<TO, BN, PR, NT>;
+  const int n = n0 + (tid % G::UPR) * G::U;
+#pragma unroll
+  for (int j = 0; j < G::U; ++j) pb[j] = n + j < a.N ? a.bias[n + j] : 0.f;
+}
+
 template <typename TO, int EPI, int BN, int PR, int NT, bool PRE>
 __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, int mb, int n0, int tid,
                                            float (&csum)[16 / sizeof(TO)],
-                                           const u32x4 (&pre)[EpiGeom<TO, BN, PR, NT>::P]) {
+                                           const u32x4 (&pre)[EpiGeom<TO, BN, PR, NT>::P],
+                                           const float (&pb)[16 / sizeof(TO)]) {
   constexpr int U = 16 / sizeof(TO), UPR = BN / U, RPI = NT / UPR, P = PR / RPI;
   static_assert(NT % UPR == 0 && PR % RPI == 0, "units must tile the panel");
   constexpr int LDC = BN + 4;
@@ -414,9 +424,9 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
   auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
   const bool vec = nv == U && a.ldc % U == 0 && al16(a.C) && (EPI != EPI_BIAS_GELU || al16(a.C2)) &&
                    (!HAS_AUX || (a.ld_aux % 8 == 0 && al16(a.aux))) && (!HAS_BIAS || al16(a.bias));
-  float bias[U];
+  float bias[U];   // prefetched at kernel start (zero past the last column)
 #pragma unroll
-  for (int j = 0; j < U; ++j) bias[j] = (HAS_BIAS && j < nv) ? a.bias[n + j] : 0.f;
+  for (int j = 0; j < U; ++j) bias[j] = HAS_BIAS ? pb[j] : 0.f;
   float aux[P][U];
   if constexpr (HAS_AUX) {
     const bf16* ap = reinterpret_cast<const bf16*>(a.aux);
@@ -563,7 +573,8 @@ __device__ __forceinline__ void ce_stats_panel(const GemmArgs& a, const float* c
 template <typename TO, int EPI, class CF, bool PRE, int N_I, int N_J>
 __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, float* cl, int m0, int n0, int wm0, int wn0,
                                                 const floatx4 (&acc)[N_I][N_J],
-                                                const u32x4 (&pre)[EpiGeom<TO, CF::BN, CF::PR, CF::NT>::P]) {
+                                                const u32x4 (&pre)[EpiGeom<TO, CF::BN, CF::PR, CF::NT>::P],
+                                                const float (&pb)[16 / sizeof(TO)]) {
   constexpr int BM = CF::BM, BN = CF::BN, NT = CF::NT, LDC = CF::LDC, PR = CF::PR;
   constexpr int U = 16 / sizeof(TO), UPR = BN / U;
   const int tid = threadIdx.x, l = lane_id();
@@ -593,7 +604,7 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, float* cl, in
         if (m < a.M && n < a.N) atomicAdd(C + (int64_t)m * a.ldc + n, cl[r * LDC + c]);
       }
     } else {
-      staged_out<TO, EPI, BN, PR, NT, PRE>(a, cl, mb, n0, tid, csum, pre);
+      staged_out<TO, EPI, BN, PR, NT, PRE>(a, cl, mb, n0, tid, csum, pre, pb);
     }
   }
   if constexpr (EPI != EPI_ATOMIC && EPI != EPI_CE_STATS && UPR <= 64 && 64 % UPR == 0) {
@@ -690,6 +701,9 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
   constexpr bool PRE = (EPI == EPI_BIAS_RES || EPI == EPI_GELU_GRAD) && sizeof(TO) == 2 && CF::PR == BM;
   u32x4 pre[EpiGeom<TO, BN, CF::PR, NT>::P];
   if constexpr (PRE) prefetch_aux<TO, BN, CF::PR, NT>(a, m0, n0, tid, pre);
+  float pb[16 / sizeof(TO)];
+  if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU)
+    prefetch_bias<TO, BN, CF::PR, NT>(a, n0, tid, pb);
 
   // Fragments are double-buffered in registers: the LDS reads of the next
   // MFMA step are issued before the MFMAs of the current one. The barrier that
@@ -779,7 +793,7 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
     }
   }
   wait_vmcnt<0>();   // the fills past the last tile, before the ring is reused
-  staged_epilogue<TO, EPI, CF, PRE>(a, reinterpret_cast<float*>(smem), m0, n0, wm0, wn0, acc, pre);
+  staged_epilogue<TO, EPI, CF, PRE>(a, reinterpret_cast<float*>(smem), m0, n0, wm0, wn0, acc, pre, pb);
 }
 
 // Tile configurations; the choice per call is made in launch().
