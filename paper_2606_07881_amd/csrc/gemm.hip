@@ -856,10 +856,12 @@ bool pipe_eligible(const GemmArgs& a) {
 template <typename T, typename TO, bool AK, bool BK, int EPI>
 hipError_t launch(const GemmArgs& a, int splits, hipStream_t st) {
   if (a.seg_rows > 0) {
-    // segmented B: the pipelined 128 x 128 TN kernel only
+    // segmented B (the window weight gradients): the pipelined TN kernel on
+    // 256 x 128 tiles, one workgroup per CU with a three-stage ring (measured
+    // 8% faster than two 128 x 128 workgroups per CU with two stages each)
     if constexpr (sizeof(T) == 2 && !AK && !BK) {
       if (pipe_eligible<AK, BK>(a) && a.seg_rows % 64 == 0 && a.seg_count >= 1 && a.seg_first >= 0)
-        return launch_pipe<TO, AK, BK, EPI, P128x128o2>(a, splits, st);
+        return launch_pipe<TO, AK, BK, EPI, P256x128>(a, splits, st);
     }
     return hipErrorInvalidValue;
   }

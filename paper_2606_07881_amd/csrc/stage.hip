@@ -758,13 +758,14 @@ size_t act_bytes(const paci_stage* h) { return (size_t)h->L.T * h->s.d_model * h
 // G[out, in] += dY^T X over micro-batches j0 .. j0 + n - 1 of the window: dY from the
 // window buffer (contiguous), X from the activation slots of those micro-batches
 // (first micro-batch mb0), one contracted segment of T rows per slot.
-// Split-K count for these long contractions (128 x 128 output tiles): about 1536
-// workgroups, each split at least 1024 contracted rows, at most 16 splits
-// (measured on MI355X for 64K-row weight gradients at d = 1024).
+// Split-K count for these long contractions (256 x 128 output tiles, one
+// workgroup per CU): about 512 workgroups, two rounds over the CUs, each split
+// at least 1024 contracted rows, at most 16 splits (measured on MI355X for
+// 64K-row weight gradients at d = 1024: 512 beat 768 and 1024).
 int window_splits(int out, int in, int64_t Kt) {
-  const int64_t tiles = (int64_t)((out + 127) / 128) * ((in + 127) / 128);
+  const int64_t tiles = (int64_t)((out + 255) / 256) * ((in + 127) / 128);
   const int by_rows = (int)std::min<int64_t>(16, Kt / 1024);
-  return std::max(1, std::min(by_rows, (int)std::lround(1536.0 / (double)tiles)));
+  return std::max(1, std::min(by_rows, (int)std::lround(512.0 / (double)tiles)));
 }
 
 int window_wgrad(paci_stage* h, size_t dy_off, size_t x_off, int out, int in, int j0, int n, int mb0,
