@@ -104,38 +104,85 @@ def gemm_reference(torch, c, reps=20):
     return out
 
 
-def cpu_baseline(c, seed=0, budget_s=20.0):
-    """The oracle (float64 NumPy) on a bounded sample of the same workload:
-    forward and backward of one sequence of seq tokens through every block of
-    the stage, repeated while the time budget lasts. Returns the JSON object."""
+def cpu_baseline(c, seed=0, budget_s=90.0):
+    """The oracle (float64 NumPy) timed on the protocol's bounded sample: the
+    first W = K + delay + 1 micro-batches of the canonical asynchronous 1F1B
+    order, with accumulation into G and the AdamW update after the K-th
+    backward, i.e. every event of the first window and every stale backward
+    that crosses its update. It runs at one sequence per micro-batch and is
+    scaled per sequence to the workload's micro-batch: the oracle's forward
+    and backward work is a sum over sequences, while the update's is not, so
+    the estimate is mu * (forward + backward time) + update time for W * mu *
+    seq tokens. If the forwards and backwards would exceed ``budget_s``, the
+    rest are extrapolated from the mean per event of each kind and the update
+    is timed on its own. BLAS threads are set to the cores this process may
+    run on. Returns the JSON object."""
     import numpy as np
     from oracle import stage as ostage
+    from oracle.schedule import canonical_events
     from paper_2606_07881_amd import inputs
+    cores = len(os.sched_getaffinity(0))
+    blas = None
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        from threadpoolctl import threadpool_info, threadpool_limits
+        threadpool_limits(cores)
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover - threadpoolctl is optional
-        threads = len(os.sched_getaffinity(0))
+        pass
+    K, delay, mu = c["K"], c["delay"], c["micro_batch"]
+    W = K + delay + 1
     one = dict(c)
     one["micro_batch"] = 1
-    params = {k: v.astype(np.float64) for k, v in inputs.make_params(c, seed).items()}
     kind = c["kind"]
-    x = inputs.make_ids(one, seed, 0) if kind == "first" else inputs.make_x(one, seed, 0)[0].astype(np.float64)
-    dy = None if kind == "last" else inputs.make_dy(one, seed, 0)[0].astype(np.float64)
-    tgt = inputs.make_targets(one, seed, 0) if kind == "last" else None
-    n, t0 = 0, time.perf_counter()
-    while True:
-        _, saved = ostage.stage_fwd(one, params, x, tgt)
-        ostage.stage_bwd(one, params, saved, dy, c["K"], ids=x if kind == "first" else None)
-        n += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or n >= 8:
+    params = {k: v.astype(np.float64) for k, v in inputs.make_params(c, seed).items()}
+    st = ostage.Stage(one, params, K, delay)
+    events = canonical_events(W, K, delay)
+    t = {"F": 0.0, "B": 0.0, "S": 0.0}
+    n = {"F": 0, "B": 0, "S": 0}
+    t_start = time.perf_counter()
+    done = True
+    for kd, i in events:
+        if kd in ("F", "B") and n["F"] and n["B"] and t["F"] + t["B"] > budget_s:
+            done = False
             break
-    tokens = n * one["seq"]
-    return {"value": tokens / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{n} x forward+backward of 1 sequence ({one['seq']} tokens) through all "
-                      f"{c['n_layers']} blocks at the workload's shapes, float64, dense masked attention "
-                      f"(about 2x the causal attention FLOPs), {el:.1f} s"}
+        if kd == "F":   # inputs are drawn outside the timed calls
+            x = inputs.make_ids(one, seed, i) if kind == "first" else inputs.make_x(one, seed, i)[0].astype(np.float64)
+            tgt = inputs.make_targets(one, seed, i) if kind == "last" else None
+            t0 = time.perf_counter()
+            st.forward(i, x, tgt)
+        elif kd == "B":
+            dy = None if kind == "last" else inputs.make_dy(one, seed, i)[0].astype(np.float64)
+            t0 = time.perf_counter()
+            st.backward(i, dy)
+        else:
+            t0 = time.perf_counter()
+            st.step()
+        t[kd] += time.perf_counter() - t0
+        n[kd] += 1
+    if not done:   # the update on its own: AdamW over every parameter, as Stage.step does it
+        if n["S"] == 0:
+            for name in st.names:
+                st.G[name] = np.full_like(st.G[name], 1e-3)
+            st.counters.c = K
+            t0 = time.perf_counter()
+            st.step()
+            t["S"] = time.perf_counter() - t0
+    elapsed = time.perf_counter() - t_start
+    fwd_bwd = W * (t["F"] / max(n["F"], 1) + t["B"] / max(n["B"], 1))
+    est = mu * fwd_bwd + t["S"]
+    tokens = W * mu * c["seq"]
+    how = ("every event timed" if done else
+           f"{n['F']} forwards and {n['B']} backwards timed within the budget, the rest extrapolated "
+           "from their means, the update timed on its own")
+    return {"value": tokens / est, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "blas_threads": blas,
+            "sample": f"oracle replay of the first W = K + delay + 1 = {W} micro-batches of the asynchronous 1F1B "
+                      f"order (K {K}, delay {delay}: {W} forwards, {W} backwards accumulated into G, 1 AdamW update "
+                      f"over {sum(v.size for v in params.values())} parameters) at 1 sequence of {c['seq']} tokens "
+                      f"per micro-batch, scaled per sequence to micro-batch {mu}: {mu} x {fwd_bwd:.1f} s forward and "
+                      f"backward + {t['S']:.1f} s update = {est:.1f} s for {tokens} tokens ({how}; {elapsed:.1f} s "
+                      f"measured); float64 NumPy, dense masked attention (about 2x the causal attention FLOPs); "
+                      f"{cores} cores in the affinity mask, BLAS threads {blas}"}
 
 
 def main():
@@ -146,10 +193,14 @@ def main():
     ap.add_argument("--config", default=None)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--cpu-budget", type=float, default=90.0,
+                    help="seconds of oracle forward and backward work before the rest is extrapolated")
     ap.add_argument("--recompute", action="store_true",
                     help="the activation-checkpointed stage: keep only stage inputs, recompute the forward "
                          "in each backward under the current parameters")
+    ap.add_argument("--window", action="store_true",
+                    help="windowed block weight gradients: K + delay activation slots instead of the paper's "
+                         "delay + 1, one contraction per weight and window")
     ap.add_argument("--fused-head", action="store_true",
                     help="last stage: the fused LM head (no [T, V] logits kept; the backward recomputes them)")
     ap.add_argument("--dropout", type=float, default=0.0,
@@ -179,6 +230,8 @@ def main():
         over["recompute"] = 1
     if args.fused_head:
         over["fused_head"] = 1
+    if args.window:
+        over["window"] = 1
     if args.dropout > 0:
         over["dropout"] = args.dropout
         over["dropout_seed"] = 2606
@@ -318,6 +371,8 @@ def main():
                                + ("; activation-checkpointed (forward recomputed in each backward)"
                                   if c.get("recompute") else "")
                                + (f"; dropout {c['dropout']} at every site" if c.get("dropout") else "")
+                               + ("; windowed weight gradients (K + delay activation slots)" if c.get("window")
+                                  else "; weight gradients accumulated per backward (delay + 1 activation slots)")
                                + (f"; LM head over V={c['vocab']} with softmax cross-entropy"
                                   + (", fused (no logits kept)" if c.get("fused_head") else ", fp32 logits kept")
                                   if c["kind"] == "last" else ""),
@@ -329,6 +384,7 @@ def main():
         "ms_per_step_with_launch_events": round(ms_instr, 3),
         "flop_per_step": flop_step,
         "stamps_delta_sum": int(stamps[:, 2].sum()),
+        "arena_gib": round(binding.arena_bytes(c) / 2 ** 30, 2),
         "roofline": roof,
         "kernels": families,
     }

@@ -91,6 +91,16 @@ typedef struct paci_shapes {
                            site, element) through Philox4x32-10, so a backward (and a recomputed
                            forward) uses its forward's masks; the element -> bits map is given with
                            paci_stage_forward */
+  int32_t window;       /* 0 (default): Alg. 1's accumulate step as written, every backward adds its
+                           block weight gradients to G, and the store holds delay + 1 micro-batch
+                           slots (the in-flight count of the appendix "Memory and synchronization
+                           properties"). 1: windowed block weight gradients (bf16, micro_batch * seq
+                           a multiple of 64, d and d_ff multiples of 8, recompute 0; else
+                           E_UNSUPPORTED): each backward keeps its blocks' output gradients, and
+                           one contraction per weight over the K micro-batches of a window adds
+                           them to G before the update or an earlier read of G. Same sum up to fp32
+                           rounding order; costs K - 1 more activation slots plus the window's
+                           output gradients */
 } paci_shapes;
 
 typedef struct paci_counters {
@@ -163,14 +173,16 @@ int paci_param_info_at(const paci_shapes* s, int index, paci_param_info* out); /
 /* ---- stage lifetime --------------------------------------------------------- */
 /* Bytes of device memory the stage needs: fp32 parameters, G, AdamW moments,
  * the bf16 working copy (bf16 stages), the activation store and the backward
- * workspace. The store has delay + 1 micro-batch slots, or K + delay when the
- * block weight gradients are windowed (bf16 stages with micro_batch * seq a
- * multiple of 64 and d, d_ff multiples of 8): such a stage also keeps every
- * block's output gradients of the K micro-batches of a window, and computes the
- * window's weight gradients as one contraction per weight (see stage_backward).
- * A checkpointed stage (recompute = 1) has delay + 1 slots holding only the
- * stage input (ids, targets) plus one work slot for the activations, and no
- * window. E_INVAL / E_UNSUPPORTED as for paci_stage_init. */
+ * workspace. The sizes follow the stage's memory model (appendix "Memory and
+ * synchronization properties": one parameter copy, no weight stash, the
+ * activations of the micro-batches in flight). The store has delay + 1
+ * micro-batch slots (a stage admits at most delay + 1 forwards whose backward
+ * has not run, Sec. 3.2), or K + delay with windowed weight gradients
+ * (paci_shapes.window = 1): such a stage also keeps every block's output
+ * gradients of the K micro-batches of a window. A checkpointed stage
+ * (recompute = 1) has delay + 1 slots holding only the stage input (ids,
+ * targets) plus one work slot for the activations. Pure host computation;
+ * E_INVAL / E_UNSUPPORTED as for paci_stage_init. */
 int paci_stage_arena_bytes(const paci_shapes* s, int K, int delay, size_t* bytes);
 
 /* stage_init(shapes, K, delay). `dev_arena` is caller-owned device memory of

@@ -241,7 +241,7 @@ def replay(cfg, params, K, delay, inputs, grad_outs=None, targets=None, events=N
 
 
 def replay_with_version_store(cfg, params, K, delay, inputs, grad_outs=None, targets=None,
-                              backward_at="current"):
+                              backward_at="current", events=None, grad_hook=None):
     """The same trajectory computed a second way, for cross-checking ``replay``.
 
     Keeps every parameter version theta^(0), theta^(1), ... and no activation
@@ -249,16 +249,20 @@ def replay_with_version_store(cfg, params, K, delay, inputs, grad_outs=None, tar
     obtain the activations, then differentiates at theta^(t^B(i))
     (``backward_at="current"``, Eq. (1)) or at theta^(t^F(i))
     (``backward_at="forward"``, weight stashing; not PACI, used to show that
-    the drift is exercised). Versions are counted from the event list itself.
+    the drift is exercised). Versions are counted from the event list itself
+    (default: the canonical order). ``grad_hook(update_index, G)`` may replace
+    G just before each update, as in ``replay``; the recorded G is the one
+    before the hook.
     """
     M = len(inputs)
-    events = canonical_events(M, K, delay)
+    if events is None:
+        events = canonical_events(M, K, delay)
     names = [n for n, _ in param_shapes(cfg)]
     versions = [{n: np.array(params[n], dtype=np.float64) for n in names}]
     G = {n: np.zeros_like(versions[0][n]) for n in names}
     m = {n: np.zeros_like(versions[0][n]) for n in names}
     v = {n: np.zeros_like(versions[0][n]) for n in names}
-    tF, out, grad_in, thetas = {}, [None] * M, [None] * M, []
+    tF, out, grad_in, thetas, Gs = {}, [None] * M, [None] * M, [], []
     for kind, i in events:
         t = len(versions) - 1
         if kind == "F":
@@ -275,6 +279,9 @@ def replay_with_version_store(cfg, params, K, delay, inputs, grad_outs=None, tar
             for n in names:
                 G[n] = G[n] + g[n]
         else:
+            Gs.append(_copy(G))
+            if grad_hook is not None:
+                G = grad_hook(len(Gs) - 1, G)
             new = {}
             for n in names:
                 wd = cfg["weight_decay"] if decayed(n) else 0.0
@@ -284,4 +291,4 @@ def replay_with_version_store(cfg, params, K, delay, inputs, grad_outs=None, tar
                 G[n] = np.zeros_like(G[n])
             versions.append(new)
             thetas.append(new)
-    return dict(out=out, grad_in=grad_in, theta=thetas)
+    return dict(out=out, grad_in=grad_in, theta=thetas, G=Gs)

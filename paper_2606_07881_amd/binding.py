@@ -39,7 +39,7 @@ class PaciShapes(ctypes.Structure):
                [(n, ctypes.c_float) for n in ("lr", "beta1", "beta2", "eps", "weight_decay", "ln_eps")] + \
                [("recompute", ctypes.c_int32), ("lr_warmup", ctypes.c_int32), ("lr_total", ctypes.c_int32),
                 ("lr_min_ratio", ctypes.c_float), ("fused_head", ctypes.c_int32), ("dropout", ctypes.c_float),
-                ("dropout_seed", ctypes.c_uint32)]
+                ("dropout_seed", ctypes.c_uint32), ("window", ctypes.c_int32)]
 
 
 class PaciCounters(ctypes.Structure):
@@ -148,6 +148,7 @@ def shapes(cfg):
     s.fused_head = int(bool(cfg.get("fused_head", False)))
     s.dropout = float(cfg.get("dropout", 0.0))
     s.dropout_seed = int(cfg.get("dropout_seed", 0)) & 0xFFFFFFFF
+    s.window = int(bool(cfg.get("window", False)))
     return s
 
 

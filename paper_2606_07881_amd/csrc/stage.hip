@@ -10,16 +10,22 @@
 // gradient kernels. The next forward reads the refreshed bf16 weights after
 // the update.
 //
-// Weight gradients of the blocks (bf16 stages whose micro-batch token count is
-// a multiple of 64) are windowed: each backward keeps its output gradients
-// (dqkv, dx1, du, dy of every block) in a per-window buffer, and the K
+// Weight gradients follow Alg. 1's accumulate step by default: every backward
+// adds its G_W += dY^T X products into the fp32 accumulator right away, so the
+// store keeps delay + 1 activation slots, the in-flight count of the paper's
+// memory model (appendix "Memory and synchronization properties"). The slot of
+// mb is reused by F(mb + delay + 1), which the admission rule lets run only
+// after B(mb).
+//
+// Optional windowed weight gradients (paci_shapes.window = 1; bf16 stages whose
+// micro-batch token count is a multiple of 64): each backward keeps its output
+// gradients (dqkv, dx1, du, dy of every block) in a per-window buffer, and the K
 // micro-batches' G_W += dY^T X products run as one long contraction per weight
 // before the update (or before G is read, loaded or the counters reset). The
 // sum is the same; G is read-modified once per window instead of once per
 // micro-batch. The saved activations X then have to outlive the window: the
-// store keeps K + delay slots (delay + 1 otherwise); the slot of mb is reused
-// by F(mb + K + delay), which the protocol admits only after the update that
-// closes mb's window.
+// store keeps K + delay slots; the slot of mb is reused by F(mb + K + delay),
+// which the protocol admits only after the update that closes mb's window.
 //
 // Drift semantics (Eq. 1): a backward differentiates the activations saved by
 // its forward but reads the current parameters. dgrad uses the current bf16
@@ -208,6 +214,7 @@ int validate_shapes(const paci_shapes* s, int K, int delay) {
   if (s->dtype != PACI_FP32 && s->dtype != PACI_BF16) return PACI_E_UNSUPPORTED;
   if (s->recompute != 0 && s->recompute != 1) return PACI_E_INVAL;
   if (s->fused_head != 0 && s->fused_head != 1) return PACI_E_INVAL;
+  if (s->window != 0 && s->window != 1) return PACI_E_INVAL;
   if (!(s->dropout >= 0.f && s->dropout < 1.f)) return PACI_E_INVAL;
   if (s->fused_head) {
     if (s->kind != PACI_LAST || s->dtype != PACI_BF16 || s->d_model % 8) return PACI_E_UNSUPPORTED;
@@ -225,6 +232,8 @@ int validate_shapes(const paci_shapes* s, int K, int delay) {
   if (s->d_model > 4096 || (s->dtype == PACI_FP32 && s->d_model > 2048)) return PACI_E_UNSUPPORTED;
   const int64_t T = (int64_t)s->micro_batch * s->seq;
   if (T > (1LL << 30)) return PACI_E_UNSUPPORTED;
+  if (s->window && (s->recompute || s->dtype != PACI_BF16 || T % 64 || s->d_model % 8 || s->d_ff % 8))
+    return PACI_E_UNSUPPORTED;   // the windowed contraction: stored bf16 activations in 64-row segments
   return PACI_OK;
 }
 
@@ -374,7 +383,7 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
   }
   L.slot_bytes = (sl.off + 255) & ~(size_t)255;
   L.recompute = s.recompute != 0;
-  L.window = !L.recompute && s.dtype == PACI_BF16 && T % 64 == 0 && d % 8 == 0 && f % 8 == 0;
+  L.window = s.window != 0;   // validate_shapes admits it only where the windowed kernels apply
   L.n_slots = L.window ? K + delay : delay + 1;
   if (L.recompute) {
     Bump c;

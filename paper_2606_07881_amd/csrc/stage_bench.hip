@@ -15,7 +15,7 @@
 //
 // usage: stage_bench [--layers L] [--d D] [--heads H] [--ff F] [--seq S] [--mu U]
 //                    [--K K] [--delay N] [--M M] [--steps n] [--warmup n] [--fp32] [--timing]
-//                    [--copy-probe] [--hbm-probe]
+//                    [--window] [--copy-probe] [--hbm-probe]
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -120,14 +120,16 @@ int main(int argc, char** argv) {
   s.eps = 1e-8f;
   s.weight_decay = 0.1f;
   s.ln_eps = 1e-5f;
+  s.window = arg_flag(argc, argv, "--window") ? 1 : 0;
   const int K = arg_int(argc, argv, "--K", 8), delay = arg_int(argc, argv, "--delay", 3);
   const int M = arg_int(argc, argv, "--M", 64);
   const int steps = arg_int(argc, argv, "--steps", 2), warmup = arg_int(argc, argv, "--warmup", 1);
   const bool timing = arg_flag(argc, argv, "--timing");
   const bool bf16 = s.dtype == PACI_BF16;
   const int64_t T = (int64_t)s.micro_batch * s.seq, d = s.d_model;
-  printf("stage_bench: layers %d d %d heads %dx%d ff %d seq %d mu %d K %d delay %d M %d %s\n", s.n_layers,
-         s.d_model, s.n_heads, s.head_dim, s.d_ff, s.seq, s.micro_batch, K, delay, M, bf16 ? "bf16" : "fp32");
+  printf("stage_bench: layers %d d %d heads %dx%d ff %d seq %d mu %d K %d delay %d M %d %s%s\n", s.n_layers,
+         s.d_model, s.n_heads, s.head_dim, s.d_ff, s.seq, s.micro_batch, K, delay, M, bf16 ? "bf16" : "fp32",
+         s.window ? " windowed" : "");
   fflush(stdout);
 
   size_t bytes = 0;

@@ -207,7 +207,7 @@ def test_fused_head_validation_and_memory():
     assert binding.lib.paci_stage_arena_bytes(ctypes.byref(s), c["K"], c["delay"], ctypes.byref(out)) == 0
     fused = out.value
     T, ldz = c["micro_batch"] * c["seq"], (c["vocab"] + 63) // 64 * 64
-    slots = c["K"] + c["delay"]        # windowed weight gradients at these shapes
+    slots = c["delay"] + 1             # the default store: the micro-batches in flight
     partials = 8 * T * (ldz // 64) + 4 * T
     assert plain - fused >= slots * 4 * T * ldz - partials - 4096
     assert plain - fused <= slots * 4 * T * ldz

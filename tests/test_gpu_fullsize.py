@@ -14,6 +14,11 @@ sequence depends on that prefix only):
   equal AdamW applied to theta_0 and the G the GPU accumulated;
 * the G of the last block's output bias after the first window equals the sum
   of every output gradient of that window (MIDDLE and FIRST);
+* GPT-2-medium-shaped middle stage (default and windowed weight gradients):
+  every G tensor of the last block after the first window, against the oracle
+  accumulated sequence by sequence (64 sequences, each a forward through all
+  blocks and the last block's backward at version 0); this reaches the weight
+  gradient products at their full shapes and split counts;
 * B_K: the input gradient of sequence 0 with activations saved at version
   t^F(K) and the parameters of version 1 (the GPU's theta_1): for delay > 0
   this is the stale backward of the method (activations of version 0,
@@ -26,6 +31,7 @@ import numpy as np
 import pytest
 
 from parity import rel_err, to_host, to_torch, tol, unflatten, adamw_np
+from oracle import model
 from oracle import schedule as osched
 from oracle import stage as ostage
 from paper_2606_07881_amd import configs, inputs
@@ -33,8 +39,11 @@ from paper_2606_07881_amd import configs, inputs
 pytestmark = pytest.mark.gpu
 
 FULL = ["gpt2s_mid_bf16", "gpt2m_mid_bf16", "gpt2m_first_bf16", "gpt2m_last_bf16", "gpt1p3b_pos0_bf16",
-        "gpt2m_mid_bf16+ckpt",   # +ckpt: the same workload on an activation-checkpointed stage
-        "gpt2m_last_bf16+fused"]  # +fused: the last stage with the fused LM head (no logits kept)
+        "gpt2m_mid_bf16+ckpt",    # +ckpt: the same workload on an activation-checkpointed stage
+        "gpt2m_last_bf16+fused",  # +fused: the last stage with the fused LM head (no logits kept)
+        "gpt2m_mid_bf16+window"]  # +window: windowed weight gradients (K + delay activation slots)
+EXTRA = {"+ckpt": {"recompute": 1}, "+fused": {"fused_head": 1}, "+window": {"window": 1}}
+LAST_BLOCK_G = {"gpt2m_mid_bf16"}   # workloads whose last block's G is compared in full
 PREFIX = 256   # tokens of a sequence whose forward is checked where the whole one is not needed
 
 
@@ -69,6 +78,35 @@ def seq_rows(c, a, b, S=None):
     return a.reshape(c["micro_batch"], c["seq"], -1)[b, :S]
 
 
+_ORACLE_G = {}
+
+
+def oracle_last_block_G(c, seed, theta0):
+    """G of the last block after the first window (micro-batches 0 .. K-1, all
+    at version 0): the sum over their sequences of the last block's parameter
+    gradients, each from a forward through every block and the last block's
+    backward. Middle stage, no dropout. Cached per workload shape."""
+    key = (c["name"].split("+")[0], seed)
+    if key in _ORACLE_G:
+        return _ORACLE_G[key]
+    L, K, mu = c["n_layers"], c["K"], c["micro_batch"]
+    cs = seq_cfg(c)
+    blocks = [{n: theta0[f"h{l}.{n}"] for n in ostage.BLOCK_PARAMS} for l in range(L)]
+    acc = None
+    for i in range(K):
+        xm = inputs.make_x(c, seed, i)[0]
+        dym = inputs.make_dy(c, seed, i)[0]
+        for b in range(mu):
+            x = seq_input(c, xm, b)
+            for l in range(L):
+                x, saved = model.block_fwd(x, blocks[l], cs, None)
+            _, g = model.block_bwd(seq_rows(c, dym, b).astype(np.float64), saved, blocks[L - 1], cs)
+            acc = g if acc is None else {n: acc[n] + g[n] for n in g}
+        print(f"  oracle: last block G, micro-batch {i + 1}/{K} accumulated", flush=True)
+    _ORACLE_G[key] = acc
+    return acc
+
+
 def oracle_grad_in(c, theta_f, theta_b, x_seq, dy_seq, tgt_seq):
     """Input gradient of one sequence: activations saved at theta_f, backward at theta_b."""
     cs = seq_cfg(c)
@@ -79,11 +117,11 @@ def oracle_grad_in(c, theta_f, theta_b, x_seq, dy_seq, tgt_seq):
     return gin
 
 
+@pytest.mark.timeout(900)   # the oracle's last-block G takes about 100 s of host time
 @pytest.mark.parametrize("name", FULL)
 def test_fullsize_sampled(binding, name):
     import torch
-    extra = {"+ckpt": {"recompute": 1}, "+fused": {"fused_head": 1}}
-    c = configs.get(name.split("+")[0], **next((v for k, v in extra.items() if name.endswith(k)), {}))
+    c = configs.get(name.split("+")[0], **next((v for k, v in EXTRA.items() if name.endswith(k)), {}))
     K, delay, seed = c["K"], c["delay"], 0
     T, d, mu = c["micro_batch"] * c["seq"], c["d_model"], c["micro_batch"]
     kind = c["kind"]
@@ -178,6 +216,16 @@ def test_fullsize_sampled(binding, name):
         print(f"{name}: G b_2 of the last block {e:.2e}", flush=True)
         assert e <= 1e-4
 
+    # every G tensor of the last block against the oracle
+    if name.split("+")[0] in LAST_BLOCK_G and not c.get("recompute"):
+        L = c["n_layers"]
+        ref = oracle_last_block_G(c, seed, theta0)
+        Gd = unflatten(c, G1)
+        for n, r in ref.items():
+            e = rel_err(Gd[f"h{L - 1}.{n}"], r)
+            print(f"{name}: G h{L - 1}.{n} after the first window {e:.2e}", flush=True)
+            assert e <= tg, n
+
     # F_0 at version 0
     out0 = to_host(outs[0])
     assert np.all(np.isfinite(out0))
@@ -208,6 +256,19 @@ def test_fullsize_sampled(binding, name):
         e = rel_err(seq_rows(c, gin, 0), ref)
         print(f"{name}: B_{i} (t^F={tF[i]}, t^B={tB[i]}) grad_in sequence 0 {e:.2e}", flush=True)
         assert e <= tg
+        if tB[i] > tF[i] and not c.get("recompute"):
+            # Eq. (1) against weight stashing: the same saved activations
+            # differentiated at the forward's parameters. At this learning rate
+            # one update separates the two by about 3 tolerances only, so the
+            # GPU's result must be at least one tolerance from the stash result
+            # and at least 3 times closer to the current-parameter result.
+            stash = oracle_grad_in(c, versions[tF[i]], versions[tF[i]], seq_input(c, x_host[i], 0),
+                                   None if kind == "last" else seq_rows(c, dy_host[i], 0).astype(np.float64),
+                                   tg_host[i][0:1] if kind == "last" else None)
+            e_st = rel_err(seq_rows(c, gin, 0), stash)
+            print(f"{name}: B_{i} distance from weight stashing {e_st:.2e} ({e_st / max(e, 1e-30):.1f}x the "
+                  f"distance from Eq. (1))", flush=True)
+            assert e_st >= tg and e_st >= 3.0 * e
 
     # the last forward, at version 1
     j = max(i for k, i in events if k == "F")
