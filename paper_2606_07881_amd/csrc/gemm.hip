@@ -644,7 +644,7 @@ __device__ __forceinline__ void interleave_reads() {
   }
 }
 
-template <typename TO, bool AK, bool BK, int EPI, class CF>
+template <typename TO, bool AK, bool BK, int EPI, class CF, bool GRP = false>
 __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, int k_per_split) {
   constexpr int BM = CF::BM, BN = CF::BN, WM = CF::WM, WN = CF::WN, NT = CF::NT, NS = CF::NS;
   constexpr int WAVES_N = BN / WN;
@@ -652,9 +652,26 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
   constexpr int L = CF::LA + CF::LB;
   __shared__ u32x4 smem[CF::SMEM_SLOTS];
   const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
+  int pid = blockIdx.x;
+  if constexpr (GRP) {
+    // grouped weight gradients: find this workgroup's problem (wave-uniform scalar loads)
+    int p = 0;
+    while (p + 1 < a.group_n && pid >= a.group[p + 1].tile0) ++p;
+    const WgradProblem& pr = a.group[p];
+    pid -= pr.tile0;
+    if (pid >= ((pr.M + BM - 1) / BM) * ((pr.N + BN - 1) / BN)) return;   // padding to a multiple of 8
+    a.A = pr.A;
+    a.B = pr.B;
+    a.C = pr.C;
+    a.M = pr.M;
+    a.N = pr.N;
+    a.lda = pr.M;
+    a.ldb = pr.N;
+    a.ldc = pr.N;
+  }
   const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.N + BN - 1) / BN;
   int tm, tn;
-  tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  tile_coords(pid, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int k_begin = blockIdx.y * k_per_split;
   const int k_end = min(a.K, k_begin + k_per_split);
@@ -950,6 +967,27 @@ hipError_t by_layout(bool out_f32, GemmLayout lay, GemmEpi epi, const GemmArgs& 
 }  // namespace
 
 void gemm_set_tile_override(int cfg) { g_tile_override = cfg; }
+
+// Grouped weight gradients on 256 x 128 tiles (one workgroup per CU, three-stage ring),
+// plain fp32 read-modify-write of each output tile.
+int wgrad_group_tiles(int M, int N) {
+  return ((M + P256x128::BM - 1) / P256x128::BM) * ((N + P256x128::BN - 1) / P256x128::BN);
+}
+
+hipError_t gemm_wgrad_grouped(const WgradProblem* probs, int n, int total_tiles, int K, const void* zeros,
+                              hipStream_t st) {
+  if (probs == nullptr || n < 1 || total_tiles < 1 || K < 1 || K % 8 || zeros == nullptr ||
+      (reinterpret_cast<uintptr_t>(zeros) & 15))
+    return hipErrorInvalidValue;
+  GemmArgs a{};
+  a.K = K;
+  a.zeros = zeros;
+  a.group = probs;
+  a.group_n = n;
+  hipLaunchKernelGGL((gemm_pipe_kernel<float, false, false, EPI_ACC, P256x128, true>), dim3(total_tiles, 1),
+                     dim3(P256x128::NT), 0, st, a, K);
+  return hipGetLastError();
+}
 
 int gemm_acc_splits(DType dt, int M, int N, int K) {
   // Split-K count for Cf32 += A^T B. Cost model, in microseconds: rounds of

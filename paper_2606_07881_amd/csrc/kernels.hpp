@@ -39,6 +39,20 @@ enum GemmLayout { GEMM_NT = 0, GEMM_NN = 1, GEMM_TN = 2 };
 enum GemmEpi { EPI_STORE = 0, EPI_BIAS, EPI_BIAS_RES, EPI_BIAS_GELU, EPI_GELU_GRAD, EPI_ACC, EPI_ATOMIC, EPI_CE_STATS,
                EPI_CE_GRAD };
 
+// Grouped weight gradients (bf16, one launch): problem p adds
+// C_p[M_p, N_p] (fp32, row stride N_p) += A_p^T B_p over K contracted rows, with
+// A_p [K, M_p] and B_p [K, N_p] bf16 row-major (the layer's output gradient and
+// its input, GEMM_TN). Every output tile belongs to one workgroup, so the sum is
+// a plain read-modify-write (no split, no atomics). `probs` is device memory
+// holding n problems; tile0 is the problem's first workgroup, a multiple of 8
+// (wgrad_group_tiles gives each problem's count; workgroups past a problem's
+// tiles exit). M_p, N_p, K multiples of 8 and 16-byte aligned operands.
+struct WgradProblem {
+  const void* A;
+  const void* B;
+  float* C;
+  int M, N, tile0, pad;
+};
 struct GemmArgs {
   const void* A; int64_t lda;
   const void* B; int64_t ldb;
@@ -61,9 +75,16 @@ struct GemmArgs {
   int64_t ld_part = 0;
   float* ce_zt = nullptr;
   float alpha = 1.f;
+  // grouped weight gradients (gemm_wgrad_grouped): device problem table
+  const WgradProblem* group = nullptr;
+  int group_n = 0;
 };
 // bf16 operands: K-major vectors that straddle K read the memory just past K,
 // which must hold zeros (true when K % 8 == 0, or for zero-padded rows).
+
+int wgrad_group_tiles(int M, int N);
+hipError_t gemm_wgrad_grouped(const WgradProblem* probs, int n, int total_tiles, int K, const void* zeros,
+                              hipStream_t st);
 
 // dtype: element type of A, B, aux and of C/C2 unless out_f32 (then C is float).
 // splits > 1 is only valid with EPI_ATOMIC.

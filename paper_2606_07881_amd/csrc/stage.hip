@@ -293,7 +293,13 @@ struct Layout {
   int nchunks = 0;
   size_t stash, slot_bytes;
   int n_slots = 1;             // activation slots: delay + 1, or K + delay with windowed weight gradients
-  bool window = false;         // weight gradients windowed (see the header)
+  bool window = false;         // weight gradients windowed over the K micro-batches of a window
+  // bf16 stages without the window: each backward keeps its blocks' output
+  // gradients (a window of one micro-batch) and adds all their weight
+  // gradients to G in one grouped launch at its end
+  bool wdefer = false;
+  size_t wgroup = 0;           // problem tables of that launch, one per activation slot (or work slot)
+  int wgroup_n = 0, wgroup_tiles = 0;
   // checkpointed stages: each slot holds the stage input only (c_* offsets,
   // c_bytes per slot); one work slot of the full layout takes the activations
   bool recompute = false;
@@ -384,6 +390,7 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
   L.slot_bytes = (sl.off + 255) & ~(size_t)255;
   L.recompute = s.recompute != 0;
   L.window = s.window != 0;   // validate_shapes admits it only where the windowed kernels apply
+  L.wdefer = !L.window && s.dtype == PACI_BF16 && T % 8 == 0 && d % 8 == 0 && f % 8 == 0;
   L.n_slots = L.window ? K + delay : delay + 1;
   if (L.recompute) {
     Bump c;
@@ -396,15 +403,26 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
   } else {
     L.stash = a.take(L.slot_bytes * (size_t)L.n_slots);
   }
-  if (L.window) {
+  if (L.window || L.wdefer) {
+    const size_t wk = L.window ? (size_t)K : 1;   // micro-batches per window buffer
     for (int l = 0; l < s.n_layers; ++l) {
       Layout::WinBlock w;
-      w.dqkv = a.take(esz * (size_t)K * T * 3 * d);
-      w.dx1 = a.take(esz * (size_t)K * T * d);
-      w.du = a.take(esz * (size_t)K * T * f);
-      w.dy = a.take(esz * (size_t)K * T * d);
+      w.dqkv = a.take(esz * wk * T * 3 * d);
+      w.dx1 = a.take(esz * wk * T * d);
+      w.du = a.take(esz * wk * T * f);
+      w.dy = a.take(esz * wk * T * d);
       L.win.push_back(w);
     }
+  }
+  if (L.wdefer) {
+    L.wgroup_n = 4 * s.n_layers;
+    const int tables = L.recompute ? 1 : L.n_slots;
+    L.wgroup = a.take(sizeof(paci::WgradProblem) * (size_t)L.wgroup_n * tables);
+    const int shapes[4][2] = {{(int)d, (int)f}, {(int)f, (int)d}, {(int)d, (int)d}, {3 * (int)d, (int)d}};
+    int tiles = 0;
+    for (int l = 0; l < s.n_layers; ++l)
+      for (int q = 0; q < 4; ++q) tiles += (paci::wgrad_group_tiles(shapes[q][0], shapes[q][1]) + 7) / 8 * 8;
+    L.wgroup_tiles = tiles;
   }
 
   // backward workspace (one micro-batch at a time)
@@ -704,7 +722,7 @@ int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx, bool dy_
   const BlockRefs& b = h->p.blocks[l];
   const BlockSlot& o = h->L.blk[l];
   const Layout& L = h->L;
-  const bool win = L.window, drop = L.dropout;
+  const bool win = L.window || L.wdefer, drop = L.dropout;
   char* du = win ? h->win(L.win[l].du, j, f) : h->ws(L.w_du);
   char* dn = h->ws(L.w_dn);
   char* dx1 = win ? h->win(L.win[l].dx1, j, d) : h->ws(L.w_dx1);
@@ -813,6 +831,52 @@ int flush_window(paci_stage* h) {
   }
   h->win_done = c;
   return PACI_OK;
+}
+
+// The weight gradients of every block of one backward, from the output
+// gradients it left in the window buffers and the activations of its slot
+// (table t), in one grouped launch: G_W += dY^T X for the four weights of each
+// block (Alg. 1's accumulate step for this backward).
+int wgrad_grouped(paci_stage* h, int t) {
+  const Layout& L = h->L;
+  const double T = (double)L.T, d = h->s.d_model, f = h->s.d_ff;
+  const double work = 2.0 * T * h->s.n_layers * (d * f + f * d + d * d + 3 * d * d);
+  const auto* tab = reinterpret_cast<const paci::WgradProblem*>(h->arena + L.wgroup) + (size_t)t * L.wgroup_n;
+  return run(h, F_GEMM_WGRAD, work, [&] {
+    return paci::gemm_wgrad_grouped(tab, L.wgroup_n, L.wgroup_tiles, (int)L.T, h->arena + L.zeros, h->st);
+  });
+}
+
+// Problem tables of the grouped launch, one per activation area a backward can read.
+std::vector<paci::WgradProblem> wgrad_tables(const paci_stage* h) {
+  const Layout& L = h->L;
+  const int d = h->s.d_model, f = h->s.d_ff;
+  const int tables = L.recompute ? 1 : L.n_slots;
+  std::vector<paci::WgradProblem> v;
+  for (int t = 0; t < tables; ++t) {
+    const char* A = L.recompute ? h->arena + L.work : h->arena + L.stash + (size_t)t * L.slot_bytes;
+    int tile0 = 0;
+    for (int l = h->s.n_layers - 1; l >= 0; --l) {   // the order the backward produced them
+      const BlockRefs& b = h->p.blocks[l];
+      const BlockSlot& o = L.blk[l];
+      const Layout::WinBlock& w = L.win[l];
+      const struct { size_t dy, x; int M, N; int64_t g; } q[4] = {
+          {w.dy, o.a, d, f, b.w_2}, {w.du, o.n2, f, d, b.w_1}, {w.dx1, o.o, d, d, b.w_o}, {w.dqkv, o.n1, 3 * d, d, b.w_qkv}};
+      for (const auto& e : q) {
+        paci::WgradProblem pr;
+        pr.A = h->arena + e.dy;
+        pr.B = A + e.x;
+        pr.C = h->G() + e.g;
+        pr.M = e.M;
+        pr.N = e.N;
+        pr.tile0 = tile0;
+        pr.pad = 0;
+        v.push_back(pr);
+        tile0 += (paci::wgrad_group_tiles(e.M, e.N) + 7) / 8 * 8;
+      }
+    }
+  }
+  return v;
 }
 
 // The stage forward of one micro-batch into the activation area A (its slot, or
@@ -945,6 +1009,11 @@ extern "C" int paci_stage_init(const paci_shapes* s, int K, int delay, void* dev
   if (e == hipSuccess)
     e = hipMemcpyAsync(h->arena + h->L.chunks, chunks.data(), chunks.size() * sizeof(int32_t),
                        hipMemcpyHostToDevice, h->st);
+  std::vector<paci::WgradProblem> tabs;
+  if (h->L.wdefer) tabs = wgrad_tables(h);
+  if (e == hipSuccess && !tabs.empty())
+    e = hipMemcpyAsync(h->arena + h->L.wgroup, tabs.data(), tabs.size() * sizeof(paci::WgradProblem),
+                       hipMemcpyHostToDevice, h->st);
   if (e == hipSuccess) e = hipStreamSynchronize(h->st);
   if (e != hipSuccess) {
     g_init_hip_error = (int)e;
@@ -1066,8 +1135,8 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
   char* bufA = h->ws(L.w_dyA);
   char* bufB = h->ws(L.w_dyB);
   const void* dy = dev_grad_out;
-  const int j = h->fsm.c;   // position in the window
-  const bool win = L.window;
+  const int j = L.window ? h->fsm.c : 0;   // position in the window buffers
+  const bool win = L.window || L.wdefer;
   // windowed: every block's output gradient lives in the window buffer
   char* dy_last = win ? h->win(L.win[s.n_layers - 1].dy, j, d) : bufA;
   int r = PACI_OK;
@@ -1123,6 +1192,7 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
     r = block_bwd(h, A, l, dy, dx, l < s.n_layers - 1 || s.kind == PACI_LAST, j, mb);
     dy = dx;
   }
+  if (!r && L.wdefer) r = wgrad_grouped(h, L.recompute ? 0 : mb % L.n_slots);
   if (!r && s.kind == PACI_FIRST && L.dropout) {   // through the embedding dropout
     r = dropout(h, dy, nullptr, h->ws(L.w_g2), h->drop(mb, 0, SITE_EMBED));
     dy = h->ws(L.w_g2);

@@ -258,17 +258,18 @@ def test_fullsize_sampled(binding, name):
         assert e <= tg
         if tB[i] > tF[i] and not c.get("recompute"):
             # Eq. (1) against weight stashing: the same saved activations
-            # differentiated at the forward's parameters. At this learning rate
-            # one update separates the two by about 3 tolerances only, so the
-            # GPU's result must be at least one tolerance from the stash result
-            # and at least 3 times closer to the current-parameter result.
+            # differentiated at the forward's parameters. One update moves the
+            # weights by about lr along sign(G), which changes this input
+            # gradient by about 10 tolerances at the GPT-2-medium shapes; the
+            # GPU's result must lie at least 3 tolerances from the stash result
+            # and at least 3 times farther from it than from Eq. (1)'s.
             stash = oracle_grad_in(c, versions[tF[i]], versions[tF[i]], seq_input(c, x_host[i], 0),
                                    None if kind == "last" else seq_rows(c, dy_host[i], 0).astype(np.float64),
                                    tg_host[i][0:1] if kind == "last" else None)
             e_st = rel_err(seq_rows(c, gin, 0), stash)
             print(f"{name}: B_{i} distance from weight stashing {e_st:.2e} ({e_st / max(e, 1e-30):.1f}x the "
                   f"distance from Eq. (1))", flush=True)
-            assert e_st >= tg and e_st >= 3.0 * e
+            assert e_st >= 3.0 * tg and e_st >= 3.0 * e
 
     # the last forward, at version 1
     j = max(i for k, i in events if k == "F")
