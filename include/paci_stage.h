@@ -185,7 +185,11 @@ int paci_param_info_at(const paci_shapes* s, int index, paci_param_info* out); /
  * E_INVAL / E_UNSUPPORTED as for paci_stage_init. */
 int paci_stage_arena_bytes(const paci_shapes* s, int K, int delay, size_t* bytes);
 
-/* stage_init(shapes, K, delay). `dev_arena` is caller-owned device memory of
+/* stage_init(shapes, K, delay): one pipeline stage of Alg. 1 (appendix
+ * "Stage-level execution rule") with a single parameter copy theta, the
+ * accumulator G and the AdamW moments (appendix "Memory and synchronization
+ * properties"), counters t = c = q = 0 (appendix "Pipeline setup and notation":
+ * versions count local updates from 0). `dev_arena` is caller-owned device memory of
  * at least paci_stage_arena_bytes bytes, 256-byte aligned, that must outlive
  * the handle; `hip_stream` is the hipStream_t all work is enqueued on (NULL =
  * the null stream). Parameters start at zero and G, m, v are cleared; load the
@@ -200,7 +204,9 @@ int paci_stage_destroy(paci_stage* h); /* frees host state only; the arena stays
 
 /* ---- state transfer --------------------------------------------------------- */
 enum paci_what { PACI_PARAMS = 0, PACI_GRADS = 1, PACI_EXP_AVG = 2, PACI_EXP_AVG_SQ = 3 };
-/* Copy n fp32 values in the canonical order into / out of the stage. n must
+/* State transfer of the stage's single parameter copy, its accumulator G
+ * (Alg. 1's local gradient sum) and the AdamW moments (appendix "Detailed
+ * experimental setup": AdamW). Copy n fp32 values in the canonical order into / out of the stage. n must
  * equal the stage's element count (paci_param_count). `src`/`dst` are device
  * pointers if `on_device` is non-zero, else host pointers (the call then
  * synchronizes the stream). Loading PARAMS also rewrites the bf16 working copy.
@@ -211,7 +217,9 @@ int paci_stage_load(paci_stage* h, int what, const float* src, int64_t n, int on
 int paci_stage_read(paci_stage* h, int what, float* dst, int64_t n, int on_device);
 
 /* ---- the three events of Alg. 1 ----------------------------------------------- */
-/* stage_forward(mb, &version): F_i of micro-batch mb at the current parameters.
+/* stage_forward(mb, &version): F_i of micro-batch mb at the current parameters
+ * (Alg. 1's forward event, admitted only while q <= delay, Sec. 3.2; the
+ * version it returns is t^F of the appendix "Pipeline setup and notation").
  * Middle/last stage: `dev_in` is the stage input [T, d] (stage dtype). First
  * stage: `dev_in` is int32 token ids [micro_batch, seq] in [0, vocab).
  * Middle/first stage: `dev_out` receives [T, d] (stage dtype). Last stage:
@@ -261,7 +269,10 @@ int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_out, void* d
 int paci_stage_step(paci_stage* h, int* new_version);
 
 /* ---- schedule driver --------------------------------------------------------- */
-/* Replays paci_schedule(M, K, delay) on the handle by calling forward,
+/* The schedule driver: the event order of Alg. 1 at one stage, each forward
+ * issued as soon as admission allows and each update right after the backward
+ * that completes its window (Sec. 3.2; the order whose worst case Eq. (2)
+ * bounds). Replays paci_schedule(M, K, delay) on the handle by calling forward,
  * backward and step. Micro-batch i reads dev_in_all + i * (input bytes) (ids
  * for a first stage), dev_targets_all + i * T (last stage), dev_grad_out_all
  * + i * (T * d elements) (middle/first), and writes dev_out_all + i * (output

@@ -503,6 +503,14 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
       for (int j = 0; j < U; ++j)
         if (j < nv) csum[j] += o[j];
     }
+    if constexpr (sizeof(TO) == 4 && (EPI == EPI_ACC || EPI == EPI_STORE)) {
+      if (a.nonfinite != nullptr) {   // uniform
+        bool bad = false;
+#pragma unroll
+        for (int j = 0; j < U; ++j) bad |= (j < nv) && !__builtin_isfinite(o[j]);
+        if (bad) *a.nonfinite = 1;
+      }
+    }
     TO* C = reinterpret_cast<TO*>(a.C);
     if (vec) {
       if constexpr (sizeof(TO) == 2) {
@@ -975,7 +983,7 @@ int wgrad_group_tiles(int M, int N) {
 }
 
 hipError_t gemm_wgrad_grouped(const WgradProblem* probs, int n, int total_tiles, int K, const void* zeros,
-                              hipStream_t st) {
+                              bool overwrite, int* nonfinite, hipStream_t st) {
   if (probs == nullptr || n < 1 || total_tiles < 1 || K < 1 || K % 8 || zeros == nullptr ||
       (reinterpret_cast<uintptr_t>(zeros) & 15))
     return hipErrorInvalidValue;
@@ -984,8 +992,13 @@ hipError_t gemm_wgrad_grouped(const WgradProblem* probs, int n, int total_tiles,
   a.zeros = zeros;
   a.group = probs;
   a.group_n = n;
-  hipLaunchKernelGGL((gemm_pipe_kernel<float, false, false, EPI_ACC, P256x128, true>), dim3(total_tiles, 1),
-                     dim3(P256x128::NT), 0, st, a, K);
+  a.nonfinite = nonfinite;
+  if (overwrite)
+    hipLaunchKernelGGL((gemm_pipe_kernel<float, false, false, EPI_STORE, P256x128, true>), dim3(total_tiles, 1),
+                       dim3(P256x128::NT), 0, st, a, K);
+  else
+    hipLaunchKernelGGL((gemm_pipe_kernel<float, false, false, EPI_ACC, P256x128, true>), dim3(total_tiles, 1),
+                       dim3(P256x128::NT), 0, st, a, K);
   return hipGetLastError();
 }
 

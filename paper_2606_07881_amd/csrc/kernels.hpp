@@ -78,13 +78,16 @@ struct GemmArgs {
   // grouped weight gradients (gemm_wgrad_grouped): device problem table
   const WgradProblem* group = nullptr;
   int group_n = 0;
+  int* nonfinite = nullptr;   // fp32 EPI_ACC / EPI_STORE: set to 1 if an element written is not finite
 };
 // bf16 operands: K-major vectors that straddle K read the memory just past K,
 // which must hold zeros (true when K % 8 == 0, or for zero-padded rows).
 
+// overwrite: C_p = A_p^T B_p instead of +=; nonfinite (nullable): set to 1 (a plain
+// store) if any element written is NaN or infinite.
 int wgrad_group_tiles(int M, int N);
 hipError_t gemm_wgrad_grouped(const WgradProblem* probs, int n, int total_tiles, int K, const void* zeros,
-                              hipStream_t st);
+                              bool overwrite, int* nonfinite, hipStream_t st);
 
 // dtype: element type of A, B, aux and of C/C2 unless out_f32 (then C is float).
 // splits > 1 is only valid with EPI_ATOMIC.
@@ -157,19 +160,28 @@ hipError_t ce_bwd(DType dt, const float* z, int64_t ldz, const int32_t* tgt, con
 // ---- AdamW over the flat parameter arena --------------------------------------------------
 // ctl: 4 device ints {G not finite, updates applied, updates skipped, unused}.
 // adamw_guard: ctl[0] = 1 if any of the n values of G is not finite (else ctl[0]
-// is left as is: clear it first with adamw_ctl(..., 0)).
-// adamw: one launch over every parameter: chunks[i] = {begin, end, decay, 0}
-// (elements; begin/end multiples of 4). Unless ctl[0] is set: with t = ctl[1] + 1,
-// theta <- theta * (1 - lr_t * wd * decay), then the Adam direction with bias
-// correction of step t; m, v updated; theta_bf16 (nullable) rewritten. G is
-// cleared either way. lr_t follows the schedule (lr_total = 0: lr).
-// adamw_ctl: mode 0 clears ctl[0]; 1 counts the update (ctl[1] or ctl[2]);
-// 2 clears all of ctl.
+// is left as is); adamw_guard_ranges: the same over ranges[i] = {begin, end}
+// (elements, multiples of 4), one workgroup per range.
+// adamw: one launch over every parameter, one workgroup per table entry:
+//   {begin, end, flags, 0}: the elements [begin, end) of one tensor (multiples of 4);
+//   {offset, r0 << 16 | c0, flags | ADAMW_TILE, rows << 16 | cols}: the 64 x 64 tile at
+//   (r0, c0) of the matrix [rows, cols] at offset (rows, cols multiples of 8), whose
+//   bf16 values also go transposed into theta_bf16T ([cols, rows] at the same offset).
+// Unless ctl[0] is set: with t = ctl[1] + 1, theta <- theta * (1 - lr_t * wd) where
+// ADAMW_DECAY, then the Adam direction with bias correction of step t; m, v updated;
+// theta_bf16 (nullable) rewritten. G is cleared either way where ADAMW_CLEAR_G.
+// lr_t follows the schedule (lr_total = 0: lr).
+// adamw_ctl: mode 0 clears ctl[0]; 1 counts the update (ctl[1] or ctl[2]) and clears
+// ctl[0]; 2 clears all of ctl.
+enum { ADAMW_DECAY = 1, ADAMW_CLEAR_G = 2, ADAMW_TILE = 4 };
 struct AdamwArgs { float lr, beta1, beta2, eps, weight_decay, lr_min_ratio; int lr_warmup, lr_total; };
 hipError_t adamw_guard(const float* G, int64_t n, int* ctl, hipStream_t st);
-hipError_t adamw(float* theta, float* G, float* m, float* v, void* theta_bf16, const int4* chunks, int nchunks,
-                 const AdamwArgs& a, const int* ctl, hipStream_t st);
+hipError_t adamw_guard_ranges(const float* G, const int2* ranges, int nranges, int* ctl, hipStream_t st);
+hipError_t adamw(float* theta, float* G, float* m, float* v, void* theta_bf16, void* theta_bf16T, const int4* chunks,
+                 int nchunks, const AdamwArgs& a, const int* ctl, hipStream_t st);
 hipError_t adamw_ctl(int* ctl, int mode, hipStream_t st);
+// p[i] = v for i < n (a kernel: no memset node when the stream is captured).
+hipError_t fill_f32(float* p, int64_t n, float v, hipStream_t st);
 // dst (bf16) = round-to-nearest-even(src), n elements.
 hipError_t f32_to_bf16(const float* src, void* dst, int64_t n, hipStream_t st);
 // dst [cols, rows] = src [rows, cols]^T for 16-bit elements; rows, cols multiples of 8.

@@ -288,9 +288,9 @@ struct Layout {
   int64_t P = 0;          // parameters
   int64_t T = 0;          // tokens per micro-batch
   int64_t ldz = 0;        // logits row stride (last stage)
-  size_t theta, G, m, v, theta16, theta16T = 0, chunks, zeros, ctl = 0;
+  size_t theta, G, m, v, theta16, theta16T = 0, chunks, zeros, ctl = 0, guard = 0;
   bool wT = false;             // transposed bf16 block weights kept (theta16T)
-  int nchunks = 0;
+  int nchunks = 0, nguard = 0;
   size_t stash, slot_bytes;
   int n_slots = 1;             // activation slots: delay + 1, or K + delay with windowed weight gradients
   bool window = false;         // weight gradients windowed over the K micro-batches of a window
@@ -328,10 +328,40 @@ constexpr int64_t CHUNK = 4096;   // AdamW elements per workgroup (many small wo
 uint32_t drop_threshold(const paci_shapes& s) { return (uint32_t)std::floor((double)s.dropout * 65536.0 + 0.5); }
 enum DropSite { SITE_EMBED = 0, SITE_ATTN = 1, SITE_PROJ = 2, SITE_FFN = 3 };
 
-int count_chunks(const ParamTable& p) {
-  int n = 0;
-  for (const auto& t : p.t) n += (int)((t.numel + CHUNK - 1) / CHUNK);
-  return n;
+// The AdamW table (paci::adamw): a range entry per CHUNK elements of a tensor, or,
+// for the block weight matrices of a stage that keeps them transposed (wT), one
+// 64 x 64 tile entry each, which also writes the tile's transposed bf16 values.
+// keep_g: the block matrices' G is not cleared by the update (the next window's
+// first backward overwrites it).
+bool is_block_matrix(const ParamTable& p, int64_t off) {
+  for (const BlockRefs& b : p.blocks)
+    if (off == b.w_qkv || off == b.w_o || off == b.w_1 || off == b.w_2) return true;
+  return false;
+}
+std::vector<int4> adamw_table(const ParamTable& p, bool wT, bool keep_g) {
+  std::vector<int4> v;
+  for (const auto& t : p.t) {
+    const bool bm = is_block_matrix(p, t.off);
+    const int flags = (t.decay ? paci::ADAMW_DECAY : 0) | ((keep_g && bm) ? 0 : paci::ADAMW_CLEAR_G);
+    if (wT && bm) {
+      for (int r0 = 0; r0 < t.rows; r0 += 64)
+        for (int c0 = 0; c0 < t.cols; c0 += 64)
+          v.push_back(int4{(int)t.off, (r0 << 16) | c0, flags | paci::ADAMW_TILE, (t.rows << 16) | t.cols});
+    } else {
+      for (int64_t b = 0; b < t.numel; b += CHUNK)
+        v.push_back(int4{(int)(t.off + b), (int)(t.off + std::min(t.numel, b + CHUNK)), flags, 0});
+    }
+  }
+  return v;
+}
+// Ranges the step's non-finite guard reads when the block matrices' G was
+// checked by the last backward of the window: every other tensor, in CHUNK pieces.
+std::vector<int2> guard_table(const ParamTable& p) {
+  std::vector<int2> v;
+  for (const auto& t : p.t)
+    if (!is_block_matrix(p, t.off))
+      for (int64_t b = 0; b < t.numel; b += CHUNK) v.push_back(int2{(int)(t.off + b), (int)(t.off + std::min(t.numel, b + CHUNK))});
+  return v;
 }
 
 Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) {
@@ -350,10 +380,13 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
   L.theta16 = s.dtype == PACI_BF16 ? a.take(2 * L.P) : 0;
   // bf16 stages: the block weight matrices also transposed ([in, out]), at the
   // same offsets, for the input-gradient GEMMs
-  L.wT = s.dtype == PACI_BF16 && d % 8 == 0 && f % 8 == 0;
+  // (tile entries of the AdamW table pack rows and columns in 16 bits each)
+  L.wT = s.dtype == PACI_BF16 && d % 8 == 0 && f % 8 == 0 && 3 * d < 32768 && f < 32768;
   L.theta16T = L.wT ? a.take(2 * L.P) : 0;
-  L.nchunks = count_chunks(p);
+  L.nchunks = (int)adamw_table(p, L.wT, false).size();
   L.chunks = a.take(16 * (size_t)L.nchunks);
+  L.nguard = (int)guard_table(p).size();
+  L.guard = a.take(8 * (size_t)std::max(1, L.nguard));
   L.zeros = a.take(256);  // never written after init: source of out-of-range GEMM tile slots
   L.ctl = a.take(256);    // update control: {G not finite, updates applied, updates skipped, 0}
 
@@ -485,6 +518,12 @@ struct paci_stage {
   int last_hip = 0;
   bool broken = false;
   int win_done = 0;   // micro-batches of the current window whose weight gradients are in G
+  // Grouped weight gradients (L.wdefer): after an update the block matrices' G is
+  // logically zero but not cleared; the next backward's products overwrite it.
+  bool g_lazy = false;
+  // the next step guards all of G (else only the ranges of L.guard: the last
+  // backward of the window checked the block matrices' G as it wrote it)
+  bool guard_full = true;
 
   // timing
   bool timing = false;
@@ -837,14 +876,28 @@ int flush_window(paci_stage* h) {
 // gradients it left in the window buffers and the activations of its slot
 // (table t), in one grouped launch: G_W += dY^T X for the four weights of each
 // block (Alg. 1's accumulate step for this backward).
-int wgrad_grouped(paci_stage* h, int t) {
+// overwrite: the block matrices' G is logically zero (after an update), so the
+// products are stored instead of added; flag: the window's last backward sets
+// the non-finite flag of the update control words if any sum it writes is not finite.
+int wgrad_grouped(paci_stage* h, int t, bool overwrite, int* flag) {
   const Layout& L = h->L;
   const double T = (double)L.T, d = h->s.d_model, f = h->s.d_ff;
   const double work = 2.0 * T * h->s.n_layers * (d * f + f * d + d * d + 3 * d * d);
   const auto* tab = reinterpret_cast<const paci::WgradProblem*>(h->arena + L.wgroup) + (size_t)t * L.wgroup_n;
   return run(h, F_GEMM_WGRAD, work, [&] {
-    return paci::gemm_wgrad_grouped(tab, L.wgroup_n, L.wgroup_tiles, (int)L.T, h->arena + L.zeros, h->st);
+    return paci::gemm_wgrad_grouped(tab, L.wgroup_n, L.wgroup_tiles, (int)L.T, h->arena + L.zeros, overwrite, flag,
+                                    h->st);
   });
+}
+
+// Makes a logically zero G of the block matrices zero in memory (before G is read).
+int materialize_g(paci_stage* h) {
+  if (!h->g_lazy) return PACI_OK;
+  for (const auto& t : h->p.t)
+    if (is_block_matrix(h->p, t.off))
+      TRY(run(h, F_COPY, 4.0 * (double)t.numel, [&] { return paci::fill_f32(h->g(t.off), t.numel, 0.f, h->st); }));
+  h->g_lazy = false;
+  return PACI_OK;
 }
 
 // Problem tables of the grouped launch, one per activation area a backward can read.
@@ -993,22 +1046,20 @@ extern "C" int paci_stage_init(const paci_shapes* s, int K, int delay, void* dev
     delete h;
     return PACI_E_UNSUPPORTED;
   }
-  // AdamW chunk table: chunks never cross a tensor boundary
-  std::vector<int32_t> chunks;
-  chunks.reserve(4 * (size_t)h->L.nchunks);
-  for (const auto& t : h->p.t)
-    for (int64_t b = 0; b < t.numel; b += CHUNK) {
-      chunks.push_back((int32_t)(t.off + b));
-      chunks.push_back((int32_t)(t.off + std::min(t.numel, b + CHUNK)));
-      chunks.push_back(t.decay ? 1 : 0);
-      chunks.push_back(0);
-    }
+  // AdamW table (entries never cross a tensor boundary) and the guard's ranges
+  const std::vector<int4> chunks = adamw_table(h->p, h->L.wT, h->L.wdefer);
+  const std::vector<int2> granges = guard_table(h->p);
+  h->g_lazy = h->L.wdefer;       // G starts zero either way
+  h->guard_full = !h->L.wdefer;
   hipError_t e = hipMemsetAsync(h->arena, 0, h->L.stash, h->st);  // theta, G, m, v, bf16 copy
   if (e == hipSuccess && h->L.fused_head)   // dz columns V .. ldz-1 stay zero (the dgrad reads them)
     e = hipMemsetAsync(h->arena + h->L.w_dz, 0, (size_t)h->esz * h->L.T * h->L.ldz, h->st);
   if (e == hipSuccess)
-    e = hipMemcpyAsync(h->arena + h->L.chunks, chunks.data(), chunks.size() * sizeof(int32_t),
-                       hipMemcpyHostToDevice, h->st);
+    e = hipMemcpyAsync(h->arena + h->L.chunks, chunks.data(), chunks.size() * sizeof(int4), hipMemcpyHostToDevice,
+                       h->st);
+  if (e == hipSuccess && !granges.empty())
+    e = hipMemcpyAsync(h->arena + h->L.guard, granges.data(), granges.size() * sizeof(int2), hipMemcpyHostToDevice,
+                       h->st);
   std::vector<paci::WgradProblem> tabs;
   if (h->L.wdefer) tabs = wgrad_tables(h);
   if (e == hipSuccess && !tabs.empty())
@@ -1050,7 +1101,13 @@ extern "C" int paci_stage_load(paci_stage* h, int what, const float* src, int64_
   if (h->broken) return PACI_E_HIP;
   float* dst = state_ptr(h, what);
   if (!dst) return PACI_E_INVAL;
-  if (what == PACI_GRADS) TRY(flush_window(h));   // pending products belong to the G being replaced
+  if (what == PACI_GRADS) {
+    TRY(flush_window(h));   // pending products belong to the G being replaced
+    // the loaded values are G as it stands: added to, and guarded in full at the next update
+    TRY(run(h, F_ADAMW, 0.0, [&] { return paci::adamw_ctl(reinterpret_cast<int*>(h->arena + h->L.ctl), 0, h->st); }));
+    h->g_lazy = false;
+    h->guard_full = true;
+  }
   hipError_t e = hipMemcpyAsync(dst, src, (size_t)n * 4, on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice,
                                 h->st);
   if (e == hipSuccess && what == PACI_PARAMS && h->dt == paci::DT_BF16) {
@@ -1070,7 +1127,10 @@ extern "C" int paci_stage_read(paci_stage* h, int what, float* dst, int64_t n, i
   if (h->broken) return PACI_E_HIP;
   const float* src = state_ptr(h, what);
   if (!src) return PACI_E_INVAL;
-  if (what == PACI_GRADS) TRY(flush_window(h));
+  if (what == PACI_GRADS) {
+    TRY(flush_window(h));
+    TRY(materialize_g(h));
+  }
   hipError_t e = hipMemcpyAsync(dst, src, (size_t)n * 4, on_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost,
                                 h->st);
   if (e == hipSuccess && !on_device) e = hipStreamSynchronize(h->st);
@@ -1192,7 +1252,11 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
     r = block_bwd(h, A, l, dy, dx, l < s.n_layers - 1 || s.kind == PACI_LAST, j, mb);
     dy = dx;
   }
-  if (!r && L.wdefer) r = wgrad_grouped(h, L.recompute ? 0 : mb % L.n_slots);
+  if (!r && L.wdefer) {
+    int* ctl = reinterpret_cast<int*>(h->arena + L.ctl);
+    r = wgrad_grouped(h, L.recompute ? 0 : mb % L.n_slots, h->g_lazy, h->fsm.c + 1 == h->fsm.K ? ctl : nullptr);
+    if (!r) h->g_lazy = false;
+  }
   if (!r && s.kind == PACI_FIRST && L.dropout) {   // through the embedding dropout
     r = dropout(h, dy, nullptr, h->ws(L.w_g2), h->drop(mb, 0, SITE_EMBED));
     dy = h->ws(L.w_g2);
@@ -1225,17 +1289,31 @@ extern "C" int paci_stage_step(paci_stage* h, int* new_version) {
   a.lr_total = s.lr_total;
   int* ctl = reinterpret_cast<int*>(h->arena + h->L.ctl);
   TRY(flush_window(h));
-  // the non-finite guard decides on the device: no host synchronization
-  TRY(run(h, F_ADAMW, 0.0, [&] { return paci::adamw_ctl(ctl, 0, h->st); }));
-  TRY(run(h, F_ADAMW, 4.0 * (double)h->p.total, [&] { return paci::adamw_guard(h->G(), h->p.total, ctl, h->st); }));
+  // the non-finite guard decides on the device: no host synchronization. The
+  // window's last backward already checked the block matrices' G as it wrote
+  // them (grouped weight gradients); the guard reads the rest, or all of G.
+  if (h->guard_full) {
+    TRY(run(h, F_ADAMW, 4.0 * (double)h->p.total, [&] { return paci::adamw_guard(h->G(), h->p.total, ctl, h->st); }));
+  } else {
+    double n = 0;
+    for (const auto& t : h->p.t)
+      if (!is_block_matrix(h->p, t.off)) n += (double)t.numel;
+    TRY(run(h, F_ADAMW, 4.0 * n, [&] {
+      return paci::adamw_guard_ranges(h->G(), reinterpret_cast<const int2*>(h->arena + h->L.guard), h->L.nguard, ctl,
+                                      h->st);
+    }));
+  }
   const int r = run(h, F_ADAMW, 30.0 * (double)h->p.total, [&] {
     return paci::adamw(h->theta(), h->G(), h->m(), h->v(),
                        h->dt == paci::DT_BF16 ? (void*)(h->arena + h->L.theta16) : nullptr,
+                       h->L.wT ? (void*)(h->arena + h->L.theta16T) : nullptr,
                        reinterpret_cast<const int4*>(h->arena + h->L.chunks), h->L.nchunks, a, ctl, h->st);
   });
   if (r) return r;
+  // counts the update as applied or skipped and clears the flag for the next window
   TRY(run(h, F_ADAMW, 0.0, [&] { return paci::adamw_ctl(ctl, 1, h->st); }));
-  TRY(refresh_wT(h));
+  h->g_lazy = h->L.wdefer;
+  h->guard_full = !h->L.wdefer;
   fsm_commit_step(h->fsm);
   h->win_done = 0;
   if (new_version) *new_version = h->fsm.t;

@@ -246,6 +246,58 @@ def test_nonfinite_gradient_skips_the_update(binding):
     st.close()
 
 
+@pytest.mark.parametrize("name", ["sched_bf16", "win_bf16", "dh64_fp32"])
+def test_nonfinite_gradient_from_a_backward(binding, name):
+    """A NaN that reaches G through a backward (in the output gradient of a
+    window's last micro-batch) skips that window's update: parameters and
+    moments bit for bit unchanged, G reads zero afterwards, and the next
+    window's update is AdamW's first on its own G (the default stage takes the
+    block matrices' flag from the last backward's weight-gradient products,
+    the windowed and fp32 stages from the guard pass over all of G)."""
+    import torch
+    c = small_cfg(name)
+    K = c["K"]
+    inp = Inputs(c, 9, 2 * K)
+    T, d = c["micro_batch"] * c["seq"], c["d_model"]
+    st = binding.Stage(c, K=K, delay=1)
+    st.load_params(inp.params)
+    xs = [to_torch(a) for a in inp.x_dev]
+    dys = [to_torch(a) for a in inp.dy_dev]
+    dys[K - 1][3, 5] = float("nan")
+    out = torch.zeros(T, d, dtype=st.act_dtype, device="cuda")
+    th0, m0, v0 = st.read(binding.PARAMS), st.read(binding.EXP_AVG), st.read(binding.EXP_AVG_SQ)
+
+    def window(i0):
+        st.forward(i0, xs[i0], out)
+        for i in range(i0, i0 + K):
+            if i + 1 < i0 + K:
+                st.forward(i + 1, xs[i + 1], out)
+            v, due = st.backward(i, dys[i])
+        assert due
+
+    window(0)
+    assert st.step() == 1
+    assert st.updates() == (0, 1)
+    assert np.array_equal(st.read(binding.PARAMS).view(np.uint32), th0.view(np.uint32))
+    assert np.array_equal(st.read(binding.EXP_AVG).view(np.uint32), m0.view(np.uint32))
+    assert np.array_equal(st.read(binding.EXP_AVG_SQ).view(np.uint32), v0.view(np.uint32))
+    assert not st.read(binding.GRADS).any()
+    window(K)
+    G2 = unflatten(c, st.read(binding.GRADS))
+    assert all(np.isfinite(g).all() for g in G2.values())
+    assert st.step() == 2
+    assert st.updates() == (1, 1)
+    th0d = unflatten(c, th0)
+    th, m, v = (unflatten(c, st.read(w)) for w in (binding.PARAMS, binding.EXP_AVG, binding.EXP_AVG_SQ))
+    for n in th:
+        g = np.asarray(G2[n], np.float64)
+        th_x, m_x, v_x = adamw_np(np.asarray(th0d[n], np.float64), g, np.zeros_like(g), np.zeros_like(g), 1, c,
+                                  ostage.decayed(n))
+        e = max(rel_err(th[n], th_x), rel_err(m[n], m_x), rel_err(v[n], v_x))
+        assert e <= 1e-5, f"{n}: {e:.3e}"
+    st.close()
+
+
 @pytest.mark.parametrize("name", ["dh32_bf16", "tiny_fp32"])
 def test_flush_schedule_parity(binding, name):
     """Synchronous 1F1B with a flush per window (Delta = 0 everywhere): the
