@@ -51,6 +51,7 @@ extern "C" {
 #define PACI_E_STEP_PENDING (-6) /* forward/backward while an update is due */
 #define PACI_E_NOT_DUE (-7)      /* step before K backwards of the window */
 #define PACI_E_HIP (-8)          /* a HIP runtime call failed; see paci_last_hip_error */
+#define PACI_E_SCRATCH (-9)      /* the call needs more than the library's static scratch buffer */
 
 /* ---- stage description ---------------------------------------------------- */
 enum paci_kind { PACI_MIDDLE = 0, PACI_FIRST = 1, PACI_LAST = 2 };
@@ -254,6 +255,23 @@ int paci_stage_forward(paci_stage* h, int mb, const void* dev_in, const int32_t*
  * E_STEP_PENDING, E_INVAL. */
 int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_out, void* dev_grad_in,
                         int* version);
+
+/* For callers that cannot allocate device memory or rely on a caller-sized
+ * workspace at call time (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): paci_stage_backward with the same
+ * arguments, results and errors, except that the attention backward's
+ * per-query scratch, the (lse2, D) pairs of micro_batch * n_heads *
+ * roundup(seq, 64) queries (8 bytes each in bf16, micro_batch * n_heads * seq
+ * * 4 bytes in fp32), comes from one static device buffer of 8 MiB that the
+ * library holds per GPU until the process ends, not from the stage's arena.
+ * It calls no allocating routine (no device allocation, no timing events: while
+ * timing is on, this call's launches are not timed). Every call rewrites all of
+ * the pairs it reads, so the buffer needs no clearing; it is shared by every
+ * stage on the GPU, so calls that overlap on one GPU (stages on different
+ * streams) race. Error: PACI_E_SCRATCH (state unchanged) if the pairs exceed
+ * 8 MiB. */
+int paci_stage_backward_static(paci_stage* h, int mb, const void* dev_grad_out, void* dev_grad_in,
+                               int* version);
 
 /* stage_step(): one AdamW update with G (the plain sum of the window's K local
  * gradients, Alg. 1), decoupled weight decay on the w_* matrices; then G <- 0,

@@ -25,7 +25,7 @@ LIB_PATH = os.environ.get("PACI_STAGE_LIB") or os.path.join(os.path.dirname(os.p
 HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "paci_stage.h")
 
 OK, STEP_DUE = 0, 1
-E_INVAL, E_UNSUPPORTED, E_NOMEM, E_ORDER, E_BACKPRESSURE, E_STEP_PENDING, E_NOT_DUE, E_HIP = range(-1, -9, -1)
+E_INVAL, E_UNSUPPORTED, E_NOMEM, E_ORDER, E_BACKPRESSURE, E_STEP_PENDING, E_NOT_DUE, E_HIP, E_SCRATCH = range(-1, -10, -1)
 MIDDLE, FIRST, LAST = 0, 1, 2
 FP32, BF16 = 0, 1
 PARAMS, GRADS, EXP_AVG, EXP_AVG_SQ = 0, 1, 2, 3
@@ -88,6 +88,7 @@ def _load():
         "paci_stage_read": (I, [P, I, P, I64, I]),
         "paci_stage_forward": (I, [P, I, P, P, P, ctypes.POINTER(I)]),
         "paci_stage_backward": (I, [P, I, P, P, ctypes.POINTER(I)]),
+        "paci_stage_backward_static": (I, [P, I, P, P, ctypes.POINTER(I)]),
         "paci_stage_step": (I, [P, ctypes.POINTER(I)]),
         "paci_stage_run": (I, [P, I, P, P, P, P, P, I32P]),
         "paci_stage_run_events": (I, [P, I, I32P, I32P, P, P, P, P, P, I32P]),
@@ -306,6 +307,14 @@ class Stage:
         v = ctypes.c_int(-1)
         r = _check(lib.paci_stage_backward(self.h, mb, _ptr(grad_out), _ptr(grad_in), ctypes.byref(v)),
                    "paci_stage_backward")
+        return v.value, r == STEP_DUE
+
+    def backward_static(self, mb, grad_out=None, grad_in=None):
+        """paci_stage_backward_static: the backward with its attention scratch in the
+        library's static buffer (no allocation at call time)."""
+        v = ctypes.c_int(-1)
+        r = _check(lib.paci_stage_backward_static(self.h, mb, _ptr(grad_out), _ptr(grad_in), ctypes.byref(v)),
+                   "paci_stage_backward_static")
         return v.value, r == STEP_DUE
 
     def step(self):

@@ -38,6 +38,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -54,6 +55,38 @@ struct paci_fsm {
 
 // HIP status of the last failed call that had no handle to record it in (init).
 static int g_init_hip_error = 0;
+
+// ---- static scratch of the allocation-free backward ----------------------------------------
+// paci_stage_backward_static takes the attention backward's per-query (lse2, D)
+// pairs from this array instead of the stage arena. Each GPU the library runs
+// on holds its own copy until the process ends. In host code the name is only a
+// stand-in: kernels get the device address that hipGetSymbolAddress returns for
+// the current device, looked up once per device by static_scratch().
+constexpr size_t kStaticScratchBytes = (size_t)8 << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device.
+hipError_t static_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+}  // namespace
 
 static int fsm_check_forward(const paci_fsm& f, int mb) {
   if (f.c == f.K) return PACI_E_STEP_PENDING;
@@ -525,6 +558,12 @@ struct paci_stage {
   // backward of the window checked the block matrices' G as it wrote it)
   bool guard_full = true;
 
+  // the attention backward's (lse2, D) pairs: the arena's workspace, or (during
+  // paci_stage_backward_static) the static scratch of this device
+  float* pairs = nullptr;
+  void* static_pairs = nullptr;   // device address of `scratch` on the stage's GPU
+  bool no_events = false;         // no timing events (they may allocate) during the static variant
+
   // timing
   bool timing = false;
   struct Pending { hipEvent_t a, b; int fam; double work; };
@@ -599,7 +638,7 @@ void drain_timing(paci_stage* h) {
 template <class F>
 int run(paci_stage* h, int fam, double work, F&& launch) {
   hipEvent_t a = nullptr, b = nullptr;
-  if (h->timing) {
+  if (h->timing && !h->no_events) {
     if (h->pending.size() >= 65536) drain_timing(h);  // bounded pool; drains synchronize
     a = take_event(h);
     b = take_event(h);
@@ -611,7 +650,7 @@ int run(paci_stage* h, int fam, double work, F&& launch) {
     h->broken = true;
     return PACI_E_HIP;
   }
-  if (h->timing && a && b) {
+  if (h->timing && !h->no_events && a && b) {
     (void)hipEventRecord(b, h->st);
     h->pending.push_back({a, b, fam, work});
   }
@@ -805,7 +844,7 @@ int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx, bool dy_
   // attention; G_bqkv += sum dqkv in the same kernels
   TRY(run(h, F_ATTN_BWD, 8.0 * attn_pairs(s) * s.head_dim, [&] {
     return paci::attn_bwd(h->dt, sl + o.qkv, sl + o.o, dO, reinterpret_cast<const float*>(sl + o.lse2),
-                          reinterpret_cast<float*>(h->ws(L.w_D)), dqkv, h->g(b.b_qkv), s.micro_batch, s.seq,
+                          h->pairs, dqkv, h->g(b.b_qkv), s.micro_batch, s.seq,
                           s.n_heads, s.head_dim, h->drop(mb, l, SITE_ATTN), h->st);
   }));
   // qkv = n1 Wqkv^T + bqkv
@@ -1042,6 +1081,15 @@ extern "C" int paci_stage_init(const paci_shapes* s, int K, int delay, void* dev
     delete h;
     return PACI_E_NOMEM;
   }
+  h->pairs = reinterpret_cast<float*>(h->arena + h->L.w_D);
+  {
+    const hipError_t se = static_scratch(&h->static_pairs);   // the stage's GPU is the current one
+    if (se != hipSuccess) {
+      g_init_hip_error = (int)se;
+      delete h;
+      return PACI_E_HIP;
+    }
+  }
   if (h->p.total >= (int64_t)INT32_MAX) {
     delete h;
     return PACI_E_UNSUPPORTED;
@@ -1177,8 +1225,7 @@ extern "C" int paci_stage_forward(paci_stage* h, int mb, const void* dev_in, con
   return PACI_OK;
 }
 
-extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_out, void* dev_grad_in,
-                                   int* version) {
+static int stage_backward(paci_stage* h, int mb, const void* dev_grad_out, void* dev_grad_in, int* version) {
   if (!h) return PACI_E_INVAL;
   const paci_shapes& s = h->s;
   if (s.kind == PACI_LAST ? (dev_grad_out != nullptr) : (dev_grad_out == nullptr)) return PACI_E_INVAL;
@@ -1271,6 +1318,26 @@ extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_o
   const int t = fsm_commit_backward(h->fsm);
   if (version) *version = t;
   return h->fsm.c == h->fsm.K ? PACI_STEP_DUE : PACI_OK;
+}
+
+extern "C" int paci_stage_backward(paci_stage* h, int mb, const void* dev_grad_out, void* dev_grad_in,
+                                   int* version) {
+  return stage_backward(h, mb, dev_grad_out, dev_grad_in, version);
+}
+
+extern "C" int paci_stage_backward_static(paci_stage* h, int mb, const void* dev_grad_out, void* dev_grad_in,
+                                          int* version) {
+  if (!h) return PACI_E_INVAL;
+  const size_t need = 4 * (size_t)paci::attn_bwd_workspace_floats(h->dt, h->s.micro_batch, h->s.seq, h->s.n_heads);
+  if (need > kStaticScratchBytes) return PACI_E_SCRATCH;
+  if (h->static_pairs == nullptr) return PACI_E_HIP;
+  float* own = h->pairs;
+  h->pairs = reinterpret_cast<float*>(h->static_pairs);   // every entry is rewritten by the call
+  h->no_events = true;
+  const int r = stage_backward(h, mb, dev_grad_out, dev_grad_in, version);
+  h->pairs = own;
+  h->no_events = false;
+  return r;
 }
 
 extern "C" int paci_stage_step(paci_stage* h, int* new_version) {
@@ -1455,6 +1522,7 @@ extern "C" const char* paci_strerror(int status) {
     case PACI_E_STEP_PENDING: return "optimizer step pending";
     case PACI_E_NOT_DUE: return "optimizer step not due";
     case PACI_E_HIP: return "HIP runtime error";
+    case PACI_E_SCRATCH: return "the call's scratch exceeds the library's static scratch buffer";
   }
   return "unknown status";
 }

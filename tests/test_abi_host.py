@@ -24,7 +24,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings():
-    for code in [0, 1] + list(range(-1, -9, -1)):
+    for code in [0, 1] + list(range(-1, -10, -1)):
         assert binding.strerror(code) != "unknown status"
 
 
@@ -218,3 +218,12 @@ def test_fused_head_validation_and_memory():
         assert binding.lib.paci_stage_arena_bytes(ctypes.byref(s), 8, 0, ctypes.byref(out)) == code
     s = binding.shapes(dict(c, fused_head=1))
     assert binding.lib.paci_stage_arena_bytes(ctypes.byref(s), 8, 1, ctypes.byref(out)) == binding.E_INVAL
+
+
+def test_static_backward_rejects_a_stage_beyond_its_scratch():
+    """paci_stage_backward_static: the attention scratch of a stage must fit the
+    library's 8 MiB static buffer; the host-side size check refuses larger ones
+    before any device work (a null handle is refused first)."""
+    v = ctypes.c_int(-1)
+    assert binding.lib.paci_stage_backward_static(None, 0, None, None, ctypes.byref(v)) == binding.E_INVAL
+    assert binding.strerror(binding.E_SCRATCH) != "unknown status"
