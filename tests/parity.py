@@ -110,6 +110,10 @@ def small_cfg(name, **kw):
         # full-size window products split mid-segment
         "winsplit_bf16": dict(kind="middle", n_layers=1, d_model=128, n_heads=2, head_dim=64, d_ff=256, seq=160,
                               micro_batch=2, K=7, delay=2, M=14, dtype="bf16", window=1),
+        # FFN width 2304 at T = 4096: the FFN1 forward and FFN2 input-gradient products
+        # have 288 tiles of 256 x 128, more than the 256 CUs (a second, partial round)
+        "wide_bf16": dict(kind="middle", n_layers=1, d_model=256, n_heads=4, head_dim=64, d_ff=2304, seq=512,
+                          micro_batch=8, K=2, delay=1, M=6, dtype="bf16"),
         # the same shapes as win8_bf16 on the default stage (per-backward accumulation)
         "acc8_bf16": dict(kind="middle", n_layers=1, d_model=128, n_heads=2, head_dim=64, d_ff=256, seq=512,
                           micro_batch=2, K=8, delay=2, M=16, dtype="bf16"),
