@@ -661,13 +661,16 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
   __shared__ u32x4 smem[CF::SMEM_SLOTS];
   const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
   int pid = blockIdx.x;
+  int xcd_m = 0;   // grouped weight gradients: XCD blocks of the tile grid (0: generic order)
   if constexpr (GRP) {
     // grouped weight gradients: find this workgroup's problem (wave-uniform scalar loads)
     int p = 0;
     while (p + 1 < a.group_n && pid >= a.group[p + 1].tile0) ++p;
     const WgradProblem& pr = a.group[p];
     pid -= pr.tile0;
-    if (pid >= ((pr.M + BM - 1) / BM) * ((pr.N + BN - 1) / BN)) return;   // padding to a multiple of 8
+    const int tm_all = (pr.M + BM - 1) / BM, tn_all = (pr.N + BN - 1) / BN;
+    if (pid >= tm_all * tn_all) return;   // padding to a multiple of 8
+    xcd_m = pr.xcd_m;
     a.A = pr.A;
     a.B = pr.B;
     a.C = pr.C;
@@ -679,7 +682,15 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
   }
   const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.N + BN - 1) / BN;
   int tm, tn;
-  tile_coords(pid, tiles_m, tiles_n, tm, tn);
+  if (xcd_m > 0) {
+    // XCD x = pid % 8 takes block (x % xcd_m, x / xcd_m) of bm x bn tiles, column by column
+    const int x = pid & 7, k = pid >> 3;
+    const int bm = tiles_m / xcd_m, bn = tiles_n / (8 / xcd_m);
+    tm = (x % xcd_m) * bm + k % bm;
+    tn = (x / xcd_m) * bn + k / bm;
+  } else {
+    tile_coords(pid, tiles_m, tiles_n, tm, tn);
+  }
   const int m0 = tm * BM, n0 = tn * BN;
   const int k_begin = blockIdx.y * k_per_split;
   const int k_end = min(a.K, k_begin + k_per_split);
@@ -980,6 +991,23 @@ void gemm_set_tile_override(int cfg) { g_tile_override = cfg; }
 // plain fp32 read-modify-write of each output tile.
 int wgrad_group_tiles(int M, int N) {
   return ((M + P256x128::BM - 1) / P256x128::BM) * ((N + P256x128::BN - 1) / P256x128::BN);
+}
+
+int wgrad_group_xcd_m(int M, int N, int K) {
+  const int tm = (M + P256x128::BM - 1) / P256x128::BM, tn = (N + P256x128::BN - 1) / P256x128::BN;
+  int best = 0;
+  double best_bytes = 0;
+  for (int xm = 1; xm <= 8; xm *= 2) {
+    const int xn = 8 / xm;
+    if (tm % xm || tn % xn) continue;
+    // panels one XCD reads: its bm row tiles of A and bn column tiles of B over K rows
+    const double bytes = (double)K * 2.0 * ((tm / xm) * P256x128::BM + (tn / xn) * P256x128::BN);
+    if (best == 0 || bytes < best_bytes) {
+      best = xm;
+      best_bytes = bytes;
+    }
+  }
+  return best;
 }
 
 hipError_t gemm_wgrad_grouped(const WgradProblem* probs, int n, int total_tiles, int K, const void* zeros,

@@ -47,11 +47,14 @@ enum GemmEpi { EPI_STORE = 0, EPI_BIAS, EPI_BIAS_RES, EPI_BIAS_GELU, EPI_GELU_GR
 // holding n problems; tile0 is the problem's first workgroup, a multiple of 8
 // (wgrad_group_tiles gives each problem's count; workgroups past a problem's
 // tiles exit). M_p, N_p, K multiples of 8 and 16-byte aligned operands.
+// xcd_m: 0, or the number of row bands of the problem's tile grid when it is
+// split into 8 equal blocks (xcd_m bands x 8 / xcd_m column bands), one per XCD
+// (see wgrad_group_xcd_m).
 struct WgradProblem {
   const void* A;
   const void* B;
   float* C;
-  int M, N, tile0, pad;
+  int M, N, tile0, xcd_m;
 };
 struct GemmArgs {
   const void* A; int64_t lda;
@@ -86,6 +89,12 @@ struct GemmArgs {
 // overwrite: C_p = A_p^T B_p instead of +=; nonfinite (nullable): set to 1 (a plain
 // store) if any element written is NaN or infinite.
 int wgrad_group_tiles(int M, int N);
+// Workgroup w of a problem runs on XCD w % 8. Each XCD streams the operand
+// panels of the tiles it runs through its own L2, so the launch gives each XCD
+// one block of the tile grid: the split of the grid into 8 equal blocks (xcd_m
+// row bands) that reads the fewest panel bytes per XCD, or 0 if the grid does
+// not split evenly (then the generic XCD-aware order applies). K contracted rows.
+int wgrad_group_xcd_m(int M, int N, int K);
 hipError_t gemm_wgrad_grouped(const WgradProblem* probs, int n, int total_tiles, int K, const void* zeros,
                               bool overwrite, int* nonfinite, hipStream_t st);
 

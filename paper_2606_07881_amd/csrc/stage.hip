@@ -962,7 +962,7 @@ std::vector<paci::WgradProblem> wgrad_tables(const paci_stage* h) {
         pr.M = e.M;
         pr.N = e.N;
         pr.tile0 = tile0;
-        pr.pad = 0;
+        pr.xcd_m = paci::wgrad_group_xcd_m(e.M, e.N, (int)L.T);
         v.push_back(pr);
         tile0 += (paci::wgrad_group_tiles(e.M, e.N) + 7) / 8 * 8;
       }

@@ -31,13 +31,15 @@ FAMILIES = {
                  "gemm_pipe_kernel<bool _Accum, bool, E, true, 3"],
     "gemm_dgrad": ["gemm_pipe_kernel<bool _Accum, bool, E, true, 0", "gemm_pipe_kernel<bool _Accum, bool, E, true, 4",
                    "gemm_pipe_kernel<bool _Accum, bool, E, false, 0", "gemm_pipe_kernel<bool _Accum, bool, E, false, 4"],
-    "gemm_wgrad_acc": ["gemm_pipe_kernel<float, false, false, 5", "gemm_pipe_kernel<float, false, false, 6"],
+    "gemm_wgrad_acc": ["gemm_pipe_kernel<float, false, false, 5", "gemm_pipe_kernel<float, false, false, 6",
+                       "gemm_pipe_kernel<float, false, false, 0"],
     "attn_fwd": ["attn_fwd_ring_kernel"],
     "attn_bwd": ["attn_pairs_kernel", "attn_dkdv_ring_kernel", "attn_dq_ring_kernel"],
     "layernorm_fwd": ["ln_fwd_kernel"],
     "layernorm_bwd": ["ln_bwd_kernel", "colsum_atomic_kernel<bool _Accum, bool, E>"],
     "bias_grad": ["colsum_atomic_kernelIDF16bLb0E"],
-    "adamw": ["adamw_kernel", "guard_kernel", "ctl_kernel", "transpose16_kernel"],
+    "adamw": ["adamw_kernel", "guard_kernel", "guard_ranges_kernel", "ctl_kernel", "transpose16_kernel"],
+    "copy": ["fill_f32_kernel"],
 }
 # families whose launch runs each of its kernels once; every other family runs
 # one of its kernels (an epilogue or shape variant) per launch

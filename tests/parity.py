@@ -114,6 +114,10 @@ def small_cfg(name, **kw):
         # have 288 tiles of 256 x 128, more than the 256 CUs (a second, partial round)
         "wide_bf16": dict(kind="middle", n_layers=1, d_model=256, n_heads=4, head_dim=64, d_ff=2304, seq=512,
                           micro_batch=8, K=2, delay=1, M=6, dtype="bf16"),
+        # d 512, FFN 2048: every weight's tile grid of the grouped weight-gradient launch
+        # splits into 8 equal blocks, one per XCD (W_qkv 6 x 4 and W_o 2 x 4 tiles of 256 x 128)
+        "xcd_bf16": dict(kind="middle", n_layers=1, d_model=512, n_heads=8, head_dim=64, d_ff=2048, seq=128,
+                         micro_batch=2, K=2, delay=1, M=4, dtype="bf16"),
         # the same shapes as win8_bf16 on the default stage (per-backward accumulation)
         "acc8_bf16": dict(kind="middle", n_layers=1, d_model=128, n_heads=2, head_dim=64, d_ff=256, seq=512,
                           micro_batch=2, K=8, delay=2, M=16, dtype="bf16"),
