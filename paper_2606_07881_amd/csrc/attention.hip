@@ -638,11 +638,15 @@ __global__ void __launch_bounds__(NT) attn_bwd_dq_kernel(const T* qkv, const T* 
 //   dQ     per 64 * SUB queries (Q and dO fragments in registers), streaming
 //          64-key blocks of K and V: S^T, dP^T with the query in the lane, then
 //          dQ^T += K^T dS^T, K^T by transpose reads.
-// head_dim 64: 8 wavefronts of 32 rows (two per SIMD, so one's softmax VALU work
-// overlaps the other's MFMAs); 128: 8 of 16 rows; 32: 4 of 64 rows.
+// head_dim 64: workgroups of 4 wavefronts of 32 rows, two per CU. Each has its
+// own barrier, so the two wavefronts of a SIMD drift apart and one's softmax
+// VALU work overlaps the other's MFMAs (one workgroup of 8 wavefronts per CU
+// keeps them in step: 9% slower for dK/dV, 4% for dQ). 128: 8 of 16 rows;
+// 32: 4 of 64 rows.
 template <int DH> struct BwdRing {
   static constexpr int CPR = DH / 8, KST = DH / 32;
-  static constexpr int SUB = DH == 32 ? 4 : (DH == 64 ? 2 : 1), WAVES = DH == 32 ? 4 : 8, NTB = 64 * WAVES;
+  static constexpr int SUB = DH == 32 ? 4 : (DH == 64 ? 2 : 1), WAVES = DH == 128 ? 8 : 4, NTB = 64 * WAVES;
+  static constexpr int OCC = DH == 32 ? 1 : 2;   // wavefronts per SIMD the register budget must allow
   static constexpr int WR = 16 * SUB, BR = WAVES * WR;
   static constexpr int NS = 4;
   static constexpr int BLK = 64 * CPR;
@@ -711,7 +715,7 @@ __device__ __forceinline__ void colsum_tiles(float (&v)[NCOL / 16][4], float* re
 }
 
 template <int DH, bool DROP>
-__global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn_dkdv_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
+__global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::OCC) attn_dkdv_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
                                                                 bf16* dqkv, int S, int S_pad, int H, int d,
                                                                 float scale_log2, float scale, float* gbias,
                                                                 DropArgs drop) {
@@ -887,7 +891,7 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn
 }
 
 template <int DH, bool DROP>
-__global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::WAVES / 4) attn_dq_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
+__global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::OCC) attn_dq_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
                                                               bf16* dqkv, int S, int S_pad, int H, int d,
                                                               float scale_log2, float scale, float* gbias,
                                                               DropArgs drop) {

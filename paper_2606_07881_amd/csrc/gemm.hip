@@ -910,11 +910,13 @@ hipError_t launch(const GemmArgs& a, int splits, hipStream_t st) {
         case 10: return launch_pipe<TO, AK, BK, EPI, P256x128>(a, splits, st);
         case 13: return launch_pipe<TO, AK, BK, EPI, P128x128o2>(a, splits, st);
         default:
-          // weight gradients (both operands MN-major): 128 x 128 tiles, two
-          // workgroups per CU, so one's epilogue overlaps the other's loop;
-          // forward and dgrad: 256 x 128 tiles, which re-read the weights
-          // half as often (measured faster inside the stage)
-          if constexpr (!AK) return launch_pipe<TO, AK, BK, EPI, P128x128o2>(a, splits, st);
+          // weight gradients (both operands MN-major) and the input gradient
+          // that reads u and writes du: 128 x 128 tiles, two workgroups per
+          // CU, so one's epilogue overlaps the other's loop (3-6% faster for
+          // the latter, slower for the other forward and input-gradient
+          // products); the rest: 256 x 128 tiles, which re-read the weights
+          // half as often
+          if constexpr (!AK || EPI == EPI_GELU_GRAD) return launch_pipe<TO, AK, BK, EPI, P128x128o2>(a, splits, st);
           else return launch_pipe<TO, AK, BK, EPI, P256x128>(a, splits, st);
       }
     }
