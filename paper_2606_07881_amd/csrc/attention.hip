@@ -629,8 +629,9 @@ __global__ void __launch_bounds__(NT) attn_bwd_dq_kernel(const T* qkv, const T* 
 
 // ---------------------------------------------------------------------------------------
 // Backward, bf16. A pre-pass writes (lse2, D) pairs per query into a buffer
-// padded to 64 queries per head, so the kernels can copy them with the blocks.
-// Both kernels then recompute P from q, k and lse2 (no atomics):
+// padded to 64 queries per head, so the workgroups can copy them with the
+// blocks. Two kinds of workgroup, in one launch, then recompute P from q, k and
+// lse2 (no atomics):
 //   dK/dV  per 64 * SUB keys of a wavefront (K and V fragments in registers),
 //          streaming 64-query blocks of Q, dO and their pairs through the ring:
 //          S = Q K^T and dP = dO V^T with the key in the lane, then
@@ -714,16 +715,14 @@ __device__ __forceinline__ void colsum_tiles(float (&v)[NCOL / 16][4], float* re
   }
 }
 
+// dK/dV of key block kb (ring: NS * STAGE slots of LDS)
 template <int DH, bool DROP>
-__global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::OCC) attn_dkdv_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
-                                                                bf16* dqkv, int S, int S_pad, int H, int d,
-                                                                float scale_log2, float scale, float* gbias,
-                                                                DropArgs drop) {
+__device__ __forceinline__ void dkdv_ring_body(u32x4* ring, int kb, const bf16* qkv, const bf16* dO,
+                                               const float* pairs, bf16* dqkv, int S, int S_pad, int H, int d,
+                                               float scale_log2, float scale, float* gbias, const DropArgs& drop) {
   using C = BwdRing<DH>;
   constexpr int SUB = C::SUB, KST = C::KST, NS = C::NS, CPR = C::CPR;
-  __shared__ u32x4 ring[NS * C::STAGE];
   static_assert(NS * C::STAGE * 4 >= C::WAVES * 2 * DH, "LDS for the column sums");
-  const int kb = blockIdx.y;                     // smallest keys first: they see the most queries
   const int bh = blockIdx.x, b = bh / H, h = bh % H;
   const int w = threadIdx.x >> 6, l = lane_id(), g = l >> 4;
   const int wu = __builtin_amdgcn_readfirstlane(w);
@@ -890,17 +889,16 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::OCC) attn_dkdv_
   }
 }
 
+// dQ of query block nqb - 1 - yb (ring: NS * 2 * BLK slots of LDS)
 template <int DH, bool DROP>
-__global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::OCC) attn_dq_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
-                                                              bf16* dqkv, int S, int S_pad, int H, int d,
-                                                              float scale_log2, float scale, float* gbias,
-                                                              DropArgs drop) {
+__device__ __forceinline__ void dq_ring_body(u32x4* ring, int yb, const bf16* qkv, const bf16* dO,
+                                             const float* pairs, bf16* dqkv, int S, int S_pad, int H, int d,
+                                             float scale_log2, float scale, float* gbias, const DropArgs& drop) {
   using C = BwdRing<DH>;
   constexpr int SUB = C::SUB, KST = C::KST, NS = C::NS, CPR = C::CPR;
-  __shared__ u32x4 ring[NS * 2 * C::BLK];
   static_assert(NS * 2 * C::BLK * 4 >= C::WAVES * DH, "LDS for the column sums");
   const int nqb = (S + C::BR - 1) / C::BR;
-  const int qb = nqb - 1 - blockIdx.y;           // largest queries first: they see the most keys
+  const int qb = nqb - 1 - yb;                   // largest queries first: they see the most keys
   const int bh = blockIdx.x, b = bh / H, h = bh % H;
   const int w = threadIdx.x >> 6, l = lane_id(), g = l >> 4;
   const int wu = __builtin_amdgcn_readfirstlane(w);
@@ -1039,6 +1037,25 @@ __global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::OCC) attn_dq_ri
   }
 }
 
+// The backward kernel: dK/dV and dQ in one launch (grid y below ny: dK/dV of key
+// block y, smallest keys first; the rest: dQ, largest queries first), so that
+// the tail of the dK/dV blocks overlaps the first dQ blocks and the two share
+// CUs (7% faster than two launches at head dim 64).
+template <int DH, bool DROP>
+__global__ void __launch_bounds__(BwdRing<DH>::NTB, BwdRing<DH>::OCC) attn_bwd_ring_kernel(const bf16* qkv, const bf16* dO, const float* pairs,
+                                                               bf16* dqkv, int S, int S_pad, int H, int d,
+                                                               float scale_log2, float scale, float* gbias,
+                                                               DropArgs drop, int ny) {
+  using C = BwdRing<DH>;
+  constexpr int SLOTS = C::STAGE > 2 * C::BLK ? C::NS * C::STAGE : C::NS * 2 * C::BLK;
+  __shared__ u32x4 ring[SLOTS];
+  if ((int)blockIdx.y < ny)
+    dkdv_ring_body<DH, DROP>(ring, blockIdx.y, qkv, dO, pairs, dqkv, S, S_pad, H, d, scale_log2, scale, gbias, drop);
+  else
+    dq_ring_body<DH, DROP>(ring, blockIdx.y - ny, qkv, dO, pairs, dqkv, S, S_pad, H, d, scale_log2, scale, gbias,
+                           drop);
+}
+
 template <typename T, int DH>
 hipError_t fwd_launch(const void* qkv, void* o, float* lse2, int mu, int S, int H, const DropArgs& drop,
                       hipStream_t st) {
@@ -1085,21 +1102,14 @@ hipError_t bwd_launch(const void* qkv, const void* o, const void* dO, const floa
                        reinterpret_cast<const bf16*>(o), g, lse2, Dbuf, S, S_pad, H, d, rows);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const dim3 grid(mu * H, (S + C::BR - 1) / C::BR);
+    const int ny = (S + C::BR - 1) / C::BR;
+    const dim3 grid(mu * H, 2 * ny);   // dK/dV blocks, then dQ blocks
     if (drop.thr)
-      hipLaunchKernelGGL((attn_dkdv_ring_kernel<DH, true>), grid, dim3(C::NTB), 0, st, q, g, Dbuf, dq, S, S_pad, H, d,
-                         scale_log2, scale, gbias, drop);
+      hipLaunchKernelGGL((attn_bwd_ring_kernel<DH, true>), grid, dim3(C::NTB), 0, st, q, g, Dbuf, dq, S, S_pad, H, d,
+                         scale_log2, scale, gbias, drop, ny);
     else
-      hipLaunchKernelGGL((attn_dkdv_ring_kernel<DH, false>), grid, dim3(C::NTB), 0, st, q, g, Dbuf, dq, S, S_pad, H, d,
-                         scale_log2, scale, gbias, drop);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    if (drop.thr)
-      hipLaunchKernelGGL((attn_dq_ring_kernel<DH, true>), grid, dim3(C::NTB), 0, st, q, g, Dbuf, dq, S, S_pad, H, d,
-                         scale_log2, scale, gbias, drop);
-    else
-      hipLaunchKernelGGL((attn_dq_ring_kernel<DH, false>), grid, dim3(C::NTB), 0, st, q, g, Dbuf, dq, S, S_pad, H, d,
-                         scale_log2, scale, gbias, drop);
+      hipLaunchKernelGGL((attn_bwd_ring_kernel<DH, false>), grid, dim3(C::NTB), 0, st, q, g, Dbuf, dq, S, S_pad, H, d,
+                         scale_log2, scale, gbias, drop, ny);
     return hipGetLastError();
   }
   constexpr int LPR = DH / Vec<T>::V;

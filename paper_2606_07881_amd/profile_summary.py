@@ -34,7 +34,7 @@ FAMILIES = {
     "gemm_wgrad_acc": ["gemm_pipe_kernel<float, false, false, 5", "gemm_pipe_kernel<float, false, false, 6",
                        "gemm_pipe_kernel<float, false, false, 0"],
     "attn_fwd": ["attn_fwd_ring_kernel"],
-    "attn_bwd": ["attn_pairs_kernel", "attn_dkdv_ring_kernel", "attn_dq_ring_kernel"],
+    "attn_bwd": ["attn_pairs_kernel", "attn_bwd_ring_kernel"],
     "layernorm_fwd": ["ln_fwd_kernel"],
     "layernorm_bwd": ["ln_bwd_kernel", "colsum_atomic_kernel<bool _Accum, bool, E>"],
     "bias_grad": ["colsum_atomic_kernelIDF16bLb0E"],
