@@ -656,27 +656,38 @@ template <int DH> struct BwdRing {
   static constexpr int L = 2 * BLK / NTB;          // block loads per thread per stage (wave 0 adds the pairs)
 };
 
+// (lse2, D) pairs: LPR threads per (token, head) row, PAIR_ROWS consecutive
+// rows per thread group with all their loads issued first.
+constexpr int PAIR_ROWS = 2;
 template <int DH>
 __global__ void __launch_bounds__(NT) attn_pairs_kernel(const bf16* o, const bf16* dO, const float* lse2, float* pairs,
                                                          int S, int S_pad, int H, int d, int64_t rows) {
   constexpr int LPR = DH / 8;
   const int64_t gid = (int64_t)blockIdx.x * NT + threadIdx.x;
-  const int64_t row = gid / LPR;  // row = token * H + h
+  const int64_t row0 = gid / LPR * PAIR_ROWS;  // row = token * H + h
   const int part = gid % LPR;
-  float sum = 0.f;
-  if (row < rows) {
-    const int64_t off = (row / H) * d + (row % H) * DH + part * 8;
-    const u32x4 a = ld16(o + off), g = ld16(dO + off);
+  u32x4 a[PAIR_ROWS], g[PAIR_ROWS];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) sum += vget<bf16>(a, j) * vget<bf16>(g, j);
+  for (int i = 0; i < PAIR_ROWS; ++i) {
+    const int64_t row = row0 + i;
+    const int64_t off = (row / H) * d + (row % H) * DH + part * 8;
+    a[i] = row < rows ? ld16(o + off) : u32x4{0, 0, 0, 0};
+    g[i] = row < rows ? ld16(dO + off) : u32x4{0, 0, 0, 0};
   }
 #pragma unroll
-  for (int m = LPR / 2; m >= 1; m >>= 1) sum += __shfl_xor(sum, m, 64);
-  if (row < rows && part == 0) {
-    const int64_t tok = row / H, bq = tok / S, q = tok % S;
-    const int64_t bh = bq * H + row % H;
-    pairs[(bh * S_pad + q) * 2] = lse2[bh * S + q];
-    pairs[(bh * S_pad + q) * 2 + 1] = sum;
+  for (int i = 0; i < PAIR_ROWS; ++i) {
+    const int64_t row = row0 + i;
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sum += vget<bf16>(a[i], j) * vget<bf16>(g[i], j);
+#pragma unroll
+    for (int m = LPR / 2; m >= 1; m >>= 1) sum += __shfl_xor(sum, m, 64);
+    if (row < rows && part == 0) {
+      const int64_t tok = row / H, bq = tok / S, q = tok % S;
+      const int64_t bh = bq * H + row % H;
+      pairs[(bh * S_pad + q) * 2] = lse2[bh * S + q];
+      pairs[(bh * S_pad + q) * 2 + 1] = sum;
+    }
   }
   // queries S .. S_pad - 1 of every head: zeros, so that masked products (p = 0) stay finite
   const int npad = S_pad - S;
@@ -1092,7 +1103,7 @@ hipError_t bwd_launch(const void* qkv, const void* o, const void* dO, const floa
     using C = BwdRing<DH>;
     const int S_pad = (S + 63) / 64 * 64;
     const int64_t rows = (int64_t)mu * S * H;
-    const int64_t threads = rows * (DH / 8);
+    const int64_t threads = (rows + PAIR_ROWS - 1) / PAIR_ROWS * (DH / 8);
     const bf16* q = reinterpret_cast<const bf16*>(qkv);
     const bf16* g = reinterpret_cast<const bf16*>(dO);
     bf16* dq = reinterpret_cast<bf16*>(dqkv);
