@@ -372,6 +372,29 @@ __device__ __forceinline__ void pipe_fill_one(int p, const bf16* src, int64_t ld
   }
 }
 
+// The address of load p of this thread for contracted offset 0 (add k0 for a
+// K-major operand, k0 rows for an MN-major one), with its row (K-major) or
+// column group (MN-major) clamped into the operand: a clamped row only feeds
+// outputs past M or N, which are never stored. Whole k-steps inside K then
+// need one address add per load; the last, partial one takes pipe_fill_one,
+// which reads the zero page for every slot outside the operand.
+template <int ROWS, bool KMAJ, int NT>
+__device__ __forceinline__ const bf16* pipe_fill_base(int p, const bf16* src, int64_t ld, int row0, int rows_total,
+                                                      int w, int l) {
+  const int blk = p * (NT / 64) + w;
+  const int slot = blk * 64 + l;
+  if (KMAJ) {
+    const int row = slot >> 3;
+    const int kv = (slot & 7) ^ ((row >> 1) & 7);
+    return src + (int64_t)min(row0 + row, rows_total - 1) * ld + kv * 8;
+  } else {
+    constexpr int CPL = ROWS / 8;
+    const int line = slot / CPL;
+    const int c = (slot % CPL) ^ trt_swz<ROWS>(line);
+    return src + (int64_t)line * ld + min(row0 + c * 8, (rows_total - 1) & ~7);
+  }
+}
+
 // Output pass of the staged epilogue (every mode but the atomic one). A unit
 // is one 16-byte store: 8 bf16 or 4 fp32 columns. Each thread keeps the same
 // unit column for all its rows, so the bias is loaded once; the aux rows of
@@ -701,11 +724,33 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
 
   const uint32_t smem_lds = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) u32x4*)smem);
   const int wu = __builtin_amdgcn_readfirstlane(w);
+  // Per-thread load addresses at contracted offset 0. When every k-step lies
+  // wholly inside K (and B is not segmented), a load is one address add
+  // (kf: true); fills past the last k-step then repeat the last one's
+  // addresses, into stages that are never read. Otherwise each load masks
+  // itself against K and the operand (pipe_fill_one).
+  const bool kfull = !(!AK && !BK && a.seg_rows > 0) && k_end - k_begin >= BKE &&
+                     (k_end - k_begin) % BKE == 0;   // uniform
+  const bf16* fa[CF::LA];
+  const bf16* fb[CF::LB];
+#pragma unroll
+  for (int p = 0; p < CF::LA; ++p) fa[p] = pipe_fill_base<BM, AK, NT>(p, A, a.lda, m0, a.M, wu, l);
+#pragma unroll
+  for (int p = 0; p < CF::LB; ++p) fb[p] = pipe_fill_base<BN, BK, NT>(p, B, a.ldb, n0, a.N, wu, l);
   // load p of the L loads of tile kt (the A operand's first, then B's)
-  auto fill_one = [&](int kt, int p) {
+  auto fill_one = [&](auto kf, int kt, int p) {
     const uint32_t st = smem_lds + (uint32_t)((kt % NS) * CF::STAGE_SLOTS * 16);
     const int k0 = k_begin + kt * BKE;
-    if (p < CF::LA) {
+    if constexpr (decltype(kf)::value) {
+      const int kc = min(k0, k_end - BKE);
+      if (p < CF::LA) {
+        const int blk = p * (NT / 64) + wu;
+        dma16(fa[p] + (AK ? (int64_t)kc : (int64_t)kc * a.lda), st + (uint32_t)(blk * 64 * 16));
+      } else {
+        const int q = p - CF::LA, blk = q * (NT / 64) + wu;
+        dma16(fb[q] + (BK ? (int64_t)kc : (int64_t)kc * a.ldb), st + CF::SLOTS_A * 16 + (uint32_t)(blk * 64 * 16));
+      }
+    } else if (p < CF::LA) {
       pipe_fill_one<BM, AK, NT>(p, A, a.lda, m0, a.M, k0, k_end, st, a.zeros, wu, l);
     } else if constexpr (!AK && !BK) {
       // weight gradients: B may come in segments of seg_rows contracted rows
@@ -723,9 +768,9 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
       pipe_fill_one<BN, BK, NT>(p - CF::LA, B, a.ldb, n0, a.N, k0, k_end, st + CF::SLOTS_A * 16, a.zeros, wu, l);
     }
   };
-  auto fill = [&](int kt) {
+  auto fill = [&](auto kf, int kt) {
 #pragma unroll
-    for (int p = 0; p < L; ++p) fill_one(kt, p);
+    for (int p = 0; p < L; ++p) fill_one(kf, kt, p);
   };
 
   floatx4 acc[WM / 16][WN / 16];
@@ -789,45 +834,49 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
   // wave's issue priority over its MFMA steps (measured 1.3% faster there,
   // slightly slower for the K-major products)
   constexpr bool PRIO = !AK && !BK;
+  auto main_loop = [&](auto kf) {
 #pragma unroll
-  for (int t = 0; t < NS; ++t) fill(t);
-  wait_vmcnt<L * (NS - 1)>();
-  barrier_no_fence();
-  read_step(0, 0, ya, xa);
-  for (int kt = 0; kt < nk; ++kt) {
-    wait_lds_reads();     // reads of ya/xa, issued one MFMA step ago
-    if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
-    read_step(kt, 1, yb, xb);
-    mma_all(ya, xa);
-    interleave_reads<NRI, NM>();
-    if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
-    wait_lds_reads();     // reads of yb/xb
-    wait_vmcnt<L * (NS - 2)>();   // tile kt + 1 has landed; kt + 2 .. kt + NS - 1 may be in flight
+    for (int t = 0; t < NS; ++t) fill(kf, t);
+    wait_vmcnt<L * (NS - 1)>();
     barrier_no_fence();
-    // Refill the stage of tile kt (every wave has read it) with tile kt + NS.
-    if constexpr (AK && BK) {
-      // One load at a time between the MFMAs of this step and the reads of
-      // the next: the loads of all waves of the CU reach the address unit
-      // spread over the step instead of in one burst that holds up the MFMAs
-      // (measured faster with both operands K-major, slower with MN-major ones).
-#pragma unroll
-      for (int p = 0; p < L; ++p) {
-        fill_one(kt + NS, p);
-#pragma unroll
-        for (int f = p * NF / L; f < (p + 1) * NF / L; ++f) read_frag(kt + 1, 0, f, ya, xa);
-#pragma unroll
-        for (int q = p * NM / L; q < (p + 1) * NM / L; ++q) mma_one(q, yb, xb);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    } else {
-      fill(kt + NS);
+    read_step(0, 0, ya, xa);
+    for (int kt = 0; kt < nk; ++kt) {
+      wait_lds_reads();     // reads of ya/xa, issued one MFMA step ago
       if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
-      read_step(kt + 1, 0, ya, xa);
-      mma_all(yb, xb);
+      read_step(kt, 1, yb, xb);
+      mma_all(ya, xa);
       interleave_reads<NRI, NM>();
       if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
+      wait_lds_reads();     // reads of yb/xb
+      wait_vmcnt<L * (NS - 2)>();   // tile kt + 1 has landed; kt + 2 .. kt + NS - 1 may be in flight
+      barrier_no_fence();
+      // Refill the stage of tile kt (every wave has read it) with tile kt + NS.
+      if constexpr (AK && BK) {
+        // One load at a time between the MFMAs of this step and the reads of
+        // the next: the loads of all waves of the CU reach the address unit
+        // spread over the step instead of in one burst that holds up the MFMAs
+        // (measured faster with both operands K-major, slower with MN-major ones).
+#pragma unroll
+        for (int p = 0; p < L; ++p) {
+          fill_one(kf, kt + NS, p);
+#pragma unroll
+          for (int f = p * NF / L; f < (p + 1) * NF / L; ++f) read_frag(kt + 1, 0, f, ya, xa);
+#pragma unroll
+          for (int q = p * NM / L; q < (p + 1) * NM / L; ++q) mma_one(q, yb, xb);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      } else {
+        fill(kf, kt + NS);
+        if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
+        read_step(kt + 1, 0, ya, xa);
+        mma_all(yb, xb);
+        interleave_reads<NRI, NM>();
+        if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
+      }
     }
-  }
+  };
+  if (kfull) main_loop(std::true_type{});
+  else main_loop(std::false_type{});
   wait_vmcnt<0>();   // the fills past the last tile, before the ring is reused
   staged_epilogue<TO, EPI, CF, PRE>(a, reinterpret_cast<float*>(smem), m0, n0, wm0, wn0, acc, pre, pb);
 }
