@@ -149,6 +149,24 @@ template <int ROWS> __device__ __forceinline__ int trt_elem(int k, int r) {
   return k * ROWS + (((r >> 3) ^ trt_swz<ROWS>(k)) << 3) + (r & 7);
 }
 typedef short i16x4 __attribute__((ext_vector_type(4)));
+// The same read from a precomputed address: off = lds_frag_tr_off<ROWS>(row0)
+// is this lane's byte offset within the tile for step 0, and the tile's LDS
+// byte address is added per read. Lines k0 + 4 and k0 + 32 s keep the swizzle
+// of line k0 (k0 = 8 g + 0..3 leaves bits 0, 1 and 3 unchanged by those
+// steps), so both reads of any step are constant offsets from it.
+template <int ROWS> __device__ __forceinline__ uint32_t lds_frag_tr_off(int row0) {
+  const int l = lane_id();
+  const int g = l >> 4, c = l & 15;
+  return (uint32_t)(2 * trt_elem<ROWS>(8 * g + (c >> 2), row0 + 4 * (c & 3)));
+}
+template <int ROWS> __device__ __forceinline__ u32x4 lds_frag_tr_at(uint32_t addr, int s) {
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  const uint32_t a0 = addr + (uint32_t)(s * 32 * ROWS * 2);
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(uintptr_t)a0);
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(uintptr_t)(a0 + 4 * ROWS * 2));
+  const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
+  return u32x4{a[0], a[1], b[0], b[1]};
+}
 template <int ROWS> __device__ __forceinline__ u32x4 lds_frag_tr(const u32x4* tile, int s, int row0) {
   const int l = lane_id();
   const int g = l >> 4, c = l & 15;

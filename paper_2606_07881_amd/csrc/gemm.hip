@@ -738,8 +738,8 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
 #pragma unroll
   for (int p = 0; p < CF::LB; ++p) fb[p] = pipe_fill_base<BN, BK, NT>(p, B, a.ldb, n0, a.N, wu, l);
   // load p of the L loads of tile kt (the A operand's first, then B's)
-  auto fill_one = [&](auto kf, int kt, int p) {
-    const uint32_t st = smem_lds + (uint32_t)((kt % NS) * CF::STAGE_SLOTS * 16);
+  auto fill_one = [&](auto kf, int kt, int stage, int p) {   // stage = kt % NS
+    const uint32_t st = smem_lds + (uint32_t)(stage * CF::STAGE_SLOTS * 16);
     const int k0 = k_begin + kt * BKE;
     if constexpr (decltype(kf)::value) {
       const int kc = min(k0, k_end - BKE);
@@ -768,9 +768,9 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
       pipe_fill_one<BN, BK, NT>(p - CF::LA, B, a.ldb, n0, a.N, k0, k_end, st + CF::SLOTS_A * 16, a.zeros, wu, l);
     }
   };
-  auto fill = [&](auto kf, int kt) {
+  auto fill = [&](auto kf, int kt, int stage) {
 #pragma unroll
-    for (int p = 0; p < L; ++p) fill_one(kf, kt, p);
+    for (int p = 0; p < L; ++p) fill_one(kf, kt, stage, p);
   };
 
   floatx4 acc[WM / 16][WN / 16];
@@ -793,15 +793,24 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
   // tile kt is free and is refilled at once with tile kt + NS. Loads of a tile
   // are thus issued NS - 1 tiles of MFMA work before they are needed.
   u32x4 ya[WM / 16], xa[WN / 16], yb[WM / 16], xb[WN / 16];
-  auto read_step = [&](int kt, int s, u32x4* yf, u32x4* xf) {
-    const u32x4* sa = smem + (kt % NS) * CF::STAGE_SLOTS;
+  // MN-major operands: each fragment's transpose-read offset within its tile,
+  // computed once (the swizzle makes it a non-affine function of the fragment)
+  uint32_t tro_a[WM / 16], tro_b[WN / 16];
+#pragma unroll
+  for (int i = 0; i < WM / 16; ++i) tro_a[i] = AK ? 0u : lds_frag_tr_off<BM>(wm0 + i * 16);
+#pragma unroll
+  for (int j = 0; j < WN / 16; ++j) tro_b[j] = BK ? 0u : lds_frag_tr_off<BN>(wn0 + j * 16);
+  // stage st (0 .. NS - 1) of the ring; the loop keeps st of k-steps kt and kt + 1
+  auto read_step = [&](int st, int s, u32x4* yf, u32x4* xf) {
+    const u32x4* sa = smem + st * CF::STAGE_SLOTS;
     const u32x4* sb = sa + CF::SLOTS_A;
+    const uint32_t la = smem_lds + (uint32_t)(st * CF::STAGE_SLOTS * 16), lb = la + CF::SLOTS_A * 16;
 #pragma unroll
     for (int i = 0; i < WM / 16; ++i)
-      yf[i] = AK ? pipe_frag_k<BM>(sa, s, wm0 + i * 16) : lds_frag_tr<BM>(sa, s, wm0 + i * 16);
+      yf[i] = AK ? pipe_frag_k<BM>(sa, s, wm0 + i * 16) : lds_frag_tr_at<BM>(la + tro_a[i], s);
 #pragma unroll
     for (int j = 0; j < WN / 16; ++j)
-      xf[j] = BK ? pipe_frag_k<BN>(sb, s, wn0 + j * 16) : lds_frag_tr<BN>(sb, s, wn0 + j * 16);
+      xf[j] = BK ? pipe_frag_k<BN>(sb, s, wn0 + j * 16) : lds_frag_tr_at<BN>(lb + tro_b[j], s);
   };
   auto mma_all = [&](const u32x4* yf, const u32x4* xf) {
 #pragma unroll
@@ -810,13 +819,14 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
       for (int j = 0; j < WN / 16; ++j) mma_step<bf16>(acc[i][j], xf[j], yf[i]);
   };
   // fragment f of step s (A's fragments first, then B's), and MFMA q of a step
-  auto read_frag = [&](int kt, int s, int f, u32x4* yf, u32x4* xf) {
-    const u32x4* sa = smem + (kt % NS) * CF::STAGE_SLOTS;
+  auto read_frag = [&](int st, int s, int f, u32x4* yf, u32x4* xf) {
+    const u32x4* sa = smem + st * CF::STAGE_SLOTS;
     const u32x4* sb = sa + CF::SLOTS_A;
-    if (f < WM / 16) yf[f] = AK ? pipe_frag_k<BM>(sa, s, wm0 + f * 16) : lds_frag_tr<BM>(sa, s, wm0 + f * 16);
+    const uint32_t la = smem_lds + (uint32_t)(st * CF::STAGE_SLOTS * 16), lb = la + CF::SLOTS_A * 16;
+    if (f < WM / 16) yf[f] = AK ? pipe_frag_k<BM>(sa, s, wm0 + f * 16) : lds_frag_tr_at<BM>(la + tro_a[f], s);
     else {
       const int j = f - WM / 16;
-      xf[j] = BK ? pipe_frag_k<BN>(sb, s, wn0 + j * 16) : lds_frag_tr<BN>(sb, s, wn0 + j * 16);
+      xf[j] = BK ? pipe_frag_k<BN>(sb, s, wn0 + j * 16) : lds_frag_tr_at<BN>(lb + tro_b[j], s);
     }
   };
   auto mma_one = [&](int q, const u32x4* yf, const u32x4* xf) {
@@ -836,14 +846,16 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
   constexpr bool PRIO = !AK && !BK;
   auto main_loop = [&](auto kf) {
 #pragma unroll
-    for (int t = 0; t < NS; ++t) fill(kf, t);
+    for (int t = 0; t < NS; ++t) fill(kf, t, t);
     wait_vmcnt<L * (NS - 1)>();
     barrier_no_fence();
     read_step(0, 0, ya, xa);
+    int st0 = 0;   // ring stage of k-step kt
     for (int kt = 0; kt < nk; ++kt) {
+      const int st1 = st0 + 1 == NS ? 0 : st0 + 1;   // of k-step kt + 1
       wait_lds_reads();     // reads of ya/xa, issued one MFMA step ago
       if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
-      read_step(kt, 1, yb, xb);
+      read_step(st0, 1, yb, xb);
       mma_all(ya, xa);
       interleave_reads<NRI, NM>();
       if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
@@ -858,21 +870,22 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
         // (measured faster with both operands K-major, slower with MN-major ones).
 #pragma unroll
         for (int p = 0; p < L; ++p) {
-          fill_one(kf, kt + NS, p);
+          fill_one(kf, kt + NS, st0, p);   // tile kt + NS reuses the stage of tile kt
 #pragma unroll
-          for (int f = p * NF / L; f < (p + 1) * NF / L; ++f) read_frag(kt + 1, 0, f, ya, xa);
+          for (int f = p * NF / L; f < (p + 1) * NF / L; ++f) read_frag(st1, 0, f, ya, xa);
 #pragma unroll
           for (int q = p * NM / L; q < (p + 1) * NM / L; ++q) mma_one(q, yb, xb);
           __builtin_amdgcn_sched_barrier(0);
         }
       } else {
-        fill(kf, kt + NS);
+        fill(kf, kt + NS, st0);
         if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
-        read_step(kt + 1, 0, ya, xa);
+        read_step(st1, 0, ya, xa);
         mma_all(yb, xb);
         interleave_reads<NRI, NM>();
         if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
       }
+      st0 = st1;
     }
   };
   if (kfull) main_loop(std::true_type{});
