@@ -725,12 +725,11 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
   const uint32_t smem_lds = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) u32x4*)smem);
   const int wu = __builtin_amdgcn_readfirstlane(w);
   // Per-thread load addresses at contracted offset 0. When every k-step lies
-  // wholly inside K (and B is not segmented), a load is one address add
-  // (kf: true); fills past the last k-step then repeat the last one's
-  // addresses, into stages that are never read. Otherwise each load masks
-  // itself against K and the operand (pipe_fill_one).
-  const bool kfull = !(!AK && !BK && a.seg_rows > 0) && k_end - k_begin >= BKE &&
-                     (k_end - k_begin) % BKE == 0;   // uniform
+  // wholly inside K, a load is one address add (kf: true; a segmented B adds
+  // its segment's offset, one per k-step); fills past the last k-step then
+  // repeat the last one's addresses, into stages that are never read.
+  // Otherwise each load masks itself against K and the operand (pipe_fill_one).
+  const bool kfull = k_end - k_begin >= BKE && (k_end - k_begin) % BKE == 0;   // uniform
   const bf16* fa[CF::LA];
   const bf16* fb[CF::LB];
 #pragma unroll
@@ -748,7 +747,15 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
         dma16(fa[p] + (AK ? (int64_t)kc : (int64_t)kc * a.lda), st + (uint32_t)(blk * 64 * 16));
       } else {
         const int q = p - CF::LA, blk = q * (NT / 64) + wu;
-        dma16(fb[q] + (BK ? (int64_t)kc : (int64_t)kc * a.ldb), st + CF::SLOTS_A * 16 + (uint32_t)(blk * 64 * 16));
+        int64_t off = BK ? (int64_t)kc : (int64_t)kc * a.ldb;
+        if constexpr (!AK && !BK) {
+          if (a.seg_rows > 0) {   // uniform: row kc of the window is row kc - sg * seg_rows of segment sg
+            const int sg = kc / (int)a.seg_rows;
+            off = (int64_t)((a.seg_first + sg) % a.seg_count) * a.seg_stride +
+                  (int64_t)(kc - sg * (int)a.seg_rows) * a.ldb;
+          }
+        }
+        dma16(fb[q] + off, st + CF::SLOTS_A * 16 + (uint32_t)(blk * 64 * 16));
       }
     } else if (p < CF::LA) {
       pipe_fill_one<BM, AK, NT>(p, A, a.lda, m0, a.M, k0, k_end, st, a.zeros, wu, l);
