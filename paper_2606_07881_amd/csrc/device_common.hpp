@@ -206,6 +206,14 @@ __device__ __forceinline__ float group4_max(float v) {
 
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(void* p, const u32x4& v) { *reinterpret_cast<u32x4*>(p) = v; }
+// The same through global-address-space pointers, for data known to be in
+// device memory: global_* instructions count in vmcnt only, where flat_* ones
+// (the compiler's choice for a pointer it cannot place) also count in
+// lgkmcnt and so hold up every later wait for LDS reads.
+__device__ __forceinline__ u32x4 ld16g(const void* p) {
+  return *(const __attribute__((address_space(1))) u32x4*)p;
+}
+__device__ __forceinline__ void st16g(void* p, const u32x4& v) { *(__attribute__((address_space(1))) u32x4*)p = v; }
 
 // ---- one-shot tile staging (global -> LDS), used by the attention kernels -----------------
 // K-major source: element (row r, contracted c) at src[r * ld + c]. Stages rows

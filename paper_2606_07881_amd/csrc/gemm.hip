@@ -417,7 +417,7 @@ __device__ __forceinline__ void prefetch_aux(const GemmArgs& a, int m0, int n0, 
 #pragma unroll
   for (int p = 0; p < G::P; ++p) {
     const int m = m0 + r0 + p * G::RPI;
-    pre[p] = (ok && m < a.M) ? ld16(ap + (int64_t)m * a.ld_aux + n) : u32x4{0, 0, 0, 0};
+    pre[p] = (ok && m < a.M) ? ld16g(ap + (int64_t)m * a.ld_aux + n) : u32x4{0, 0, 0, 0};
   }
 }
 
@@ -450,6 +450,18 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
   float bias[U];   // prefetched at kernel start (zero past the last column)
 #pragma unroll
   for (int j = 0; j < U; ++j) bias[j] = HAS_BIAS ? pb[j] : 0.f;
+  // EPI_ACC: every old value of this thread's units is loaded before the
+  // first store, so the loads overlap (the compiler cannot order a load past
+  // an earlier store to C, which might alias it)
+  u32x4 acc_old[EPI == EPI_ACC ? P : 1];
+  if constexpr (EPI == EPI_ACC) {
+    const float* Cc = reinterpret_cast<const float*>(a.C);
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const int m = mb + r0 + p * RPI;
+      acc_old[p] = (vec && m < a.M) ? ld16g(Cc + (int64_t)m * a.ldc + n) : u32x4{0, 0, 0, 0};
+    }
+  }
   float aux[P][U];
   if constexpr (HAS_AUX) {
     const bf16* ap = reinterpret_cast<const bf16*>(a.aux);
@@ -465,7 +477,7 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
 #pragma unroll
           for (int h = 0; h < U / 8 + (U < 8 ? 1 : 0); ++h) {
             if constexpr (U >= 8) {
-              const u32x4 w = ld16(ap + off + 8 * h);
+              const u32x4 w = ld16g(ap + off + 8 * h);
 #pragma unroll
               for (int j = 0; j < 8; ++j) aux[p][8 * h + j] = vget<bf16>(w, j);
             } else {
@@ -499,9 +511,8 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
     if constexpr (EPI == EPI_ACC) {
       float* C = reinterpret_cast<float*>(a.C);
       if (vec) {
-        const u32x4 old = ld16(C + off);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) o[j] += as_float(old[j]);
+        for (int j = 0; j < 4; ++j) o[j] += as_float(acc_old[p][j]);
       } else {
 #pragma unroll
         for (int j = 0; j < U; ++j)
@@ -537,10 +548,10 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
     TO* C = reinterpret_cast<TO*>(a.C);
     if (vec) {
       if constexpr (sizeof(TO) == 2) {
-        st16(C + off, u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
+        st16g(C + off, u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
                             pack_bf16x2(o[6], o[7])});
       } else {
-        st16(C + off, u32x4{__builtin_bit_cast(uint32_t, o[0]), __builtin_bit_cast(uint32_t, o[1]),
+        st16g(C + off, u32x4{__builtin_bit_cast(uint32_t, o[0]), __builtin_bit_cast(uint32_t, o[1]),
                             __builtin_bit_cast(uint32_t, o[2]), __builtin_bit_cast(uint32_t, o[3])});
       }
     } else {
@@ -554,10 +565,10 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
       for (int j = 0; j < U; ++j) o[j] = gelu_f(o[j]);
       if (vec) {
         if constexpr (sizeof(TO) == 2)
-          st16(C2 + off, u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
+          st16g(C2 + off, u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
                                pack_bf16x2(o[6], o[7])});
         else
-          st16(C2 + off, u32x4{__builtin_bit_cast(uint32_t, o[0]), __builtin_bit_cast(uint32_t, o[1]),
+          st16g(C2 + off, u32x4{__builtin_bit_cast(uint32_t, o[0]), __builtin_bit_cast(uint32_t, o[1]),
                                __builtin_bit_cast(uint32_t, o[2]), __builtin_bit_cast(uint32_t, o[3])});
       } else {
 #pragma unroll
