@@ -880,29 +880,23 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
       wait_lds_reads();     // reads of yb/xb
       wait_vmcnt<L * (NS - 2)>();   // tile kt + 1 has landed; kt + 2 .. kt + NS - 1 may be in flight
       barrier_no_fence();
-      // Refill the stage of tile kt (every wave has read it) with tile kt + NS.
-      if constexpr (AK && BK) {
-        // One load at a time between the MFMAs of this step and the reads of
-        // the next: the loads of all waves of the CU reach the address unit
-        // spread over the step instead of in one burst that holds up the MFMAs
-        // (measured faster with both operands K-major, slower with MN-major ones).
+      // Refill the stage of tile kt (every wave has read it) with tile kt + NS,
+      // one load at a time between the MFMAs of this step and the reads of
+      // the next: the loads of all waves of the CU reach the address unit
+      // spread over the step instead of in one burst that holds up the MFMAs
+      // (measured faster with every layout once a load is one address add; the
+      // weight gradients also raise the wave's issue priority over the step).
+      if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-        for (int p = 0; p < L; ++p) {
-          fill_one(kf, kt + NS, st0, p);   // tile kt + NS reuses the stage of tile kt
+      for (int p = 0; p < L; ++p) {
+        fill_one(kf, kt + NS, st0, p);   // tile kt + NS reuses the stage of tile kt
 #pragma unroll
-          for (int f = p * NF / L; f < (p + 1) * NF / L; ++f) read_frag(st1, 0, f, ya, xa);
+        for (int f = p * NF / L; f < (p + 1) * NF / L; ++f) read_frag(st1, 0, f, ya, xa);
 #pragma unroll
-          for (int q = p * NM / L; q < (p + 1) * NM / L; ++q) mma_one(q, yb, xb);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      } else {
-        fill(kf, kt + NS, st0);
-        if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
-        read_step(st1, 0, ya, xa);
-        mma_all(yb, xb);
-        interleave_reads<NRI, NM>();
-        if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
+        for (int q = p * NM / L; q < (p + 1) * NM / L; ++q) mma_one(q, yb, xb);
+        __builtin_amdgcn_sched_barrier(0);
       }
+      if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
       st0 = st1;
     }
   };
