@@ -126,10 +126,18 @@ __device__ __forceinline__ float gelu_sig(float u, float u2) {
   const float k = -2.0f * 1.4426950408889634f * 0.7978845608028654f;   // -2 c log2 e
   return __builtin_amdgcn_rcpf(1.0f + fast_exp2(k * u * fmaf(0.044715f, u2, 1.0f)));
 }
-__device__ __forceinline__ float gelu_f(float u) { return u * gelu_sig(u, u * u); }
-__device__ __forceinline__ float gelu_grad_f(float u) {
+// The derivative from u, u^2 and s: s + s (1 - s) u (2c + 6ac u^2).
+__device__ __forceinline__ float gelu_grad_s(float u, float u2, float sg) {
+  constexpr float c2 = 2.0f * 0.7978845608028654f, c6a = 6.0f * 0.044715f * 0.7978845608028654f;
+  return fmaf(fmaf(-sg, sg, sg), u * fmaf(c6a, u2, c2), sg);
+}
+// The FFN up-projection's epilogue keeps gelu'(u) for the backward instead of
+// u, the only use of u there: both values then share one exponential and one
+// reciprocal, and the down-projection's input gradient only multiplies.
+__device__ __forceinline__ void gelu_and_grad(float u, float& g, float& dg) {
   const float u2 = u * u, sg = gelu_sig(u, u2);
-  return fmaf(2.0f * 0.7978845608028654f * fmaf(-sg, sg, sg), u * fmaf(3.0f * 0.044715f, u2, 1.0f), sg);
+  g = u * sg;
+  dg = gelu_grad_s(u, u2, sg);
 }
 
 // Four consecutive elements [i, i+4) of a T array as floats (one 8- or 16-byte load).
@@ -202,19 +210,17 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int m, int n, const 
       if (HAS_AUX) aux[j] = ldf<T>(a.aux, (int64_t)m * a.ld_aux + n + j);
     }
   }
+  float g[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     float x = acc[j] + bias[j];
     if (EPI == EPI_BIAS_RES) x += aux[j];
-    if (EPI == EPI_GELU_GRAD) x *= gelu_grad_f(aux[j]);
+    if (EPI == EPI_GELU_GRAD) x *= aux[j];
+    if (EPI == EPI_BIAS_GELU) gelu_and_grad(x, g[j], x);
     o[j] = x;
   }
   store4<TO>(reinterpret_cast<TO*>(a.C), (int64_t)m * a.ldc + n, o, nv);
-  if (EPI == EPI_BIAS_GELU) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) o[j] = gelu_f(o[j]);
-    store4<TO>(reinterpret_cast<TO*>(a.C2), (int64_t)m * a.ldc + n, o, nv);
-  }
+  if (EPI == EPI_BIAS_GELU) store4<TO>(reinterpret_cast<TO*>(a.C2), (int64_t)m * a.ldc + n, g, nv);
 }
 
 __device__ __forceinline__ void tile_coords(int pid, int tiles_m, int tiles_n, int& tm, int& tn) {
@@ -500,7 +506,7 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
   for (int p = 0; p < P; ++p) {
     const int r = r0 + p * RPI, m = mb + r;
     if (m >= a.M) continue;
-    float o[U];
+    float o[U], g2[EPI == EPI_BIAS_GELU ? U : 1];
 #pragma unroll
     for (int q = 0; q < U / 4; ++q) {
       const floatx4 v = *reinterpret_cast<const floatx4*>(cl + r * LDC + cu * U + 4 * q);
@@ -528,7 +534,8 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
       for (int j = 0; j < U; ++j) {
         float x = o[j] + bias[j];
         if constexpr (EPI == EPI_BIAS_RES) x += aux[p][j];
-        if constexpr (EPI == EPI_GELU_GRAD) x *= gelu_grad_f(aux[p][j]);
+        if constexpr (EPI == EPI_GELU_GRAD) x *= aux[p][j];
+        if constexpr (EPI == EPI_BIAS_GELU) gelu_and_grad(x, g2[j], x);
         o[j] = x;
       }
     }
@@ -562,7 +569,7 @@ __device__ __forceinline__ void staged_out(const GemmArgs& a, const float* cl, i
     if constexpr (EPI == EPI_BIAS_GELU) {
       TO* C2 = reinterpret_cast<TO*>(a.C2);
 #pragma unroll
-      for (int j = 0; j < U; ++j) o[j] = gelu_f(o[j]);
+      for (int j = 0; j < U; ++j) o[j] = g2[j];
       if (vec) {
         if constexpr (sizeof(TO) == 2)
           st16g(C2 + off, u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),

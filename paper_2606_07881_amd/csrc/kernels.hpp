@@ -27,8 +27,8 @@ enum GemmLayout { GEMM_NT = 0, GEMM_NN = 1, GEMM_TN = 2 };
 //   EPI_STORE      C = acc
 //   EPI_BIAS       C = acc + bias[n]
 //   EPI_BIAS_RES   C = acc + bias[n] + aux[m*ld_aux + n]        (residual add)
-//   EPI_BIAS_GELU  C = u = acc + bias[n];  C2 = gelu(u)          (FFN up-projection)
-//   EPI_GELU_GRAD  C = acc * gelu'(aux[m*ld_aux + n])            (FFN down-projection dgrad)
+//   EPI_BIAS_GELU  u = acc + bias[n];  C = gelu'(u);  C2 = gelu(u)  (FFN up-projection)
+//   EPI_GELU_GRAD  C = acc * aux[m*ld_aux + n]  (aux = gelu'(u); FFN down-projection dgrad)
 //   EPI_ACC        Cf32 += acc  (plain read-modify-write; one split only)
 //   EPI_ATOMIC     Cf32 += acc  (atomic add; any number of splits)
 // Softmax cross-entropy over the output columns (bf16 GEMM_NT only, one split):

@@ -314,7 +314,7 @@ struct Bump {
 };
 
 struct BlockSlot {  // byte offsets inside one activation slot
-  size_t x, n1, qkv, o, x1, n2, u, a, mean1, rstd1, mean2, rstd2, lse2;
+  size_t x, n1, qkv, o, x1, n2, gu, a, mean1, rstd1, mean2, rstd2, lse2;   // gu = gelu'(u), a = gelu(u)
 };
 
 struct Layout {
@@ -433,7 +433,7 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
     b.o = sl.take(esz * T * d);
     b.x1 = sl.take(esz * T * d);
     b.n2 = sl.take(esz * T * d);
-    b.u = sl.take(esz * T * f);
+    b.gu = sl.take(esz * T * f);
     b.a = sl.take(esz * T * f);
     b.mean1 = sl.take(4 * T);
     b.rstd1 = sl.take(4 * T);
@@ -777,7 +777,7 @@ int blocks_fwd(paci_stage* h, char* sl, const void* in, void* x0_copy, void* out
     }
     TRY(ln_fwd(h, sl + o.x1, sl + o.n2, reinterpret_cast<float*>(sl + o.mean2), reinterpret_cast<float*>(sl + o.rstd2),
                b.ln2_g, b.ln2_b, nullptr));
-    TRY(linear_fwd(h, sl + o.n2, b.w_1, b.b_1, T, f, d, paci::EPI_BIAS_GELU, sl + o.u, nullptr, sl + o.a));
+    TRY(linear_fwd(h, sl + o.n2, b.w_1, b.b_1, T, f, d, paci::EPI_BIAS_GELU, sl + o.gu, nullptr, sl + o.a));
     void* y = (l + 1 < s.n_layers) ? (void*)(sl + h->L.blk[l + 1].x) : out;
     if (zd) {
       TRY(linear_fwd(h, sl + o.a, b.w_2, b.b_2, T, d, f, paci::EPI_BIAS, zd, nullptr, nullptr));
@@ -824,8 +824,8 @@ int block_bwd(paci_stage* h, char* sl, int l, const void* dy, void* dx, bool dy_
   }
   if (!win) TRY(linear_wgrad(h, g2, d, sl + o.a, f, d, f, T, b.w_2));
   if (!dy_bias_done || drop) TRY(bias_grad(h, g2, d, T, d, b.b_2));
-  // du = (g2 W2) * gelu'(u), and G_b1 += sum du in the same epilogue
-  TRY(linear_dgrad(h, g2, d, b.w_2, T, f, d, paci::EPI_GELU_GRAD, du, sl + o.u, b.b_1));
+  // du = (g2 W2) * gelu'(u) (kept by the forward), and G_b1 += sum du in the same epilogue
+  TRY(linear_dgrad(h, g2, d, b.w_2, T, f, d, paci::EPI_GELU_GRAD, du, sl + o.gu, b.b_1));
   // u = n2 W1^T + b1
   if (!win) TRY(linear_wgrad(h, du, f, sl + o.n2, d, f, d, T, b.w_1));
   TRY(linear_dgrad(h, du, f, b.w_1, T, d, f, paci::EPI_STORE, dn, nullptr));
