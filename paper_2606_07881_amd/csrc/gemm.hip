@@ -808,8 +808,10 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
   u32x4 pre[EpiGeom<TO, BN, CF::PR, NT>::P];
   if constexpr (PRE) prefetch_aux<TO, BN, CF::PR, NT>(a, m0, n0, tid, pre);
   float pb[16 / sizeof(TO)];
-  if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU)
-    prefetch_bias<TO, BN, CF::PR, NT>(a, n0, tid, pb);
+  // (tall wave tiles load it after the loop: their registers are taken by the fragments)
+  constexpr bool HAS_BIAS = EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU;
+  constexpr bool TALL = WM / 16 >= 8;
+  if constexpr (HAS_BIAS && !TALL) prefetch_bias<TO, BN, CF::PR, NT>(a, n0, tid, pb);
 
   // Fragments are double-buffered in registers: the LDS reads of the next
   // MFMA step are issued before the MFMAs of the current one. The barrier that
@@ -907,9 +909,60 @@ __global__ void __launch_bounds__(CF::NT, CF::OCC) gemm_pipe_kernel(GemmArgs a, 
       st0 = st1;
     }
   };
-  if (kfull) main_loop(std::true_type{});
-  else main_loop(std::false_type{});
+  // Tall wave tiles (WM = 128: eight A fragments per step, 128 accumulator
+  // VGPRs) fit two wavefronts per SIMD only with the A fragments single-
+  // buffered: each is re-read for the next step right after its row's MFMAs
+  // have issued, so its register is reused (B stays double-buffered). The
+  // ring, barriers and waits are those of the loop above; the refill loads
+  // are spread one or more per A row.
+  constexpr int G = WM / 16;
+  auto main_loop_tall = [&](auto kf) {
+#pragma unroll
+    for (int t = 0; t < NS; ++t) fill(kf, t, t);
+    wait_vmcnt<L * (NS - 1)>();
+    barrier_no_fence();
+    read_step(0, 0, ya, xa);
+    int st0 = 0;
+    for (int kt = 0; kt < nk; ++kt) {
+      const int st1 = st0 + 1 == NS ? 0 : st0 + 1;
+      wait_lds_reads();   // ya/xa of step 0 of tile kt
+#pragma unroll
+      for (int j = 0; j < WN / 16; ++j) read_frag(st0, 1, G + j, ya, xb);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < G; ++i) {
+#pragma unroll
+        for (int j = 0; j < WN / 16; ++j) mma_step<bf16>(acc[i][j], xa[j], ya[i]);
+        read_frag(st0, 1, i, ya, xb);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      wait_lds_reads();   // ya/xb of step 1
+      wait_vmcnt<L * (NS - 2)>();
+      barrier_no_fence();
+#pragma unroll
+      for (int j = 0; j < WN / 16; ++j) read_frag(st1, 0, G + j, ya, xa);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < G; ++i) {
+#pragma unroll
+        for (int p = i * L / G; p < (i + 1) * L / G; ++p) fill_one(kf, kt + NS, st0, p);
+#pragma unroll
+        for (int j = 0; j < WN / 16; ++j) mma_step<bf16>(acc[i][j], xb[j], ya[i]);
+        read_frag(st1, 0, i, ya, xa);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      st0 = st1;
+    }
+  };
+  if constexpr (TALL) {
+    if (kfull) main_loop_tall(std::true_type{});
+    else main_loop_tall(std::false_type{});
+  } else {
+    if (kfull) main_loop(std::true_type{});
+    else main_loop(std::false_type{});
+  }
   wait_vmcnt<0>();   // the fills past the last tile, before the ring is reused
+  if constexpr (HAS_BIAS && TALL) prefetch_bias<TO, BN, CF::PR, NT>(a, n0, tid, pb);
   staged_epilogue<TO, EPI, CF, PRE>(a, reinterpret_cast<float*>(smem), m0, n0, wm0, wn0, acc, pre, pb);
 }
 
@@ -922,6 +975,9 @@ typedef PipeTile<256, 128, 64, 64, 3> P256x128;
 typedef PipeTile<128, 128, 64, 64, 4> P128x128;
 typedef PipeTile<128, 256, 64, 64, 3> P128x256;
 typedef PipeTile<128, 128, 64, 64, 2, 2> P128x128o2;   // two workgroups per CU
+// 256 x 256 in eight 128 x 64 wave tiles, two-stage ring (128 KB): a quarter
+// fewer LDS reads and a third fewer global -> LDS bytes per FLOP than 256 x 128
+typedef PipeTile<256, 256, 128, 64, 2> P256x256;
 
 template <typename TO, bool AK, bool BK, int EPI, class CF>
 hipError_t launch_pipe(const GemmArgs& a, int splits, hipStream_t st) {
@@ -997,6 +1053,13 @@ hipError_t launch(const GemmArgs& a, int splits, hipStream_t st) {
           // the latter, slower for the other forward and input-gradient
           // products); the rest: 256 x 128 tiles, which re-read the weights
           // half as often
+          // The FFN up-projection and the input gradient through gelu'(u),
+          // when 256 x 256 tiles fill whole rounds of the CUs: those
+          // (measured 13% and 2% faster per call at 8192 x 4096)
+          if constexpr (AK && BK && (EPI == EPI_BIAS_GELU || EPI == EPI_GELU_GRAD)) {
+            const int t256 = ((a.M + 255) / 256) * ((a.N + 255) / 256);
+            if (splits == 1 && t256 % cu_count() == 0) return launch_pipe<TO, AK, BK, EPI, P256x256>(a, splits, st);
+          }
           if constexpr (!AK || EPI == EPI_GELU_GRAD) return launch_pipe<TO, AK, BK, EPI, P128x128o2>(a, splits, st);
           else return launch_pipe<TO, AK, BK, EPI, P256x128>(a, splits, st);
       }

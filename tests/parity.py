@@ -114,6 +114,12 @@ def small_cfg(name, **kw):
         # have 288 tiles of 256 x 128, more than the 256 CUs (a second, partial round)
         "wide_bf16": dict(kind="middle", n_layers=1, d_model=256, n_heads=4, head_dim=64, d_ff=2304, seq=512,
                           micro_batch=8, K=2, delay=1, M=6, dtype="bf16"),
+        # T = 4000, FFN width 4064, d 96: the FFN1 forward and FFN2 input-gradient
+        # products run on 256 x 256 tiles (16 x 16 = 256 tiles, whole rounds of the
+        # 256 CUs), both with a ragged last row and column tile, and their
+        # contraction over d = 96 ends in a partial k-step
+        "tall_bf16": dict(kind="middle", n_layers=1, d_model=96, n_heads=3, head_dim=32, d_ff=4064, seq=500,
+                          micro_batch=8, K=2, delay=1, M=3, dtype="bf16"),
         # d 512, FFN 2048: every weight's tile grid of the grouped weight-gradient launch
         # splits into 8 equal blocks, one per XCD (W_qkv 6 x 4 and W_o 2 x 4 tiles of 256 x 128)
         "xcd_bf16": dict(kind="middle", n_layers=1, d_model=512, n_heads=8, head_dim=64, d_ff=2048, seq=128,

@@ -72,7 +72,7 @@ def _fmt(rep):
 
 
 @pytest.mark.parametrize("name", ["tiny_fp32", "ragged_bf16", "ragged_fp32", "win_bf16", "win8_bf16", "winsplit_bf16",
-                                  "acc8_bf16", "wide_bf16", "xcd_bf16", "dh128_bf16",
+                                  "acc8_bf16", "wide_bf16", "tall_bf16", "xcd_bf16", "dh128_bf16",
                                   "dh32_bf16", "first_bf16", "last_bf16", "first_fp32", "last_fp32",
                                   "ckpt_tiny_fp32", "ckpt_ragged_bf16", "ckpt_win_bf16", "ckpt_first_bf16",
                                   "ckpt_last_bf16", "sched_bf16", "fused_last_bf16", "ckpt_fused_last_bf16",
