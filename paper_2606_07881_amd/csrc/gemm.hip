@@ -1133,21 +1133,19 @@ hipError_t by_layout(bool out_f32, GemmLayout lay, GemmEpi epi, const GemmArgs& 
 
 void gemm_set_tile_override(int cfg) { g_tile_override = cfg; }
 
-// Grouped weight gradients on 256 x 128 tiles (one workgroup per CU, three-stage ring),
-// plain fp32 read-modify-write of each output tile.
-int wgrad_group_tiles(int M, int N) {
-  return ((M + P256x128::BM - 1) / P256x128::BM) * ((N + P256x128::BN - 1) / P256x128::BN);
-}
-
-int wgrad_group_xcd_m(int M, int N, int K) {
-  const int tm = (M + P256x128::BM - 1) / P256x128::BM, tn = (N + P256x128::BN - 1) / P256x128::BN;
+// Grouped weight gradients on 256 x 128 tiles (one workgroup per CU, three-stage
+// ring) or 256 x 256 (two-stage ring), plain fp32 read-modify-write of each output tile.
+namespace {
+template <class CF> int group_tiles(int M, int N) { return ((M + CF::BM - 1) / CF::BM) * ((N + CF::BN - 1) / CF::BN); }
+template <class CF> int group_xcd_m(int M, int N, int K) {
+  const int tm = (M + CF::BM - 1) / CF::BM, tn = (N + CF::BN - 1) / CF::BN;
   int best = 0;
   double best_bytes = 0;
   for (int xm = 1; xm <= 8; xm *= 2) {
     const int xn = 8 / xm;
     if (tm % xm || tn % xn) continue;
     // panels one XCD reads: its bm row tiles of A and bn column tiles of B over K rows
-    const double bytes = (double)K * 2.0 * ((tm / xm) * P256x128::BM + (tn / xn) * P256x128::BN);
+    const double bytes = (double)K * 2.0 * ((tm / xm) * CF::BM + (tn / xn) * CF::BN);
     if (best == 0 || bytes < best_bytes) {
       best = xm;
       best_bytes = bytes;
@@ -1155,9 +1153,47 @@ int wgrad_group_xcd_m(int M, int N, int K) {
   }
   return best;
 }
+template <class CF, int EPI>
+void launch_grouped(const GemmArgs& a, int total_tiles, int K, hipStream_t st) {
+  hipLaunchKernelGGL((gemm_pipe_kernel<float, false, false, EPI, CF, true>), dim3(total_tiles, 1), dim3(CF::NT), 0, st,
+                     a, K);
+}
+}  // namespace
+
+int wgrad_group_tiles(int M, int N, bool wide) {
+  return wide ? group_tiles<P256x256>(M, N) : group_tiles<P256x128>(M, N);
+}
+
+int wgrad_group_xcd_m(int M, int N, int K, bool wide) {
+  return wide ? group_xcd_m<P256x256>(M, N, K) : group_xcd_m<P256x128>(M, N, K);
+}
+
+int wgrad_group_wide(const int* M, const int* N, int n) {
+  const int cus = cu_count();
+  auto padded = [](int t) { return (t + 7) / 8 * 8; };
+  // cost in rounds of narrow tiles; n1 = 0 is the single narrow launch
+  auto cost = [&](int n1) {
+    int t1 = 0, t2 = 0;
+    for (int p = 0; p < n; ++p) {
+      if (p < n1) t1 += padded(group_tiles<P256x256>(M[p], N[p]));
+      else t2 += padded(group_tiles<P256x128>(M[p], N[p]));
+    }
+    return 1.8 * ((t1 + cus - 1) / cus) + 1.0 * ((t2 + cus - 1) / cus);
+  };
+  int best = 0;
+  double best_cost = cost(0);
+  for (int n1 = n; n1 >= 1; --n1) {
+    const double c = cost(n1);
+    if (c < best_cost - 1e-9) {
+      best = n1;
+      best_cost = c;
+    }
+  }
+  return best;
+}
 
 hipError_t gemm_wgrad_grouped(const WgradProblem* probs, int n, int total_tiles, int K, const void* zeros,
-                              bool overwrite, int* nonfinite, hipStream_t st) {
+                              bool overwrite, bool wide, int* nonfinite, hipStream_t st) {
   if (probs == nullptr || n < 1 || total_tiles < 1 || K < 1 || K % 8 || zeros == nullptr ||
       (reinterpret_cast<uintptr_t>(zeros) & 15))
     return hipErrorInvalidValue;
@@ -1167,12 +1203,13 @@ hipError_t gemm_wgrad_grouped(const WgradProblem* probs, int n, int total_tiles,
   a.group = probs;
   a.group_n = n;
   a.nonfinite = nonfinite;
-  if (overwrite)
-    hipLaunchKernelGGL((gemm_pipe_kernel<float, false, false, EPI_STORE, P256x128, true>), dim3(total_tiles, 1),
-                       dim3(P256x128::NT), 0, st, a, K);
-  else
-    hipLaunchKernelGGL((gemm_pipe_kernel<float, false, false, EPI_ACC, P256x128, true>), dim3(total_tiles, 1),
-                       dim3(P256x128::NT), 0, st, a, K);
+  if (wide) {
+    if (overwrite) launch_grouped<P256x256, EPI_STORE>(a, total_tiles, K, st);
+    else launch_grouped<P256x256, EPI_ACC>(a, total_tiles, K, st);
+  } else {
+    if (overwrite) launch_grouped<P256x128, EPI_STORE>(a, total_tiles, K, st);
+    else launch_grouped<P256x128, EPI_ACC>(a, total_tiles, K, st);
+  }
   return hipGetLastError();
 }
 

@@ -86,17 +86,23 @@ struct GemmArgs {
 // bf16 operands: K-major vectors that straddle K read the memory just past K,
 // which must hold zeros (true when K % 8 == 0, or for zero-padded rows).
 
+// Two tile shapes: wide = 256 x 256 (eight 128 x 64 wave tiles), else 256 x 128.
 // overwrite: C_p = A_p^T B_p instead of +=; nonfinite (nullable): set to 1 (a plain
 // store) if any element written is NaN or infinite.
-int wgrad_group_tiles(int M, int N);
+int wgrad_group_tiles(int M, int N, bool wide);
 // Workgroup w of a problem runs on XCD w % 8. Each XCD streams the operand
 // panels of the tiles it runs through its own L2, so the launch gives each XCD
 // one block of the tile grid: the split of the grid into 8 equal blocks (xcd_m
 // row bands) that reads the fewest panel bytes per XCD, or 0 if the grid does
 // not split evenly (then the generic XCD-aware order applies). K contracted rows.
-int wgrad_group_xcd_m(int M, int N, int K);
+int wgrad_group_xcd_m(int M, int N, int K, bool wide);
+// How many leading problems (of n, shapes M[p] x N[p]) go on wide tiles, the rest
+// in a second launch on 256 x 128 tiles: the split with the fewest rounds of
+// workgroups over the CUs, a wide tile costing 1.8 narrow ones (measured); the
+// whole list on narrow tiles when no split does better.
+int wgrad_group_wide(const int* M, const int* N, int n);
 hipError_t gemm_wgrad_grouped(const WgradProblem* probs, int n, int total_tiles, int K, const void* zeros,
-                              bool overwrite, int* nonfinite, hipStream_t st);
+                              bool overwrite, bool wide, int* nonfinite, hipStream_t st);
 
 // dtype: element type of A, B, aux and of C/C2 unless out_f32 (then C is float).
 // splits > 1 is only valid with EPI_ATOMIC.

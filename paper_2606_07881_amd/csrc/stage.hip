@@ -332,7 +332,8 @@ struct Layout {
   // gradients to G in one grouped launch at its end
   bool wdefer = false;
   size_t wgroup = 0;           // problem tables of that launch, one per activation slot (or work slot)
-  int wgroup_n = 0, wgroup_tiles = 0;
+  int wgroup_n = 0, wgroup_tiles = 0;   // problems per table; workgroups of the 256 x 128 launch
+  int wgroup_n1 = 0, wgroup_tiles1 = 0; // leading problems on 256 x 256 tiles (their own launch); its workgroups
   // checkpointed stages: each slot holds the stage input only (c_* offsets,
   // c_bytes per slot); one work slot of the full layout takes the activations
   bool recompute = false;
@@ -484,10 +485,21 @@ Layout make_layout(const paci_shapes& s, int K, int delay, const ParamTable& p) 
     L.wgroup_n = 4 * s.n_layers;
     const int tables = L.recompute ? 1 : L.n_slots;
     L.wgroup = a.take(sizeof(paci::WgradProblem) * (size_t)L.wgroup_n * tables);
+    // shapes in table order (wgrad_tables): per block W_2, W_1, W_o, W_qkv
     const int shapes[4][2] = {{(int)d, (int)f}, {(int)f, (int)d}, {(int)d, (int)d}, {3 * (int)d, (int)d}};
-    int tiles = 0;
+    std::vector<int> Ms, Ns;
     for (int l = 0; l < s.n_layers; ++l)
-      for (int q = 0; q < 4; ++q) tiles += (paci::wgrad_group_tiles(shapes[q][0], shapes[q][1]) + 7) / 8 * 8;
+      for (int q = 0; q < 4; ++q) {
+        Ms.push_back(shapes[q][0]);
+        Ns.push_back(shapes[q][1]);
+      }
+    L.wgroup_n1 = paci::wgrad_group_wide(Ms.data(), Ns.data(), L.wgroup_n);
+    int tiles1 = 0, tiles = 0;
+    for (int p = 0; p < L.wgroup_n; ++p) {
+      const bool wide = p < L.wgroup_n1;
+      (wide ? tiles1 : tiles) += (paci::wgrad_group_tiles(Ms[p], Ns[p], wide) + 7) / 8 * 8;
+    }
+    L.wgroup_tiles1 = tiles1;
     L.wgroup_tiles = tiles;
   }
 
@@ -923,9 +935,18 @@ int wgrad_grouped(paci_stage* h, int t, bool overwrite, int* flag) {
   const double T = (double)L.T, d = h->s.d_model, f = h->s.d_ff;
   const double work = 2.0 * T * h->s.n_layers * (d * f + f * d + d * d + 3 * d * d);
   const auto* tab = reinterpret_cast<const paci::WgradProblem*>(h->arena + L.wgroup) + (size_t)t * L.wgroup_n;
+  const int n1 = L.wgroup_n1;
   return run(h, F_GEMM_WGRAD, work, [&] {
-    return paci::gemm_wgrad_grouped(tab, L.wgroup_n, L.wgroup_tiles, (int)L.T, h->arena + L.zeros, overwrite, flag,
-                                    h->st);
+    // the leading problems on 256 x 256 tiles, the rest on 256 x 128 (each launch
+    // fills whole rounds of the CUs where the shapes allow)
+    hipError_t e = hipSuccess;
+    if (n1 > 0)
+      e = paci::gemm_wgrad_grouped(tab, n1, L.wgroup_tiles1, (int)L.T, h->arena + L.zeros, overwrite, true, flag,
+                                   h->st);
+    if (e == hipSuccess && n1 < L.wgroup_n)
+      e = paci::gemm_wgrad_grouped(tab + n1, L.wgroup_n - n1, L.wgroup_tiles, (int)L.T, h->arena + L.zeros,
+                                   overwrite, false, flag, h->st);
+    return e;
   });
 }
 
@@ -947,7 +968,7 @@ std::vector<paci::WgradProblem> wgrad_tables(const paci_stage* h) {
   std::vector<paci::WgradProblem> v;
   for (int t = 0; t < tables; ++t) {
     const char* A = L.recompute ? h->arena + L.work : h->arena + L.stash + (size_t)t * L.slot_bytes;
-    int tile0 = 0;
+    int tile0 = 0, p = 0;   // tile0 restarts at the first problem of the 256 x 128 launch
     for (int l = h->s.n_layers - 1; l >= 0; --l) {   // the order the backward produced them
       const BlockRefs& b = h->p.blocks[l];
       const BlockSlot& o = L.blk[l];
@@ -955,6 +976,8 @@ std::vector<paci::WgradProblem> wgrad_tables(const paci_stage* h) {
       const struct { size_t dy, x; int M, N; int64_t g; } q[4] = {
           {w.dy, o.a, d, f, b.w_2}, {w.du, o.n2, f, d, b.w_1}, {w.dx1, o.o, d, d, b.w_o}, {w.dqkv, o.n1, 3 * d, d, b.w_qkv}};
       for (const auto& e : q) {
+        const bool wide = p < L.wgroup_n1;
+        if (p++ == L.wgroup_n1) tile0 = 0;
         paci::WgradProblem pr;
         pr.A = h->arena + e.dy;
         pr.B = A + e.x;
@@ -962,9 +985,9 @@ std::vector<paci::WgradProblem> wgrad_tables(const paci_stage* h) {
         pr.M = e.M;
         pr.N = e.N;
         pr.tile0 = tile0;
-        pr.xcd_m = paci::wgrad_group_xcd_m(e.M, e.N, (int)L.T);
+        pr.xcd_m = paci::wgrad_group_xcd_m(e.M, e.N, (int)L.T, wide);
         v.push_back(pr);
-        tile0 += (paci::wgrad_group_tiles(e.M, e.N) + 7) / 8 * 8;
+        tile0 += (paci::wgrad_group_tiles(e.M, e.N, wide) + 7) / 8 * 8;
       }
     }
   }

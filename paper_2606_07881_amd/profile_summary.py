@@ -44,6 +44,10 @@ FAMILIES = {
 # families whose launch runs each of its kernels once; every other family runs
 # one of its kernels (an epilogue or shape variant) per launch
 SEQUENCES = {"attn_bwd", "layernorm_bwd"}
+# families whose launch can run a second kernel of another tile shape (the
+# grouped weight gradients: a 256 x 256 part, then the 256 x 128 rest): a launch
+# is counted once, by its 256 x 128 kernel when the run has one
+SPLIT_LAUNCH = {"gemm_wgrad_acc": "PipeTile<256, 128"}
 
 
 def sources_sha256():
@@ -96,6 +100,7 @@ def traffic(fetch_csv, write_csv, copy_bytes=COPY_BYTES):
     w_scale = copy_bytes / (1024.0 * sum(w[copy[0]]) / len(w[copy[0]]))
     fams = collections.defaultdict(float)
     launches = collections.defaultdict(int)
+    split = {fam for fam, tag in SPLIT_LAUNCH.items() if any(tag in k and family_of(k) == fam for k in f)}
     lines = [f"Scale factors from {COPY_KERNEL} ({copy_bytes / 2 ** 20:.0f} MiB read and written per dispatch): "
              f"FETCH_SIZE x {f_scale:.3f}, WRITE_SIZE x {w_scale:.3f}.", "",
              "| kernel | family | dispatches | FETCH_SIZE KiB/dispatch | WRITE_SIZE KiB/dispatch | HBM MiB/dispatch (scaled) |",
@@ -107,7 +112,10 @@ def traffic(fetch_csv, write_csv, copy_bytes=COPY_BYTES):
         fam = family_of(k)
         if fam:
             fams[fam] += b * len(f[k])
-            if fam not in SEQUENCES or FAMILIES[fam][0] in k:
+            if fam in split:
+                if SPLIT_LAUNCH[fam] in k:
+                    launches[fam] += len(f[k])
+            elif fam not in SEQUENCES or FAMILIES[fam][0] in k:
                 launches[fam] += len(f[k])
         lines.append(f"| `{k.replace('|', '/')[:110]}` | {fam or '-'} | {len(f[k])} | {fk:.1f} | {wk:.1f} | {b / 2 ** 20:.1f} |")
     record = {"sources_sha256": sources_sha256(), "fetch_scale": f_scale, "write_scale": w_scale,
