@@ -630,8 +630,13 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, float* cl, in
   float csum[U];
 #pragma unroll
   for (int j = 0; j < U; ++j) csum[j] = 0.f;
+  // bf16 aux rows of a multi-panel epilogue: each panel's are loaded before its
+  // staging, so their latency overlaps the staging and its barriers
+  constexpr bool PANEL_AUX = (EPI == EPI_BIAS_RES || EPI == EPI_GELU_GRAD) && sizeof(TO) == 2 && !PRE;
 #pragma unroll
   for (int p = 0; p < BM / PR; ++p) {
+    u32x4 pre_p[PANEL_AUX ? EpiGeom<TO, BN, PR, NT>::P : 1];
+    if constexpr (PANEL_AUX) prefetch_aux<TO, BN, PR, NT>(a, m0 + p * PR, n0, tid, pre_p);
     __syncthreads();   // every wave is done with the ring (or with the previous panel)
     if (wm0 >= p * PR && wm0 < (p + 1) * PR) {
 #pragma unroll
@@ -653,7 +658,8 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, float* cl, in
         if (m < a.M && n < a.N) atomicAdd(C + (int64_t)m * a.ldc + n, cl[r * LDC + c]);
       }
     } else {
-      staged_out<TO, EPI, BN, PR, NT, PRE>(a, cl, mb, n0, tid, csum, pre, pb);
+      if constexpr (PANEL_AUX) staged_out<TO, EPI, BN, PR, NT, true>(a, cl, mb, n0, tid, csum, pre_p, pb);
+      else staged_out<TO, EPI, BN, PR, NT, PRE>(a, cl, mb, n0, tid, csum, pre, pb);
     }
   }
   if constexpr (EPI != EPI_ATOMIC && EPI != EPI_CE_STATS && UPR <= 64 && 64 % UPR == 0) {
