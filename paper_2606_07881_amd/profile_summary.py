@@ -74,7 +74,7 @@ def kernels_md(stats_csv, top=24):
     out = ["| kernel | family | calls | total ms | avg us | min us | max us | % |", "|---|---|---|---|---|---|---|---|"]
     for r in rows[:top]:
         name = r["Name"].replace("|", "/")
-        out.append(f"| `{name[:110]}` | {family_of(name) or '-'} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.1f} | "
+        out.append(f"| `{name[:130]}` | {family_of(name) or '-'} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.1f} | "
                    f"{float(r['AverageNs']) / 1e3:.1f} | {float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
                    f"{float(r['Percentage']):.2f} |")
     return "\n".join(out)
@@ -117,7 +117,7 @@ def traffic(fetch_csv, write_csv, copy_bytes=COPY_BYTES):
                     launches[fam] += len(f[k])
             elif fam not in SEQUENCES or FAMILIES[fam][0] in k:
                 launches[fam] += len(f[k])
-        lines.append(f"| `{k.replace('|', '/')[:110]}` | {fam or '-'} | {len(f[k])} | {fk:.1f} | {wk:.1f} | {b / 2 ** 20:.1f} |")
+        lines.append(f"| `{k.replace('|', '/')[:130]}` | {fam or '-'} | {len(f[k])} | {fk:.1f} | {wk:.1f} | {b / 2 ** 20:.1f} |")
     record = {"sources_sha256": sources_sha256(), "fetch_scale": f_scale, "write_scale": w_scale,
               "bytes_per_launch": {k: round(v / max(launches[k], 1)) for k, v in sorted(fams.items())}}
     return "\n".join(lines), record
@@ -155,7 +155,7 @@ def mfma(counters_csv):
             fam_busy[fam] += busy
             fam_active[fam] += active
             fam_flop[fam] += mops * 512
-        lines.append(f"| `{k.replace('|', '/')[:100]}` | {fam or '-'} | {n} | {100 * busy / (active * SIMD_NUM):.1f} | "
+        lines.append(f"| `{k.replace('|', '/')[:130]}` | {fam or '-'} | {n} | {100 * busy / (active * SIMD_NUM):.1f} | "
                      f"{mops * 512 / n / 1e9:.1f} | {active / n / 1e3:.0f} |")
     lines += ["", "| family | MFMA busy % | executed bf16 MFMA FLOP per GPU-active cycle, fraction of the dense peak |",
               "|---|---|---|"]
