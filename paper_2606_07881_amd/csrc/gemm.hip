@@ -1053,15 +1053,15 @@ hipError_t launch(const GemmArgs& a, int splits, hipStream_t st) {
         case 10: return launch_pipe<TO, AK, BK, EPI, P256x128>(a, splits, st);
         case 13: return launch_pipe<TO, AK, BK, EPI, P128x128o2>(a, splits, st);
         default:
-          // weight gradients (both operands MN-major) and the input gradient
-          // that reads u and writes du: 128 x 128 tiles, two workgroups per
-          // CU, so one's epilogue overlaps the other's loop (3-6% faster for
-          // the latter, slower for the other forward and input-gradient
-          // products); the rest: 256 x 128 tiles, which re-read the weights
-          // half as often
-          // The FFN up-projection and the input gradient through gelu'(u),
-          // when 256 x 256 tiles fill whole rounds of the CUs: those
-          // (measured 13% and 2% faster per call at 8192 x 4096)
+          // The FFN up-projection and the input gradient through gelu'(u):
+          // 256 x 256 tiles when they fill whole rounds of the CUs (measured
+          // 13% and 2% faster per call at 8192 x 4096, 11% for the latter
+          // with its per-panel aux loads). Otherwise weight gradients (both
+          // operands MN-major) and the input gradient through gelu'(u): 128 x
+          // 128 tiles, two workgroups per CU, so one's epilogue overlaps the
+          // other's loop (3-6% faster for the latter, slower for the other
+          // forward and input-gradient products); the rest: 256 x 128 tiles,
+          // which re-read the weights half as often.
           if constexpr (AK && BK && (EPI == EPI_BIAS_GELU || EPI == EPI_GELU_GRAD)) {
             const int t256 = ((a.M + 255) / 256) * ((a.N + 255) / 256);
             if (splits == 1 && t256 % cu_count() == 0) return launch_pipe<TO, AK, BK, EPI, P256x256>(a, splits, st);
